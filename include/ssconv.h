@@ -1,0 +1,204 @@
+/*
+ * ssconv.h -- C ABI of the MI355X (gfx950) Sparse Steerable Convolution library.
+ *
+ * Sparse Steerable Convolution (SS-Conv, Lin et al., NeurIPS 2021,
+ * arXiv 2111.07383) convolves a sparse tensor (H_n, F_n) -- a hash table of
+ * active voxel sites and a feature matrix whose rows follow it -- with a
+ * rotation-steerable kernel kappa to give (H_{n+1}, F_{n+1}) (Sec. 3.2).
+ * The library implements the three steps of Sec. 3.2:
+ *   1. rule book construction (Sec. 3.2.2 site state, Sec. 3.2.3 Alg. 1
+ *      lines 1-7) over a GPU coordinate hash table;
+ *   2. kernel synthesis as a linear combination of steerable basis kernels
+ *      (Sec. 3.2.1, Eq. 7-9);
+ *   3. the feature update of Alg. 1 (lines 8-12) as an output-stationary
+ *      gather -> matrix-core GEMM -> single write per output row;
+ * plus the exact adjoint (feature and coefficient gradients) and the gated
+ * nonlinearity of Sec. 3.3 (Eq. 12).
+ *
+ * Conventions shared by every call
+ *  - Pointers are DEVICE pointers unless marked (host).  The caller owns every
+ *    buffer it passes and every stream; the library owns only the internal
+ *    buffers of a rule book handle.
+ *  - Every call returns 0 (SSCONV_OK) or a negative SSCONV_E_* code and never
+ *    throws; ssconv_last_error() gives a message (thread-local).  On error no
+ *    handle is returned (the out-handle is set to NULL).
+ *  - Work is enqueued on the given stream and is asynchronous, except
+ *    ssconv_build_rulebook, which synchronises the stream to size its
+ *    outputs and to report device-detected errors.
+ *  - Sites are int32 (b, x, y, z) with 0 <= x < grid[0], 0 <= y < grid[1],
+ *    0 <= z < grid[2], b >= 0 and (max b + 1) * grid[0]*grid[1]*grid[2] < 2^32.
+ *  - Kernel offsets s = (dx, dy, dz) in S = {-h..h}^3, h = (ksize-1)/2, are
+ *    indexed s_idx = ((dx+h)*ksize + (dy+h))*ksize + (dz+h)   (Sec. 3.2, Eq. 6).
+ *  - Channel layout (Sec. 3.1, Eq. 5): a feature row stacks irreducible fields
+ *    in the order of an ssconv_fields list; the fields of one entry are
+ *    consecutive and each field's 2l+1 components are contiguous, ordered
+ *    m = -l..l in the real spherical-harmonic basis (no Condon-Shortley phase;
+ *    Y_1 is proportional to (y, z, x)).
+ *  - Feature matrices are row-major [rows, channels]; row r of F_n belongs to
+ *    site r of H_n (Sec. 3.2).
+ *  - The kernel tensor W is kappa(s) of Eq. 9 for every offset, stored
+ *    row-major [ksize^3][Cout][Cin]: out_row(x) = sum_s kappa(s) in_row(y).
+ */
+#ifndef SSCONV_H
+#define SSCONV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- status codes ------------------------------------------------------- */
+#define SSCONV_OK 0
+#define SSCONV_E_INVALID (-1)   /* bad argument (null pointer, bad size/flag/alignment) */
+#define SSCONV_E_BOUNDS (-2)    /* a site lies outside the grid or the 32-bit key space */
+#define SSCONV_E_DUPLICATE (-3) /* the same site appears twice in the input */
+#define SSCONV_E_HASH_FULL (-4) /* hash table capacity exhausted (only with a forced capacity) */
+#define SSCONV_E_NOMEM (-5)     /* device allocation failed */
+#define SSCONV_E_HIP (-6)       /* a HIP runtime call failed */
+#define SSCONV_E_DTYPE (-7)     /* unsupported dtype */
+
+typedef enum { SSCONV_F32 = 0, SSCONV_BF16 = 1 } ssconv_dtype;
+
+#define SSCONV_MAX_ENTRIES 8
+#define SSCONV_MAX_L 4
+#define SSCONV_MAX_SHELLS 8
+
+/* A feature type: entries (l[e], mult[e]) in channel order (Sec. 3.1, Eq. 5).
+ * Channels = sum_e mult[e] * (2 l[e] + 1).  0 <= l[e] <= SSCONV_MAX_L. */
+typedef struct {
+  int n;
+  int l[SSCONV_MAX_ENTRIES];
+  int mult[SSCONV_MAX_ENTRIES];
+} ssconv_fields;
+
+/* Basis of one layer (Sec. 3.2.1, Eq. 8): for every out field (order k) and in
+ * field (order l), elements kappa^{kl,Jm} for J = |k-l| .. min(k+l, jmax) and
+ * every radial shell m, with phi^m(r) = exp(-(r - shells[m])^2 / (2 eps^2)).
+ * jmax < 0 means no band limit.  Each element is normalised to unit Frobenius
+ * norm over (offset, row, column) with its first entry of magnitude above
+ * 1e-3 of its maximum made positive; elements that vanish on the grid
+ * (J > 0 on a 1x1x1 kernel) are left out. */
+typedef struct {
+  ssconv_fields in, out;
+  int ksize;
+  int n_shells;
+  double shells[SSCONV_MAX_SHELLS];
+  double eps;
+  int jmax;
+} ssconv_basis_desc;
+
+typedef struct ssconv_rulebook* ssconv_rulebook_t;
+
+const char* ssconv_last_error(void);
+const char* ssconv_version(void);
+
+/* ---- steerable basis (host) ---------------------------------------------
+ * Sec. 3.2.1, Eq. 7-8.  Computed on the host in fp64 from Clebsch-Gordan
+ * coefficients (Racah's formula) carried to the real harmonic basis.
+ *
+ * ssconv_basis_info: number of floats of the basis buffer and number of
+ * learned coefficients (sum over field pairs of the block's element count;
+ * without vanishing elements M (2 min(k,l)+1) per block when J is uncapped).
+ *
+ * ssconv_basis_build: fills (host) basis[basis_floats] as fp32.  Layout: for
+ * every distinct out order k (ascending) and distinct in order l (ascending):
+ * [nq(k,l)][ksize^3][2k+1][2l+1], elements ordered (J ascending, shell).
+ *
+ * Coefficient layout (ssconv_synth_kernel / ssconv_backward): for every out
+ * field i, every in field j (channel order), the nq(k_i, l_j) weights
+ * w^{k l, J m} in element order. */
+int ssconv_basis_info(const ssconv_basis_desc* desc /*host*/, int64_t* basis_floats /*host*/,
+                      int64_t* n_coeff /*host*/);
+int ssconv_basis_build(const ssconv_basis_desc* desc /*host*/, float* basis /*host*/);
+
+/* ---- rule book (Sec. 3.2.2, Eq. 10; Sec. 3.2.3, Alg. 1 lines 1-7) --------
+ * coords: [n, 4] int32 (b, x, y, z), n >= 0, no duplicates.
+ * grid (host): input grid extent per axis.  ksize: odd, 1..5.
+ * stride: 1 or 2.  submanifold = 1 keeps H_{n+1} = H_n (stride must be 1, rows
+ * unchanged); otherwise H_{n+1} = { x : exists y in H_n, stride*x - y in S }
+ * clipped to the output grid ceil(grid/stride), rows in lexicographic
+ * (b, x, y, z) order.  Pairs satisfy stride*x - y = s and never cross b.
+ * The call synchronises `stream` and returns a handle that owns all device
+ * buffers (coordinate hash tables, neighbour map, per-offset pair lists);
+ * they are freed by ssconv_rulebook_destroy, stream-ordered on `stream`,
+ * which must still be valid then.  Errors: E_INVALID, E_BOUNDS,
+ * E_DUPLICATE, E_HASH_FULL, E_NOMEM, E_HIP. */
+int ssconv_build_rulebook(const int32_t* coords, int64_t n, const int32_t* grid /*host [3]*/,
+                          int ksize, int stride, int submanifold, hipStream_t stream,
+                          ssconv_rulebook_t* out /*host*/);
+
+/* n_in, n_out (host) and, if non-NULL, pair_counts (host [ksize^3]) = |R_s|. */
+int ssconv_rulebook_info(ssconv_rulebook_t rb, int64_t* n_in, int64_t* n_out,
+                         int64_t* pair_counts);
+/* Copies H_{n+1} as [n_out, 4] int32 into dst. */
+int ssconv_rulebook_out_coords(ssconv_rulebook_t rb, int32_t* dst, hipStream_t stream);
+/* Copies all R_s concatenated in s_idx order as [P, 2] int32 (out row, in row)
+ * into dst, P = sum of pair_counts; within R_s pairs follow the output rows. */
+int ssconv_rulebook_pairs(ssconv_rulebook_t rb, int32_t* dst, hipStream_t stream);
+/* Copies the neighbour map nbr[s_idx][out row] (in row or -1) as [ksize^3, n_out] int32. */
+int ssconv_rulebook_neighbours(ssconv_rulebook_t rb, int32_t* dst, hipStream_t stream);
+/* Copies a coordinate hash table (which = 0: H_n, 1: H_{n+1}) as its raw uint64
+ * slots (key << 32 | row, key = ((b*G0 + x)*G1 + y)*G2 + z, empty = ~0) into dst
+ * [capacity]; *capacity (host) is set when dst is NULL. */
+int ssconv_rulebook_hash(ssconv_rulebook_t rb, int which, uint64_t* dst, int64_t* capacity /*host*/,
+                         hipStream_t stream);
+void ssconv_rulebook_destroy(ssconv_rulebook_t rb);
+
+/* ---- kernel synthesis (Sec. 3.2.1, Eq. 7 and Eq. 9) -----------------------
+ * W[s][o][i] = sum over the basis elements q of the block holding out channel
+ * o and in channel i of coeffs[q] * basis_q[s][a][b].  basis and coeffs are
+ * fp32 device buffers in the layouts of ssconv_basis_build; W is written in
+ * w_dtype (fp32, or bf16 rounded to nearest even from the fp32 sum). */
+int ssconv_synth_kernel(const ssconv_basis_desc* desc /*host*/, const float* basis,
+                        const float* coeffs, ssconv_dtype w_dtype, void* W, hipStream_t stream);
+
+/* ---- forward (Sec. 3.2.3, Alg. 1 lines 8-12) -------------------------------
+ * out[x] = sum_s sum_{(x,y) in R_s} kappa(s) feats[y], every output row written
+ * exactly once (rows with no pair become 0).  feats [n_in, cin], W
+ * [ksize^3, cout, cin], out [n_out, cout], all in `dtype` (bf16 inputs are
+ * multiplied exactly and accumulated in fp32).  Buffers must be 16-byte
+ * aligned.  feats and out must not overlap. */
+int ssconv_forward(const void* feats, ssconv_dtype dtype, int cin, ssconv_rulebook_t rb,
+                   const void* W, int cout, void* out, hipStream_t stream);
+
+/* ---- backward (adjoint of the forward and of the synthesis) ---------------
+ * For L = <out, grad_out>:
+ *   grad_feats[y] = sum_s sum_{(x,y) in R_s} kappa(s)^T grad_out[x]       (dtype)
+ *   dW[s]        = sum_{(x,y) in R_s} grad_out[x] feats[y]^T             (fp32, in workspace)
+ *   grad_coeffs[q] = sum_s <dW[s] block, basis_q[s]>                     (fp32)
+ * grad_feats or grad_coeffs may be NULL to skip them (desc and basis may then
+ * be NULL as well when grad_coeffs is NULL).  workspace: device scratch of at
+ * least ssconv_backward_workspace_size bytes, 256-byte aligned; the result
+ * is deterministic (no atomics in the reductions). */
+size_t ssconv_backward_workspace_size(ssconv_rulebook_t rb, ssconv_dtype dtype, int cin, int cout);
+int ssconv_backward(const void* feats, const void* grad_out, ssconv_dtype dtype, int cin, int cout,
+                    ssconv_rulebook_t rb, const void* W, const ssconv_basis_desc* desc /*host*/,
+                    const float* basis, void* grad_feats, float* grad_coeffs, void* workspace,
+                    size_t ws_bytes, hipStream_t stream);
+
+/* ---- gated nonlinearity (Sec. 3.3, Eq. 12) ---------------------------------
+ * x: [n, C + G] where C = channels of `fields` and G = number of l > 0 fields
+ * (the gate channels, appended after the fields in field order).
+ * y: [n, C]: ReLU on l = 0 fields, sigmoid(gate) * f on l > 0 fields.
+ * Backward: dx [n, C + G] from x and dy [n, C] (ReLU'(0) = 0). */
+int ssconv_gate_forward(const ssconv_fields* fields /*host*/, const void* x, ssconv_dtype dtype,
+                        int64_t n, void* y, hipStream_t stream);
+int ssconv_gate_backward(const ssconv_fields* fields /*host*/, const void* x, const void* dy,
+                         ssconv_dtype dtype, int64_t n, void* dx, hipStream_t stream);
+
+/* ---- test hooks --------------------------------------------------------
+ * Forces failure paths from the host so they can be tested without faulting
+ * a device: option 1 = hash capacity (slots) used by the next rule book builds
+ * (0 restores automatic sizing); option 2 = make the N-th following device
+ * allocation fail (0 disables).  Returns E_INVALID for unknown options. */
+int ssconv_debug_set(int option, int64_t value);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SSCONV_H */

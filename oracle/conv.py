@@ -57,13 +57,20 @@ def synth_adjoint(layer, basis, dkappa: np.ndarray) -> np.ndarray:
     return dw
 
 
+def _unique(idx: np.ndarray) -> np.ndarray:
+    # Within one R_s an output row pairs with at most one input row (y = stride*x - s)
+    # and vice versa, so a buffered fancy-index update adds every pair exactly once.
+    assert len(np.unique(idx)) == len(idx), "rule book offset lists must not repeat a row"
+    return idx
+
+
 def forward(feats_in: np.ndarray, R: List[np.ndarray], kappa: np.ndarray, n_out: int) -> np.ndarray:
     """F_out[o] += kappa(s) F_in[i] for every (o, i) in every R_s; F_out starts at zero."""
     f = np.asarray(feats_in, np.float64)
     out = np.zeros((n_out, kappa.shape[1]))
     for si, r in enumerate(R):
         if len(r):
-            np.add.at(out, r[:, 0], f[r[:, 1]] @ kappa[si].T)
+            out[_unique(r[:, 0])] += f[r[:, 1]] @ kappa[si].T
     return out
 
 
@@ -89,17 +96,30 @@ def forward_rows(feats_in, nbr: np.ndarray, kappa, rows: np.ndarray) -> np.ndarr
     return out
 
 
-def backward(feats_in, grad_out, R, kappa, n_in):
-    """(dF_in [n_in, Cin], dkappa [|S|, Cout, Cin]) for L = <F_out, grad_out>."""
-    f = np.asarray(feats_in, np.float64)
+def grad_feats(grad_out, R, kappa, n_in):
+    """dF_in[i] = sum_s sum_{(o, i) in R_s} kappa(s)^T grad_out[o] (adjoint of ``forward``)."""
     g = np.asarray(grad_out, np.float64)
     d_in = np.zeros((n_in, kappa.shape[2]))
-    dk = np.zeros_like(kappa, dtype=np.float64)
     for si, r in enumerate(R):
         if len(r):
-            np.add.at(d_in, r[:, 1], g[r[:, 0]] @ kappa[si])
+            d_in[_unique(r[:, 1])] += g[r[:, 0]] @ kappa[si]
+    return d_in
+
+
+def grad_kappa(feats_in, grad_out, R, kappa_shape):
+    """dkappa(s) = sum_{(o, i) in R_s} grad_out[o] F_in[i]^T."""
+    f = np.asarray(feats_in, np.float64)
+    g = np.asarray(grad_out, np.float64)
+    dk = np.zeros(kappa_shape)
+    for si, r in enumerate(R):
+        if len(r):
             dk[si] = g[r[:, 0]].T @ f[r[:, 1]]
-    return d_in, dk
+    return dk
+
+
+def backward(feats_in, grad_out, R, kappa, n_in):
+    """(dF_in [n_in, Cin], dkappa [|S|, Cout, Cin]) for L = <F_out, grad_out>."""
+    return grad_feats(grad_out, R, kappa, n_in), grad_kappa(feats_in, grad_out, R, kappa.shape)
 
 
 def dense_conv(coords_in, feats_in, kappa, grid: int, stride: int, batch: int) -> np.ndarray:

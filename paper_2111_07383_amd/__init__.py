@@ -1,0 +1,23 @@
+"""MI355X (gfx950) Sparse Steerable Convolution hot path (arXiv 2111.07383).
+
+The computation lives in ``libssconv.so`` (HIP kernels behind the C ABI of
+include/ssconv.h); ``binding`` only marshals torch tensors and streams into it.
+"""
+from ._abi import LIB_PATH, SSConvError, lib  # noqa: F401
+from .binding import (  # noqa: F401
+    Rulebook,
+    backward,
+    backward_workspace_size,
+    basis_build,
+    basis_desc,
+    basis_info,
+    build_rulebook,
+    debug_set,
+    forward,
+    gate_backward,
+    gate_forward,
+    layer_desc,
+    make_fields,
+    n_channels,
+    synth_kernel,
+)

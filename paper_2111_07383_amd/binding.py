@@ -1,0 +1,249 @@
+"""Thin PyTorch binding of the C ABI: device memory and streams come from torch,
+every step of the computation runs in the HIP library.
+
+Names follow the C entry points (``ssconv_build_rulebook`` -> ``build_rulebook``
+etc.).  Tensors must live on the current HIP device; bf16 tensors map to
+SSCONV_BF16 and fp32 tensors to SSCONV_F32.
+"""
+import ctypes
+from ctypes import byref, c_int, c_int64, c_void_p
+from typing import Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+from ._abi import BF16, F32, BasisDesc, Fields, check, lib
+
+FieldList = Sequence[Tuple[int, int]]
+
+
+def _stream(stream=None) -> c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return c_void_p(s.cuda_stream)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> c_void_p:
+    return c_void_p(0 if t is None else t.data_ptr())
+
+
+def _dtype(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}")
+
+
+def _need(t: torch.Tensor, name: str, dtype=None, shape=None):
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def make_fields(fields: FieldList) -> Fields:
+    f = Fields()
+    f.n = len(fields)
+    for e, (l, m) in enumerate(fields):
+        f.l[e] = int(l)
+        f.mult[e] = int(m)
+    return f
+
+
+def n_channels(fields: FieldList) -> int:
+    return sum(m * (2 * l + 1) for l, m in fields)
+
+
+def basis_desc(fields_in: FieldList, fields_out: FieldList, ksize: int, shells: Sequence[float],
+               eps: float = 0.6, jmax: Optional[int] = None) -> BasisDesc:
+    d = BasisDesc()
+    d.in_ = make_fields(fields_in)
+    d.out = make_fields(fields_out)
+    d.ksize = int(ksize)
+    d.n_shells = len(shells)
+    for i, m in enumerate(shells):
+        d.shells[i] = float(m)
+    d.eps = float(eps)
+    d.jmax = -1 if jmax is None else int(jmax)
+    return d
+
+
+def layer_desc(layer) -> BasisDesc:
+    """Descriptor of a layer spec with fields_in/out, ksize, shells, eps, jmax attributes."""
+    return basis_desc(layer.fields_in, layer.fields_out, layer.ksize, layer.shells, layer.eps, layer.jmax)
+
+
+def basis_info(desc: BasisDesc) -> Tuple[int, int]:
+    floats, ncoef = c_int64(), c_int64()
+    check(lib().ssconv_basis_info(byref(desc), byref(floats), byref(ncoef)), "ssconv_basis_info")
+    return floats.value, ncoef.value
+
+
+def basis_build(desc: BasisDesc) -> np.ndarray:
+    """Host-built basis (fp32 numpy, layout of ssconv_basis_build)."""
+    n, _ = basis_info(desc)
+    out = np.zeros(max(n, 1), np.float32)
+    check(lib().ssconv_basis_build(byref(desc), out.ctypes.data_as(c_void_p)), "ssconv_basis_build")
+    return out[:n]
+
+
+class Rulebook:
+    """Owner of an ssconv_rulebook_t (hash tables, neighbour map, pair lists)."""
+
+    def __init__(self, coords: torch.Tensor, grid, ksize: int, stride: int = 1, submanifold: bool = True,
+                 stream=None):
+        _need(coords, "coords", torch.int32)
+        if coords.dim() != 2 or coords.shape[1] != 4:
+            raise ValueError("coords must be [n, 4] (b, x, y, z)")
+        g = (c_int * 3)(*([int(grid)] * 3 if np.isscalar(grid) else [int(v) for v in grid]))
+        h = c_void_p()
+        self._h = None
+        self.device = coords.device
+        check(lib().ssconv_build_rulebook(_ptr(coords), coords.shape[0], g, int(ksize), int(stride),
+                                          int(bool(submanifold)), _stream(stream), byref(h)),
+              "ssconv_build_rulebook")
+        self._h = h
+        self.ksize, self.K, self.stride, self.submanifold = ksize, ksize ** 3, stride, bool(submanifold)
+        n_in, n_out = c_int64(), c_int64()
+        counts = (c_int64 * self.K)()
+        check(lib().ssconv_rulebook_info(h, byref(n_in), byref(n_out), counts), "ssconv_rulebook_info")
+        self.n_in, self.n_out = n_in.value, n_out.value
+        self.pair_counts = np.array(counts[:], np.int64)
+        self.n_pairs = int(self.pair_counts.sum())
+
+    @property
+    def handle(self) -> c_void_p:
+        if self._h is None:
+            raise RuntimeError("rule book has been destroyed")
+        return self._h
+
+    def out_coords(self, stream=None) -> torch.Tensor:
+        t = torch.empty((self.n_out, 4), dtype=torch.int32, device=self.device)
+        check(lib().ssconv_rulebook_out_coords(self.handle, _ptr(t), _stream(stream)), "ssconv_rulebook_out_coords")
+        return t
+
+    def pairs(self, stream=None) -> torch.Tensor:
+        t = torch.empty((self.n_pairs, 2), dtype=torch.int32, device=self.device)
+        check(lib().ssconv_rulebook_pairs(self.handle, _ptr(t), _stream(stream)), "ssconv_rulebook_pairs")
+        return t
+
+    def neighbours(self, stream=None) -> torch.Tensor:
+        t = torch.empty((self.K, self.n_out), dtype=torch.int32, device=self.device)
+        check(lib().ssconv_rulebook_neighbours(self.handle, _ptr(t), _stream(stream)), "ssconv_rulebook_neighbours")
+        return t
+
+    def hash_slots(self, which: int = 0, stream=None) -> torch.Tensor:
+        cap = c_int64()
+        check(lib().ssconv_rulebook_hash(self.handle, which, None, byref(cap), _stream(stream)), "ssconv_rulebook_hash")
+        t = torch.empty((cap.value,), dtype=torch.int64, device=self.device)
+        check(lib().ssconv_rulebook_hash(self.handle, which, _ptr(t), byref(cap), _stream(stream)),
+              "ssconv_rulebook_hash")
+        return t
+
+    def close(self):
+        if self._h is not None:
+            lib().ssconv_rulebook_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def build_rulebook(coords, grid, ksize, stride=1, submanifold=True, stream=None) -> Rulebook:
+    return Rulebook(coords, grid, ksize, stride, submanifold, stream)
+
+
+def synth_kernel(desc: BasisDesc, basis: torch.Tensor, coeffs: torch.Tensor, dtype=torch.float32,
+                 out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    _need(basis, "basis", torch.float32)
+    _need(coeffs, "coeffs", torch.float32)
+    n_floats, n_coeff = basis_info(desc)
+    if basis.numel() < n_floats or coeffs.numel() != n_coeff:
+        raise ValueError(f"basis needs {n_floats} floats and coeffs {n_coeff} values")
+    K = desc.ksize ** 3
+    cin = sum(desc.in_.mult[e] * (2 * desc.in_.l[e] + 1) for e in range(desc.in_.n))
+    cout = sum(desc.out.mult[e] * (2 * desc.out.l[e] + 1) for e in range(desc.out.n))
+    if out is None:
+        out = torch.empty((K, cout, cin), dtype=dtype, device=basis.device)
+    _need(out, "W", dtype, (K, cout, cin))
+    check(lib().ssconv_synth_kernel(byref(desc), _ptr(basis), _ptr(coeffs), _dtype(out), _ptr(out), _stream(stream)),
+          "ssconv_synth_kernel")
+    return out
+
+
+def forward(feats: torch.Tensor, rb: Rulebook, W: torch.Tensor, out: Optional[torch.Tensor] = None,
+            stream=None) -> torch.Tensor:
+    _need(feats, "feats")
+    _need(W, "W", feats.dtype)
+    K, cout, cin = W.shape
+    if feats.shape != (rb.n_in, cin):
+        raise ValueError(f"feats must be [{rb.n_in}, {cin}]")
+    if out is None:
+        out = torch.empty((rb.n_out, cout), dtype=feats.dtype, device=feats.device)
+    _need(out, "out", feats.dtype, (rb.n_out, cout))
+    check(lib().ssconv_forward(_ptr(feats), _dtype(feats), cin, rb.handle, _ptr(W), cout, _ptr(out), _stream(stream)),
+          "ssconv_forward")
+    return out
+
+
+def backward_workspace_size(rb: Rulebook, dtype: torch.dtype, cin: int, cout: int) -> int:
+    return lib().ssconv_backward_workspace_size(rb.handle, BF16 if dtype == torch.bfloat16 else F32, cin, cout)
+
+
+def backward(feats: torch.Tensor, grad_out: torch.Tensor, rb: Rulebook, W: torch.Tensor,
+             desc: Optional[BasisDesc] = None, basis: Optional[torch.Tensor] = None,
+             need_feats: bool = True, need_coeffs: bool = True, n_coeff: Optional[int] = None,
+             workspace: Optional[torch.Tensor] = None, stream=None):
+    """(grad_feats or None, grad_coeffs or None) for L = <forward(feats), grad_out>."""
+    _need(feats, "feats")
+    _need(grad_out, "grad_out", feats.dtype)
+    _need(W, "W", feats.dtype)
+    K, cout, cin = W.shape
+    gf = torch.empty_like(feats) if need_feats else None
+    gc = None
+    if need_coeffs:
+        if desc is None or basis is None:
+            raise ValueError("desc and basis are required for the coefficient gradient")
+        if n_coeff is None:
+            n_coeff = basis_info(desc)[1]
+        gc = torch.empty((n_coeff,), dtype=torch.float32, device=feats.device)
+    ws_bytes = backward_workspace_size(rb, feats.dtype, cin, cout)
+    if workspace is None or workspace.numel() < ws_bytes:
+        workspace = torch.empty((max(ws_bytes, 256),), dtype=torch.uint8, device=feats.device)
+    check(lib().ssconv_backward(_ptr(feats), _ptr(grad_out), _dtype(feats), cin, cout, rb.handle, _ptr(W),
+                                byref(desc) if desc is not None else None, _ptr(basis), _ptr(gf), _ptr(gc),
+                                _ptr(workspace), workspace.numel(), _stream(stream)),
+          "ssconv_backward")
+    return gf, gc
+
+
+def gate_forward(fields: FieldList, x: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    _need(x, "x")
+    f = make_fields(fields)
+    C = n_channels(fields)
+    if out is None:
+        out = torch.empty((x.shape[0], C), dtype=x.dtype, device=x.device)
+    check(lib().ssconv_gate_forward(byref(f), _ptr(x), _dtype(x), x.shape[0], _ptr(out), _stream(stream)),
+          "ssconv_gate_forward")
+    return out
+
+
+def gate_backward(fields: FieldList, x: torch.Tensor, dy: torch.Tensor, stream=None) -> torch.Tensor:
+    _need(x, "x")
+    _need(dy, "dy", x.dtype)
+    f = make_fields(fields)
+    dx = torch.empty_like(x)
+    check(lib().ssconv_gate_backward(byref(f), _ptr(x), _ptr(dy), _dtype(x), x.shape[0], _ptr(dx), _stream(stream)),
+          "ssconv_gate_backward")
+    return dx
+
+
+def debug_set(option: int, value: int) -> None:
+    check(lib().ssconv_debug_set(int(option), int(value)), "ssconv_debug_set")

@@ -1,0 +1,70 @@
+// C ABI entry points of the convolution: argument checks and launches.
+#include <algorithm>
+
+#include "conv.hpp"
+#include "synth.hpp"
+
+using namespace ssconv;
+
+namespace {
+
+int check_conv_args(const void* a, const void* b, ssconv_dtype dt, int cin, int cout, ssconv_rulebook_t rb,
+                    const void* W) {
+  if (dt != SSCONV_F32 && dt != SSCONV_BF16) return fail(SSCONV_E_DTYPE, "unsupported dtype %d", (int)dt);
+  if (!rb) return fail(SSCONV_E_INVALID, "NULL rule book");
+  if (cin < 1 || cout < 1) return fail(SSCONV_E_INVALID, "channel counts must be positive");
+  if (!W) return fail(SSCONV_E_INVALID, "NULL kernel tensor");
+  if (!aligned16(W) || (a && !aligned16(a)) || (b && !aligned16(b)))
+    return fail(SSCONV_E_INVALID, "device buffers must be 16-byte aligned");
+  return SSCONV_OK;
+}
+
+}  // namespace
+
+extern "C" int ssconv_forward(const void* feats, ssconv_dtype dtype, int cin, ssconv_rulebook_t rb, const void* W,
+                              int cout, void* out, hipStream_t stream) {
+  SSC_TRY(check_conv_args(feats, out, dtype, cin, cout, rb, W));
+  if ((rb->n_in > 0 && !feats) || (rb->n_out > 0 && !out)) return fail(SSCONV_E_INVALID, "NULL feature buffer");
+  if (rb->n_in == 0 && rb->n_out > 0) {
+    SSC_HIP(hipMemsetAsync(out, 0, (size_t)rb->n_out * cout * dtype_bytes(dtype), stream));
+    return SSCONV_OK;
+  }
+  return conv_forward(feats, dtype, cin, rb, W, cout, out, stream);
+}
+
+extern "C" size_t ssconv_backward_workspace_size(ssconv_rulebook_t rb, ssconv_dtype dtype, int cin, int cout) {
+  if (!rb || cin < 1 || cout < 1) return 0;
+  return bwd_layout(rb, dtype, cin, cout).total;
+}
+
+extern "C" int ssconv_backward(const void* feats, const void* grad_out, ssconv_dtype dtype, int cin, int cout,
+                               ssconv_rulebook_t rb, const void* W, const ssconv_basis_desc* desc, const float* basis,
+                               void* grad_feats, float* grad_coeffs, void* workspace, size_t ws_bytes,
+                               hipStream_t stream) {
+  SSC_TRY(check_conv_args(feats, grad_out, dtype, cin, cout, rb, W));
+  if (grad_feats && !aligned16(grad_feats)) return fail(SSCONV_E_INVALID, "grad_feats must be 16-byte aligned");
+  const BwdLayout L = bwd_layout(rb, dtype, cin, cout);
+  if (!workspace || ws_bytes < L.total || (reinterpret_cast<uintptr_t>(workspace) & 255))
+    return fail(SSCONV_E_INVALID, "workspace must be 256-byte aligned and hold %zu bytes", L.total);
+  if ((rb->n_out > 0 && !grad_out) || (rb->n_in > 0 && !feats)) return fail(SSCONV_E_INVALID, "NULL input buffer");
+  SynthArgs sa;
+  if (grad_coeffs) {
+    if (!basis) return fail(SSCONV_E_INVALID, "basis is required for the coefficient gradient");
+    SSC_TRY(make_synth_args(desc, &sa));
+    if (sa.cin != cin || sa.cout != cout || sa.K != rb->K)
+      return fail(SSCONV_E_INVALID, "basis descriptor does not match cin/cout/ksize");
+  }
+  char* ws = (char*)workspace;
+  if (grad_feats) {
+    if (rb->n_out == 0 && rb->n_in > 0)
+      SSC_HIP(hipMemsetAsync(grad_feats, 0, (size_t)rb->n_in * cin * dtype_bytes(dtype), stream));
+    else
+      SSC_TRY(conv_backward_feats(grad_out, dtype, cin, cout, rb, W, grad_feats, ws, L, stream));
+  }
+  if (grad_coeffs) {
+    float* dW = nullptr;
+    SSC_TRY(conv_backward_dw(feats, grad_out, dtype, cin, cout, rb, ws, L, &dW, stream));
+    SSC_TRY(launch_synth_adjoint(sa, basis, dW, grad_coeffs, stream));
+  }
+  return SSCONV_OK;
+}

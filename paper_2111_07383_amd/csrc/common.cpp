@@ -1,0 +1,96 @@
+// Error reporting, allocation and field tables shared by the SS-Conv entry points.
+#include "common.hpp"
+
+#include <atomic>
+
+namespace ssconv {
+
+namespace {
+thread_local std::string g_error;
+std::atomic<int64_t> g_debug_hash_cap{0};
+std::atomic<int64_t> g_debug_fail_alloc{0};
+}  // namespace
+
+void set_error(const char* fmt, ...) {
+  char buf[1024];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_error = buf;
+}
+
+int fail(int code, const char* fmt, ...) {
+  char buf[1024];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return code;
+}
+
+int dev_alloc(void** p, size_t bytes, hipStream_t stream) {
+  *p = nullptr;
+  if (bytes == 0) bytes = 256;
+  int64_t n = g_debug_fail_alloc.load();
+  if (n > 0) {
+    if (n == 1) {
+      g_debug_fail_alloc.store(0);
+      return fail(SSCONV_E_NOMEM, "device allocation of %zu bytes failed (forced by test hook)", bytes);
+    }
+    g_debug_fail_alloc.store(n - 1);
+  }
+  hipError_t e = hipMallocAsync(p, bytes, stream);
+  if (e != hipSuccess || !*p) {
+    *p = nullptr;
+    (void)hipGetLastError();
+    return fail(SSCONV_E_NOMEM, "device allocation of %zu bytes failed: %s", bytes, hipGetErrorString(e));
+  }
+  return SSCONV_OK;
+}
+
+void dev_free(void* p, hipStream_t stream) {
+  if (p) (void)hipFreeAsync(p, stream);
+}
+
+int64_t debug_hash_capacity() { return g_debug_hash_cap.load(); }
+
+int make_fieldtab(const ssconv_fields* f, FieldTab* t) {
+  if (!f || f->n < 1 || f->n > SSCONV_MAX_ENTRIES) return fail(SSCONV_E_INVALID, "bad field list");
+  t->n = f->n;
+  int ch = 0, fi = 0;
+  for (int e = 0; e < f->n; ++e) {
+    if (f->l[e] < 0 || f->l[e] > SSCONV_MAX_L || f->mult[e] < 1) return fail(SSCONV_E_INVALID, "bad field entry");
+    t->l[e] = f->l[e];
+    t->mult[e] = f->mult[e];
+    t->ch0[e] = ch;
+    t->f0[e] = fi;
+    ch += f->mult[e] * (2 * f->l[e] + 1);
+    fi += f->mult[e];
+  }
+  for (int e = f->n; e <= SSCONV_MAX_ENTRIES; ++e) {
+    t->ch0[e] = ch;
+    t->f0[e] = fi;
+    if (e < SSCONV_MAX_ENTRIES) t->l[e] = 0, t->mult[e] = 0;
+  }
+  return SSCONV_OK;
+}
+
+}  // namespace ssconv
+
+extern "C" const char* ssconv_last_error(void) { return ssconv::g_error.c_str(); }
+
+extern "C" const char* ssconv_version(void) { return "ssconv-gfx950 0.1"; }
+
+extern "C" int ssconv_debug_set(int option, int64_t value) {
+  if (option == 1) {
+    ssconv::g_debug_hash_cap.store(value < 0 ? 0 : value);
+    return SSCONV_OK;
+  }
+  if (option == 2) {
+    ssconv::g_debug_fail_alloc.store(value < 0 ? 0 : value);
+    return SSCONV_OK;
+  }
+  return ssconv::fail(SSCONV_E_INVALID, "unknown debug option %d", option);
+}

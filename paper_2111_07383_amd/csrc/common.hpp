@@ -1,0 +1,101 @@
+// Shared host/device helpers of the SS-Conv library (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <hip/hip_bf16.h>
+
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+#include <string>
+
+#include "../../include/ssconv.h"
+
+namespace ssconv {
+
+// ---------------------------------------------------------------------------
+// errors: thread-local message, negative status codes, no exceptions across the ABI
+// ---------------------------------------------------------------------------
+void set_error(const char* fmt, ...);
+int fail(int code, const char* fmt, ...);
+
+#define SSC_HIP(expr)                                                                       \
+  do {                                                                                      \
+    hipError_t e_ = (expr);                                                                 \
+    if (e_ != hipSuccess)                                                                   \
+      return ::ssconv::fail(SSCONV_E_HIP, "%s failed: %s (%s:%d)", #expr,                   \
+                            hipGetErrorString(e_), __FILE__, __LINE__);                     \
+  } while (0)
+
+#define SSC_TRY(expr)            \
+  do {                           \
+    int rc_ = (expr);            \
+    if (rc_ != SSCONV_OK) return rc_; \
+  } while (0)
+
+// stream-ordered device allocation with the test hook for forced failures
+int dev_alloc(void** p, size_t bytes, hipStream_t stream);
+void dev_free(void* p, hipStream_t stream);
+int64_t debug_hash_capacity();
+
+// ---------------------------------------------------------------------------
+// field tables (channel -> field, order, component) passed by value to kernels
+// ---------------------------------------------------------------------------
+struct FieldTab {
+  int n;                         // entries
+  int l[SSCONV_MAX_ENTRIES];     // order per entry
+  int mult[SSCONV_MAX_ENTRIES];  // fields per entry
+  int ch0[SSCONV_MAX_ENTRIES + 1];  // first channel of each entry (ch0[n] = channels)
+  int f0[SSCONV_MAX_ENTRIES + 1];   // first field index of each entry
+};
+
+int make_fieldtab(const ssconv_fields* f, FieldTab* t);
+
+// ---------------------------------------------------------------------------
+// bf16 helpers (storage as uint16, round-to-nearest-even from fp32)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);  // quiet NaN
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+
+template <typename T> struct DT;
+template <> struct DT<float> {
+  static constexpr int bytes = 4;
+  __device__ static __forceinline__ float to_f(float v) { return v; }
+  __device__ static __forceinline__ float from_f(float v) { return v; }
+};
+template <> struct DT<uint16_t> {
+  static constexpr int bytes = 2;
+  __device__ static __forceinline__ float to_f(uint16_t v) { return bf16_to_f32(v); }
+  __device__ static __forceinline__ uint16_t from_f(float v) { return f32_to_bf16_rne(v); }
+};
+
+inline size_t dtype_bytes(ssconv_dtype d) { return d == SSCONV_BF16 ? 2 : 4; }
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+inline unsigned cdiv(int64_t a, int64_t b) { return (unsigned)((a + b - 1) / b); }
+
+}  // namespace ssconv
+
+// The rule book handle (opaque to callers).
+struct ssconv_rulebook {
+  int ksize = 0, K = 0, stride = 1, submanifold = 1;
+  int grid[3] = {0, 0, 0}, grid_out[3] = {0, 0, 0};
+  int64_t n_in = 0, n_out = 0, n_pairs = 0, nbatch = 0;
+  hipStream_t stream = nullptr;
+  // device buffers (owned)
+  uint64_t* hash_in = nullptr;
+  int64_t cap_in = 0;
+  uint64_t* hash_out = nullptr;  // == hash_in for submanifold
+  int64_t cap_out = 0;
+  int32_t* out_coords = nullptr;  // [n_out, 4]
+  int32_t* nbr = nullptr;         // [K, n_out]
+  int32_t* pairs = nullptr;       // [n_pairs, 2] grouped by offset
+  int64_t* pair_off_dev = nullptr;  // [K + 1]
+  // host copies
+  int64_t* pair_off = nullptr;  // [K + 1] (host)
+};

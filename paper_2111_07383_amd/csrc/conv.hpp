@@ -1,0 +1,21 @@
+// Internal interface of the gather-GEMM kernels.
+#pragma once
+
+#include "common.hpp"
+
+namespace ssconv {
+
+struct BwdLayout {
+  size_t nbrT = 0, Wt = 0, part = 0, dW = 0, total = 0;  // byte offsets in the workspace
+  int nsplit = 1;
+};
+
+int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_rulebook* rb, const void* W, int cout,
+                 void* out, hipStream_t st);
+BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout);
+int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout, const ssconv_rulebook* rb,
+                        const void* W, void* grad_feats, char* ws, const BwdLayout& L, hipStream_t st);
+int conv_backward_dw(const void* feats, const void* grad_out, ssconv_dtype dt, int cin, int cout,
+                     const ssconv_rulebook* rb, char* ws, const BwdLayout& L, float** dW_out, hipStream_t st);
+
+}  // namespace ssconv

@@ -1,0 +1,436 @@
+// Rule book construction on the GPU (Sec. 3.2.2, Eq. 10; Sec. 3.2.3, Alg. 1 lines 1-7).
+//
+// Instead of Alg. 1's all-pairs loop, every input site is inserted into an
+// open-addressing hash table in HBM (64-bit slots key<<32 | row, lock-free
+// atomicCAS, linear probing), and every (output site, offset) pair probes it
+// once for y = stride*x - s.  Results:
+//   nbr[s][x]   neighbour map (input row or -1), offset-major so that the
+//               forward gather reads one coalesced index vector per offset;
+//   pairs       R_s for every offset, compacted with wavefront ballots and a
+//               device-wide scan (count pass, scan, write pass), so the order
+//               is deterministic: grouped by s, output rows ascending.
+// Dilated / strided output sets are marked in a bitmap over the output grid
+// and emitted in lexicographic (b, x, y, z) order by a scan of popcounts.
+#include "scan.hpp"
+
+namespace ssconv {
+
+namespace {
+
+constexpr uint64_t kEmpty = ~0ull;
+constexpr int kFlagBounds = 1, kFlagDup = 2, kFlagFull = 4;
+
+__device__ __forceinline__ uint32_t mix32(uint32_t h) {
+  h ^= h >> 16;
+  h *= 0x85ebca6bu;
+  h ^= h >> 13;
+  h *= 0xc2b2ae35u;
+  h ^= h >> 16;
+  return h;
+}
+
+__device__ __forceinline__ uint32_t site_key(int b, int x, int y, int z, int g0, int g1, int g2) {
+  return (uint32_t)((((uint64_t)b * g0 + x) * g1 + y) * g2 + z);
+}
+
+__device__ __forceinline__ int hash_find(const uint64_t* __restrict__ slots, uint64_t mask, uint32_t key) {
+  uint64_t pos = mix32(key) & mask;
+  for (uint64_t probe = 0; probe <= mask; ++probe) {
+    uint64_t v = slots[pos];
+    if (v == kEmpty) return -1;
+    if ((uint32_t)(v >> 32) == key) return (int)(uint32_t)v;
+    pos = (pos + 1) & mask;
+  }
+  return -1;
+}
+
+__global__ void validate_kernel(const int32_t* __restrict__ c, int64_t n, int g0, int g1, int g2,
+                                int* __restrict__ flags, int* __restrict__ maxb) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int bad = 0, mb = -1;
+  if (i < n) {
+    int4 v = reinterpret_cast<const int4*>(c)[i];
+    bad = (v.x < 0) | (v.y < 0) | (v.y >= g0) | (v.z < 0) | (v.z >= g1) | (v.w < 0) | (v.w >= g2);
+    mb = v.x;
+  }
+  // one atomic per wavefront
+  for (int d = 32; d >= 1; d >>= 1) {
+    bad |= __shfl_xor(bad, d, 64);
+    mb = max(mb, __shfl_xor(mb, d, 64));
+  }
+  if ((threadIdx.x & 63) == 0) {
+    if (bad) atomicOr(flags, kFlagBounds);
+    atomicMax(maxb, mb);
+  }
+}
+
+__global__ void fill_u64(uint64_t* __restrict__ p, int64_t n, uint64_t v) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = v;
+}
+
+__global__ void hash_insert_kernel(const int32_t* __restrict__ c, int64_t n, int g0, int g1, int g2,
+                                   uint64_t* __restrict__ slots, uint64_t mask, int* __restrict__ flags) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  int4 v = reinterpret_cast<const int4*>(c)[i];
+  uint32_t key = site_key(v.x, v.y, v.z, v.w, g0, g1, g2);
+  uint64_t item = ((uint64_t)key << 32) | (uint32_t)i;
+  uint64_t pos = mix32(key) & mask;
+  for (uint64_t probe = 0; probe <= mask; ++probe) {
+    unsigned long long prev =
+        atomicCAS(reinterpret_cast<unsigned long long*>(&slots[pos]), (unsigned long long)kEmpty,
+                  (unsigned long long)item);
+    if (prev == kEmpty) return;
+    if ((uint32_t)(prev >> 32) == key) {
+      atomicOr(flags, kFlagDup);
+      return;
+    }
+    pos = (pos + 1) & mask;
+  }
+  atomicOr(flags, kFlagFull);
+}
+
+// Output-set marking: for input y and offset s, stride*x = y + s must divide exactly.
+__global__ void mark_outputs(const int32_t* __restrict__ c, int64_t n, int ksize, int stride, int go0, int go1,
+                             int go2, uint32_t* __restrict__ bits) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  int s = blockIdx.y;
+  if (i >= n) return;
+  int h = (ksize - 1) / 2;
+  int dx = s / (ksize * ksize) - h, dy = (s / ksize) % ksize - h, dz = s % ksize - h;
+  int4 v = reinterpret_cast<const int4*>(c)[i];
+  int tx = v.y + dx, ty = v.z + dy, tz = v.w + dz;
+  if (tx < 0 || ty < 0 || tz < 0) return;
+  if (tx % stride || ty % stride || tz % stride) return;
+  int x = tx / stride, y = ty / stride, z = tz / stride;
+  if (x >= go0 || y >= go1 || z >= go2) return;
+  uint64_t bit = (((uint64_t)v.x * go0 + x) * go1 + y) * go2 + z;
+  atomicOr(&bits[bit >> 5], 1u << (bit & 31));
+}
+
+__global__ void popcount_words(const uint32_t* __restrict__ bits, int64_t nw, int32_t* __restrict__ cnt) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < nw) cnt[i] = __popc(bits[i]);
+}
+
+__global__ void emit_outputs(const uint32_t* __restrict__ bits, int64_t nw, const int64_t* __restrict__ offs,
+                             int go0, int go1, int go2, int32_t* __restrict__ out) {
+  int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (w >= nw) return;
+  uint32_t m = bits[w];
+  int64_t o = offs[w];
+  const int64_t per_b = (int64_t)go0 * go1 * go2;
+  while (m) {
+    int b = __ffs(m) - 1;
+    m &= m - 1;
+    int64_t bit = w * 32 + b;
+    int bb = (int)(bit / per_b);
+    int64_t r = bit - (int64_t)bb * per_b;
+    int z = (int)(r % go2);
+    int y = (int)((r / go2) % go1);
+    int x = (int)(r / ((int64_t)go1 * go2));
+    reinterpret_cast<int4*>(out)[o++] = make_int4(bb, x, y, z);
+  }
+}
+
+// Pass 1 (count=true) writes nbr and per-(offset, block) counts; pass 2 writes the pairs.
+template <bool kCount>
+__global__ __launch_bounds__(256) void probe_kernel(const int32_t* __restrict__ out_c, int64_t n_out, int ksize,
+                                                    int stride, int g0, int g1, int g2,
+                                                    const uint64_t* __restrict__ slots, uint64_t mask,
+                                                    int32_t* __restrict__ nbr, int32_t* __restrict__ counts,
+                                                    const int64_t* __restrict__ offs, int32_t* __restrict__ pairs) {
+  __shared__ int wcount[4];
+  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int s = blockIdx.y;
+  const int nblk = gridDim.x;
+  int nb = -1;
+  if (kCount) {
+    if (p < n_out) {
+      int h = (ksize - 1) / 2;
+      int dx = s / (ksize * ksize) - h, dy = (s / ksize) % ksize - h, dz = s % ksize - h;
+      int4 v = reinterpret_cast<const int4*>(out_c)[p];
+      int yx = stride * v.y - dx, yy = stride * v.z - dy, yz = stride * v.w - dz;
+      if (yx >= 0 && yy >= 0 && yz >= 0 && yx < g0 && yy < g1 && yz < g2)
+        nb = hash_find(slots, mask, site_key(v.x, yx, yy, yz, g0, g1, g2));
+      nbr[(int64_t)s * n_out + p] = nb;
+    }
+  } else if (p < n_out) {
+    nb = nbr[(int64_t)s * n_out + p];
+  }
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const uint64_t ball = __ballot(nb >= 0);
+  if (lane == 0) wcount[w] = __popcll(ball);
+  __syncthreads();
+  if (kCount) {
+    if (threadIdx.x == 0) counts[(int64_t)s * nblk + blockIdx.x] = wcount[0] + wcount[1] + wcount[2] + wcount[3];
+  } else if (nb >= 0) {
+    int before = 0;
+    for (int i = 0; i < w; ++i) before += wcount[i];
+    const uint64_t lower = lane ? (ball & ((1ull << lane) - 1)) : 0ull;
+    int64_t at = offs[(int64_t)s * nblk + blockIdx.x] + before + __popcll(lower);
+    reinterpret_cast<int2*>(pairs)[at] = make_int2((int)p, nb);
+  }
+}
+
+__global__ void gather_offsets(const int64_t* __restrict__ offs, int K, int nblk, const int64_t* __restrict__ total,
+                               int64_t* __restrict__ pair_off) {
+  int s = threadIdx.x;
+  if (s < K) pair_off[s] = offs[(int64_t)s * nblk];
+  if (s == 0) pair_off[K] = *total;
+}
+
+int64_t next_pow2(int64_t v) {
+  int64_t c = 64;
+  while (c < v) c <<= 1;
+  return c;
+}
+
+// Pinned host staging for the few values the build reads back.
+struct Staging {
+  int64_t* p = nullptr;
+  int get(int64_t** out) {
+    if (!p) {
+      void* q = nullptr;
+      if (hipHostMalloc(&q, 4096, hipHostMallocDefault) != hipSuccess || !q) {
+        (void)hipGetLastError();
+        return fail(SSCONV_E_NOMEM, "pinned host staging allocation failed");
+      }
+      p = (int64_t*)q;
+    }
+    *out = p;
+    return SSCONV_OK;
+  }
+};
+thread_local Staging g_stage;
+
+}  // namespace
+
+void rulebook_free(ssconv_rulebook* rb) {
+  if (!rb) return;
+  hipStream_t s = rb->stream;
+  if (rb->hash_out && rb->hash_out != rb->hash_in) dev_free(rb->hash_out, s);
+  dev_free(rb->hash_in, s);
+  dev_free(rb->out_coords, s);
+  dev_free(rb->nbr, s);
+  dev_free(rb->pairs, s);
+  dev_free(rb->pair_off_dev, s);
+  delete[] rb->pair_off;
+  delete rb;
+}
+
+// Temporary device buffers released on every exit path.
+struct Scratch {
+  hipStream_t s;
+  void* ptrs[8] = {};
+  int n = 0;
+  explicit Scratch(hipStream_t st) : s(st) {}
+  int alloc(void** p, size_t bytes) {
+    SSC_TRY(dev_alloc(p, bytes, s));
+    ptrs[n++] = *p;
+    return SSCONV_OK;
+  }
+  ~Scratch() {
+    for (int i = 0; i < n; ++i) dev_free(ptrs[i], s);
+  }
+};
+
+static int build_hash(const int32_t* coords, int64_t n, const int* g, hipStream_t st, uint64_t** slots,
+                      int64_t* cap, int* flags) {
+  int64_t c = debug_hash_capacity();
+  if (c <= 0) c = next_pow2(2 * n);
+  if (c & (c - 1)) return fail(SSCONV_E_INVALID, "forced hash capacity must be a power of two");
+  *cap = c;
+  SSC_TRY(dev_alloc((void**)slots, (size_t)c * 8, st));
+  fill_u64<<<cdiv(c, 256), 256, 0, st>>>(*slots, c, kEmpty);
+  if (n > 0) hash_insert_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, g[0], g[1], g[2], *slots, (uint64_t)(c - 1), flags);
+  SSC_HIP(hipGetLastError());
+  return SSCONV_OK;
+}
+
+static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int ksize, int stride, int submanifold,
+                      hipStream_t st, ssconv_rulebook* rb) {
+  rb->ksize = ksize;
+  rb->K = ksize * ksize * ksize;
+  rb->stride = stride;
+  rb->submanifold = submanifold;
+  rb->stream = st;
+  rb->n_in = n;
+  for (int a = 0; a < 3; ++a) {
+    rb->grid[a] = grid[a];
+    rb->grid_out[a] = (grid[a] + stride - 1) / stride;
+  }
+  const int K = rb->K;
+  rb->pair_off = new int64_t[K + 1]();
+  int64_t* host = nullptr;
+  SSC_TRY(g_stage.get(&host));
+
+  Scratch tmp(st);
+  int* dflags = nullptr;  // [0] flags, [1] max b
+  SSC_TRY(tmp.alloc((void**)&dflags, 64));
+  SSC_HIP(hipMemsetAsync(dflags, 0, 4, st));
+  SSC_HIP(hipMemsetAsync(dflags + 1, 0xff, 4, st));  // max b = -1
+  if (n > 0) validate_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, grid[0], grid[1], grid[2], dflags, dflags + 1);
+  SSC_HIP(hipGetLastError());
+  SSC_HIP(hipMemcpyAsync(host, dflags, 8, hipMemcpyDeviceToHost, st));
+  SSC_HIP(hipStreamSynchronize(st));
+  const int flags0 = ((int*)host)[0], maxb = ((int*)host)[1];
+  if (flags0 & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid or has b < 0");
+  const int64_t cells = (int64_t)grid[0] * grid[1] * grid[2];
+  if ((int64_t)(maxb + 1) * cells > 0xFFFFFFFFll)
+    return fail(SSCONV_E_BOUNDS, "(max b + 1) * grid volume exceeds the 32-bit key space");
+  rb->nbatch = maxb + 1;
+
+  SSC_TRY(build_hash(coords, n, rb->grid, st, &rb->hash_in, &rb->cap_in, dflags));
+
+  // ---- output site set ----
+  if (submanifold) {
+    rb->n_out = n;
+    SSC_TRY(dev_alloc((void**)&rb->out_coords, (size_t)n * 16, st));
+    if (n) SSC_HIP(hipMemcpyAsync(rb->out_coords, coords, (size_t)n * 16, hipMemcpyDeviceToDevice, st));
+    rb->hash_out = rb->hash_in;
+    rb->cap_out = rb->cap_in;
+  } else {
+    const int* go = rb->grid_out;
+    const int64_t nbits = rb->nbatch * (int64_t)go[0] * go[1] * go[2];
+    const int64_t nw = (nbits + 31) / 32;
+    uint32_t* bits = nullptr;
+    int32_t* wcnt = nullptr;
+    int64_t *woff = nullptr, *stmp = nullptr, *dtotal = nullptr;
+    SSC_TRY(tmp.alloc((void**)&bits, (size_t)nw * 4));
+    SSC_TRY(tmp.alloc((void**)&wcnt, (size_t)nw * 4));
+    SSC_TRY(tmp.alloc((void**)&woff, (size_t)nw * 8));
+    SSC_TRY(tmp.alloc((void**)&stmp, (size_t)scan_tmp_elems(nw) * 8 + 8));
+    dtotal = stmp + scan_tmp_elems(nw);
+    if (nw) SSC_HIP(hipMemsetAsync(bits, 0, (size_t)nw * 4, st));
+    if (n > 0) {
+      dim3 gm(cdiv(n, 256), K);
+      mark_outputs<<<gm, 256, 0, st>>>(coords, n, ksize, stride, go[0], go[1], go[2], bits);
+    }
+    if (nw) {
+      popcount_words<<<cdiv(nw, 256), 256, 0, st>>>(bits, nw, wcnt);
+      SSC_TRY(exclusive_scan(wcnt, nw, woff, dtotal, stmp, st));
+    } else {
+      SSC_HIP(hipMemsetAsync(dtotal, 0, 8, st));
+    }
+    SSC_HIP(hipMemcpyAsync(host, dtotal, 8, hipMemcpyDeviceToHost, st));
+    SSC_HIP(hipStreamSynchronize(st));
+    rb->n_out = host[0];
+    SSC_TRY(dev_alloc((void**)&rb->out_coords, (size_t)rb->n_out * 16, st));
+    if (nw) emit_outputs<<<cdiv(nw, 256), 256, 0, st>>>(bits, nw, woff, go[0], go[1], go[2], rb->out_coords);
+    SSC_HIP(hipGetLastError());
+    SSC_TRY(build_hash(rb->out_coords, rb->n_out, go, st, &rb->hash_out, &rb->cap_out, dflags));
+  }
+
+  // ---- neighbour map and per-offset pair lists ----
+  const int64_t n_out = rb->n_out;
+  SSC_TRY(dev_alloc((void**)&rb->nbr, (size_t)K * n_out * 4, st));
+  SSC_TRY(dev_alloc((void**)&rb->pair_off_dev, (size_t)(K + 1) * 8, st));
+  if (n_out > 0) {
+    const int nblk = (int)cdiv(n_out, 256);
+    const int64_t ncnt = (int64_t)K * nblk;
+    int32_t* counts = nullptr;
+    int64_t *offs = nullptr, *stmp = nullptr;
+    SSC_TRY(tmp.alloc((void**)&counts, (size_t)ncnt * 4));
+    SSC_TRY(tmp.alloc((void**)&offs, (size_t)ncnt * 8));
+    SSC_TRY(tmp.alloc((void**)&stmp, (size_t)scan_tmp_elems(ncnt) * 8 + 8));
+    int64_t* dtotal = stmp + scan_tmp_elems(ncnt);
+    dim3 gp(nblk, K);
+    probe_kernel<true><<<gp, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0], grid[1], grid[2],
+                                          rb->hash_in, (uint64_t)(rb->cap_in - 1), rb->nbr, counts, nullptr, nullptr);
+    SSC_HIP(hipGetLastError());
+    SSC_TRY(exclusive_scan(counts, ncnt, offs, dtotal, stmp, st));
+    gather_offsets<<<1, 256, 0, st>>>(offs, K, nblk, dtotal, rb->pair_off_dev);
+    SSC_HIP(hipMemcpyAsync(host, rb->pair_off_dev, (size_t)(K + 1) * 8, hipMemcpyDeviceToHost, st));
+    SSC_HIP(hipMemcpyAsync(host + K + 1, dflags, 4, hipMemcpyDeviceToHost, st));
+    SSC_HIP(hipStreamSynchronize(st));
+    for (int s = 0; s <= K; ++s) rb->pair_off[s] = host[s];
+    rb->n_pairs = host[K];
+    const int fl = (int)(host[K + 1] & 0xffffffff);
+    if (fl & kFlagDup) return fail(SSCONV_E_DUPLICATE, "duplicate input site");
+    if (fl & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
+    SSC_TRY(dev_alloc((void**)&rb->pairs, (size_t)rb->n_pairs * 8, st));
+    probe_kernel<false><<<gp, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0], grid[1], grid[2],
+                                           rb->hash_in, (uint64_t)(rb->cap_in - 1), rb->nbr, nullptr, offs, rb->pairs);
+    SSC_HIP(hipGetLastError());
+  } else {
+    SSC_HIP(hipMemsetAsync(rb->pair_off_dev, 0, (size_t)(K + 1) * 8, st));
+    SSC_HIP(hipMemcpyAsync(host, dflags, 4, hipMemcpyDeviceToHost, st));
+    SSC_HIP(hipStreamSynchronize(st));
+    const int fl = (int)(host[0] & 0xffffffff);
+    if (fl & kFlagDup) return fail(SSCONV_E_DUPLICATE, "duplicate input site");
+    if (fl & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
+    SSC_TRY(dev_alloc((void**)&rb->pairs, 8, st));
+  }
+  return SSCONV_OK;
+}
+
+}  // namespace ssconv
+
+using namespace ssconv;
+
+extern "C" int ssconv_build_rulebook(const int32_t* coords, int64_t n, const int32_t* grid, int ksize, int stride,
+                                     int submanifold, hipStream_t stream, ssconv_rulebook_t* out) {
+  if (!out) return fail(SSCONV_E_INVALID, "out handle pointer is NULL");
+  *out = nullptr;
+  if (!grid) return fail(SSCONV_E_INVALID, "grid is NULL");
+  if (n < 0 || (n > 0 && !coords)) return fail(SSCONV_E_INVALID, "bad coords/n");
+  if (n > 0x7fffffffll) return fail(SSCONV_E_INVALID, "at most 2^31-1 sites");
+  if (n > 0 && !aligned16(coords)) return fail(SSCONV_E_INVALID, "coords must be 16-byte aligned");
+  if (ksize < 1 || ksize > 5 || (ksize & 1) == 0) return fail(SSCONV_E_INVALID, "ksize must be odd, 1..5");
+  if (stride != 1 && stride != 2) return fail(SSCONV_E_INVALID, "stride must be 1 or 2");
+  if (submanifold && stride != 1) return fail(SSCONV_E_INVALID, "submanifold requires stride 1");
+  for (int a = 0; a < 3; ++a)
+    if (grid[a] < 1) return fail(SSCONV_E_INVALID, "grid extents must be positive");
+  auto* rb = new ssconv_rulebook();
+  int rc = build_impl(coords, n, grid, ksize, stride, submanifold ? 1 : 0, stream, rb);
+  if (rc != SSCONV_OK) {
+    std::string msg = ssconv_last_error();
+    rulebook_free(rb);
+    set_error("%s", msg.c_str());
+    return rc;
+  }
+  *out = rb;
+  return SSCONV_OK;
+}
+
+extern "C" int ssconv_rulebook_info(ssconv_rulebook_t rb, int64_t* n_in, int64_t* n_out, int64_t* pair_counts) {
+  if (!rb) return fail(SSCONV_E_INVALID, "NULL rule book");
+  if (n_in) *n_in = rb->n_in;
+  if (n_out) *n_out = rb->n_out;
+  if (pair_counts)
+    for (int s = 0; s < rb->K; ++s) pair_counts[s] = rb->pair_off[s + 1] - rb->pair_off[s];
+  return SSCONV_OK;
+}
+
+extern "C" int ssconv_rulebook_out_coords(ssconv_rulebook_t rb, int32_t* dst, hipStream_t stream) {
+  if (!rb || (!dst && rb->n_out)) return fail(SSCONV_E_INVALID, "NULL argument");
+  if (rb->n_out) SSC_HIP(hipMemcpyAsync(dst, rb->out_coords, (size_t)rb->n_out * 16, hipMemcpyDeviceToDevice, stream));
+  return SSCONV_OK;
+}
+
+extern "C" int ssconv_rulebook_pairs(ssconv_rulebook_t rb, int32_t* dst, hipStream_t stream) {
+  if (!rb || (!dst && rb->n_pairs)) return fail(SSCONV_E_INVALID, "NULL argument");
+  if (rb->n_pairs) SSC_HIP(hipMemcpyAsync(dst, rb->pairs, (size_t)rb->n_pairs * 8, hipMemcpyDeviceToDevice, stream));
+  return SSCONV_OK;
+}
+
+extern "C" int ssconv_rulebook_neighbours(ssconv_rulebook_t rb, int32_t* dst, hipStream_t stream) {
+  if (!rb || (!dst && rb->n_out)) return fail(SSCONV_E_INVALID, "NULL argument");
+  if (rb->n_out)
+    SSC_HIP(hipMemcpyAsync(dst, rb->nbr, (size_t)rb->K * rb->n_out * 4, hipMemcpyDeviceToDevice, stream));
+  return SSCONV_OK;
+}
+
+extern "C" int ssconv_rulebook_hash(ssconv_rulebook_t rb, int which, uint64_t* dst, int64_t* capacity,
+                                    hipStream_t stream) {
+  if (!rb || (which != 0 && which != 1)) return fail(SSCONV_E_INVALID, "bad argument");
+  const uint64_t* src = which ? rb->hash_out : rb->hash_in;
+  int64_t cap = which ? rb->cap_out : rb->cap_in;
+  if (capacity) *capacity = cap;
+  if (dst) SSC_HIP(hipMemcpyAsync(dst, src, (size_t)cap * 8, hipMemcpyDeviceToDevice, stream));
+  return SSCONV_OK;
+}
+
+extern "C" void ssconv_rulebook_destroy(ssconv_rulebook_t rb) { rulebook_free(rb); }

@@ -1,0 +1,153 @@
+// Kernel synthesis (Sec. 3.2.1, Eq. 7 with the block matrix of Eq. 9) and its adjoint.
+//
+// W[s][o][i] = sum_q w[off(field(o), field(i)) + q] * B^{k l}_q[s][a][b], one thread per
+// element of W so the dominant cost -- writing W -- is a coalesced stream.
+// The adjoint dw[off + q] = sum_{s,a,b} dW[s][o][i] B_q[s][a][b] uses one
+// workgroup per (out field, in field) pair with a fixed reduction tree.
+#include "synth.hpp"
+
+namespace ssconv {
+
+int make_synth_args(const ssconv_basis_desc* d, SynthArgs* a) {
+  int nq[SSCONV_MAX_L + 1][SSCONV_MAX_L + 1];
+  int64_t base[SSCONV_MAX_L + 1][SSCONV_MAX_L + 1];
+  int64_t floats = 0;
+  SSC_TRY(basis_nq_table(d, nq, base, &floats));
+  SSC_TRY(make_fieldtab(&d->in, &a->in));
+  SSC_TRY(make_fieldtab(&d->out, &a->out));
+  a->K = d->ksize * d->ksize * d->ksize;
+  a->cin = a->in.ch0[a->in.n];
+  a->cout = a->out.ch0[a->out.n];
+  for (int k = 0; k <= SSCONV_MAX_L; ++k) {
+    int64_t r = 0;
+    for (int e = 0; e < a->in.n; ++e) r += (int64_t)a->in.mult[e] * nq[k][a->in.l[e]];
+    a->rowsz[k] = r;
+    for (int l = 0; l <= SSCONV_MAX_L; ++l) {
+      a->nq[k][l] = nq[k][l];
+      a->base[k][l] = base[k][l];
+    }
+  }
+  // coefficient offset of the first field of every out entry
+  int64_t off = 0;
+  for (int e = 0; e < a->out.n; ++e) {
+    a->row0[e] = off;
+    off += (int64_t)a->out.mult[e] * a->rowsz[a->out.l[e]];
+  }
+  a->n_coeff = off;
+  a->n_out_fields = a->out.f0[a->out.n];
+  a->n_in_fields = a->in.f0[a->in.n];
+  return SSCONV_OK;
+}
+
+namespace {
+
+struct ChanInfo {
+  int entry, field, comp, l;
+};
+
+__device__ __forceinline__ ChanInfo chan_info(const FieldTab& t, int c) {
+  int e = 0;
+  while (e + 1 < t.n && c >= t.ch0[e + 1]) ++e;
+  const int d = 2 * t.l[e] + 1, r = c - t.ch0[e];
+  return ChanInfo{e, r / d, r % d, t.l[e]};
+}
+
+// Offset of the first coefficient of the (out field (eo, fo), in field (ei, fi)) block.
+__device__ __forceinline__ int64_t coeff_off(const SynthArgs& a, int eo, int fo, int k, int ei, int fi) {
+  int64_t off = a.row0[eo] + (int64_t)fo * a.rowsz[k];
+  for (int e = 0; e < ei; ++e) off += (int64_t)a.in.mult[e] * a.nq[k][a.in.l[e]];
+  return off + (int64_t)fi * a.nq[k][a.in.l[ei]];
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void synth_kernel(SynthArgs a, const float* __restrict__ basis,
+                                                    const float* __restrict__ coeffs, T* __restrict__ W) {
+  const int64_t total = (int64_t)a.K * a.cout * a.cin;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= total) return;
+  const int ci = (int)(idx % a.cin);
+  const int co = (int)((idx / a.cin) % a.cout);
+  const int s = (int)(idx / ((int64_t)a.cin * a.cout));
+  const ChanInfo o = chan_info(a.out, co), i = chan_info(a.in, ci);
+  const int k = o.l, l = i.l, dk = 2 * k + 1, dl = 2 * l + 1;
+  const int nq = a.nq[k][l];
+  const int64_t off = coeff_off(a, o.entry, o.field, k, i.entry, i.field);
+  const float* bp = basis + a.base[k][l] + ((int64_t)s * dk + o.comp) * dl + i.comp;
+  const int64_t qstride = (int64_t)a.K * dk * dl;
+  float acc = 0.f;
+  for (int q = 0; q < nq; ++q) acc = fmaf(coeffs[off + q], bp[q * qstride], acc);
+  W[idx] = DT<T>::from_f(acc);
+}
+
+constexpr int kMaxNq = 2 * SSCONV_MAX_SHELLS * (2 * SSCONV_MAX_L + 1);
+
+__global__ __launch_bounds__(256) void synth_adjoint_kernel(SynthArgs a, const float* __restrict__ basis,
+                                                            const float* __restrict__ dW, float* __restrict__ dcoef) {
+  // block = (in field j, out field i)
+  const int fi_all = blockIdx.x, fo_all = blockIdx.y;
+  int eo = 0, ei = 0;
+  while (eo + 1 < a.out.n && fo_all >= a.out.f0[eo + 1]) ++eo;
+  while (ei + 1 < a.in.n && fi_all >= a.in.f0[ei + 1]) ++ei;
+  const int fo = fo_all - a.out.f0[eo], fi = fi_all - a.in.f0[ei];
+  const int k = a.out.l[eo], l = a.in.l[ei], dk = 2 * k + 1, dl = 2 * l + 1;
+  const int nq = a.nq[k][l];
+  if (nq == 0) return;
+  const int ro = a.out.ch0[eo] + fo * dk, cc = a.in.ch0[ei] + fi * dl;
+  const int64_t off = coeff_off(a, eo, fo, k, ei, fi);
+  const int n = a.K * dk * dl;
+  const int64_t qstride = (int64_t)a.K * dk * dl;
+  const float* bp = basis + a.base[k][l];
+  float acc[kMaxNq];
+  for (int q = 0; q < nq; ++q) acc[q] = 0.f;
+  for (int e = threadIdx.x; e < n; e += 256) {
+    const int s = e / (dk * dl), r = e % (dk * dl), aa = r / dl, bb = r % dl;
+    const float g = dW[((int64_t)s * a.cout + ro + aa) * a.cin + cc + bb];
+    for (int q = 0; q < nq; ++q) acc[q] = fmaf(g, bp[q * qstride + e], acc[q]);
+  }
+  __shared__ float red[256];
+  for (int q = 0; q < nq; ++q) {
+    red[threadIdx.x] = acc[q];
+    __syncthreads();
+    for (int w = 128; w > 0; w >>= 1) {
+      if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) dcoef[off + q] = red[0];
+    __syncthreads();
+  }
+}
+
+}  // namespace
+
+int launch_synth(const SynthArgs& a, const float* basis, const float* coeffs, ssconv_dtype dt, void* W,
+                 hipStream_t st) {
+  const int64_t total = (int64_t)a.K * a.cout * a.cin;
+  if (total == 0) return SSCONV_OK;
+  if (dt == SSCONV_F32)
+    synth_kernel<float><<<cdiv(total, 256), 256, 0, st>>>(a, basis, coeffs, (float*)W);
+  else
+    synth_kernel<uint16_t><<<cdiv(total, 256), 256, 0, st>>>(a, basis, coeffs, (uint16_t*)W);
+  SSC_HIP(hipGetLastError());
+  return SSCONV_OK;
+}
+
+int launch_synth_adjoint(const SynthArgs& a, const float* basis, const float* dW, float* dcoef, hipStream_t st) {
+  if (a.n_coeff == 0) return SSCONV_OK;
+  dim3 g(a.n_in_fields, a.n_out_fields);
+  synth_adjoint_kernel<<<g, 256, 0, st>>>(a, basis, dW, dcoef);
+  SSC_HIP(hipGetLastError());
+  return SSCONV_OK;
+}
+
+}  // namespace ssconv
+
+using namespace ssconv;
+
+extern "C" int ssconv_synth_kernel(const ssconv_basis_desc* desc, const float* basis, const float* coeffs,
+                                   ssconv_dtype w_dtype, void* W, hipStream_t stream) {
+  if (w_dtype != SSCONV_F32 && w_dtype != SSCONV_BF16) return fail(SSCONV_E_DTYPE, "unsupported W dtype");
+  if (!basis || !coeffs || !W) return fail(SSCONV_E_INVALID, "NULL device pointer");
+  SynthArgs a;
+  SSC_TRY(make_synth_args(desc, &a));
+  return launch_synth(a, basis, coeffs, w_dtype, W, stream);
+}

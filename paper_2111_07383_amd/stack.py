@@ -1,0 +1,89 @@
+"""A stack of SS-Conv layers with the gated nonlinearity between them (Sec. 3.2-3.3).
+
+Every step calls the C ABI through ``binding``; this module only sequences the
+calls and keeps what the backward pass needs.  A layer object provides
+``fields_in``, ``fields_out`` (gate channels included when ``gated``),
+``ksize``, ``stride``, ``submanifold``, ``shells``, ``eps``, ``jmax``, ``gated``.
+"""
+from dataclasses import dataclass, field
+from typing import List, Optional
+
+import torch
+
+from . import binding as B
+
+
+@dataclass
+class LayerState:
+    layer: object
+    desc: object
+    basis: torch.Tensor          # fp32 device basis of ssconv_basis_build
+    coeffs: torch.Tensor         # fp32 device coefficients
+    n_coeff: int
+    grid: int                    # input grid extent
+    rb: Optional[B.Rulebook] = None
+    W: Optional[torch.Tensor] = None
+    x: Optional[torch.Tensor] = None   # layer input features
+    y: Optional[torch.Tensor] = None   # convolution output (before the gate)
+
+
+def regular_fields(layer):
+    """Output fields without the appended gate channels."""
+    return tuple(layer.fields_out[:-1]) if layer.gated else tuple(layer.fields_out)
+
+
+@dataclass
+class Stack:
+    layers: List[LayerState] = field(default_factory=list)
+    dtype: torch.dtype = torch.float32
+
+    @staticmethod
+    def create(layer_specs, coeffs_list, grid: int, device, dtype=torch.float32) -> "Stack":
+        st = Stack(dtype=dtype)
+        g = grid
+        for spec, w in zip(layer_specs, coeffs_list):
+            desc = B.layer_desc(spec)
+            basis = torch.from_numpy(B.basis_build(desc)).to(device)
+            n_coeff = B.basis_info(desc)[1]
+            c = torch.as_tensor(w, dtype=torch.float32).to(device)
+            if c.numel() != n_coeff:
+                raise ValueError(f"layer expects {n_coeff} coefficients, got {c.numel()}")
+            st.layers.append(LayerState(spec, desc, basis, c, n_coeff, g))
+            g = -(-g // spec.stride)
+        return st
+
+    def forward(self, coords: torch.Tensor, feats: torch.Tensor):
+        """Returns (output coords, output features); rule books are rebuilt every call."""
+        h, c = feats, coords
+        for L in self.layers:
+            s = L.layer
+            if L.rb is not None:
+                L.rb.close()
+            L.rb = B.Rulebook(c, L.grid, s.ksize, s.stride, s.submanifold)
+            L.W = B.synth_kernel(L.desc, L.basis, L.coeffs, self.dtype)
+            L.x = h
+            L.y = B.forward(h, L.rb, L.W)
+            h = B.gate_forward(regular_fields(s), L.y) if s.gated else L.y
+            c = c if s.submanifold else L.rb.out_coords()
+        return c, h
+
+    def backward(self, grad: torch.Tensor, need_input_grad: bool = True):
+        """Returns (grad of the stack input or None, [grad_coeffs per layer])."""
+        g = grad
+        gcs = [None] * len(self.layers)
+        for idx in range(len(self.layers) - 1, -1, -1):
+            L = self.layers[idx]
+            s = L.layer
+            if s.gated:
+                g = B.gate_backward(regular_fields(s), L.y, g)
+            gf, gc = B.backward(L.x, g, L.rb, L.W, L.desc, L.basis, need_feats=(idx > 0 or need_input_grad),
+                                need_coeffs=True, n_coeff=L.n_coeff)
+            gcs[idx] = gc
+            g = gf
+        return g, gcs
+
+    def close(self):
+        for L in self.layers:
+            if L.rb is not None:
+                L.rb.close()
+                L.rb = None

@@ -1,0 +1,135 @@
+"""GPU edge cases and failure paths of the C ABI.
+
+Failures are forced from the host (bad arguments, duplicate or out-of-grid
+sites, a forced small hash capacity, a forced allocation failure); every
+kernel still runs to completion.  Ragged shapes exercise partial tiles, odd
+channel counts (scalar gather path) and empty inputs.
+"""
+import numpy as np
+import pytest
+
+from cases import rel_err
+from oracle import conv as oc
+from oracle import rulebook as orb
+from workloads.configs import LayerSpec
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+P = pytest.importorskip("paper_2111_07383_amd")
+from paper_2111_07383_amd._abi import E_BOUNDS, E_DUPLICATE, E_HASH_FULL, E_INVALID, E_NOMEM, SSConvError  # noqa: E402
+
+DEV = "cuda:0"
+
+
+def _coords(seed, n, grid, batch=1):
+    rng = np.random.default_rng(seed)
+    c = np.concatenate([rng.integers(0, batch, (n, 1)), rng.integers(0, grid, (n, 3))], 1)
+    return np.unique(c, axis=0).astype(np.int32)
+
+
+def _code(fn):
+    with pytest.raises(SSConvError) as e:
+        fn()
+    return e.value.code
+
+
+def test_error_codes():
+    c = torch.from_numpy(_coords(0, 50, 8)).to(DEV)
+    dup = torch.cat([c, c[:1]])
+    assert _code(lambda: P.Rulebook(dup, 8, 3)) == E_DUPLICATE
+    bad = c.clone()
+    bad[3, 2] = 8
+    assert _code(lambda: P.Rulebook(bad, 8, 3)) == E_BOUNDS
+    neg = c.clone()
+    neg[0, 0] = -1
+    assert _code(lambda: P.Rulebook(neg, 8, 3)) == E_BOUNDS
+    assert _code(lambda: P.Rulebook(c, 8, 3, stride=2, submanifold=True)) == E_INVALID
+    assert _code(lambda: P.Rulebook(c, 8, 4)) == E_INVALID
+    assert _code(lambda: P.Rulebook(c, 8, 3, stride=3, submanifold=False)) == E_INVALID
+    big = c.clone()
+    big[:, 0] = 70000                                   # (b+1) * 8^3 exceeds 32 bits
+    assert _code(lambda: P.Rulebook(big, 8, 3)) == E_BOUNDS
+    P.debug_set(1, 16)                                  # 16 slots for 50 sites
+    try:
+        assert _code(lambda: P.Rulebook(c, 8, 3)) == E_HASH_FULL
+    finally:
+        P.debug_set(1, 0)
+    P.debug_set(2, 2)                                   # second allocation fails
+    assert _code(lambda: P.Rulebook(c, 8, 3)) == E_NOMEM
+    P.debug_set(2, 0)
+    rb = P.Rulebook(c, 8, 3)                            # library still healthy
+    assert rb.n_out == len(c)
+    rb.close()
+
+
+def test_empty_input():
+    c = torch.zeros((0, 4), dtype=torch.int32, device=DEV)
+    for stride, sub in ((1, True), (2, False)):
+        rb = P.Rulebook(c, 16, 3, stride, sub)
+        assert rb.n_in == 0 and rb.n_out == 0 and rb.n_pairs == 0
+        W = torch.zeros((27, 8, 4), device=DEV)
+        out = P.forward(torch.zeros((0, 4), device=DEV), rb, W)
+        assert out.shape == (0, 8)
+        rb.close()
+
+
+@pytest.mark.parametrize("ksize,stride,sub,dtype", [
+    (3, 1, True, "f32"), (5, 1, True, "f32"), (3, 2, False, "f32"), (3, 1, False, "f32"),
+    (5, 2, False, "f32"), (1, 1, True, "f32"), (3, 1, True, "bf16"), (5, 2, False, "bf16")])
+def test_ragged_layers(ksize, stride, sub, dtype):
+    """Odd channel counts (13 -> 14), a partial last tile and several batch entries."""
+    spec = LayerSpec(ksize, stride, sub, ((0, 2), (1, 2), (2, 1)), ((0, 1), (1, 1), (2, 2)),
+                     shells=tuple(float(m) for m in range(ksize // 2 + 1)))
+    grid = 12
+    c = _coords(ksize * 7 + stride, 333, grid, batch=3)
+    lay = oc.Layer(spec)
+    rng = np.random.default_rng(5)
+    w = rng.standard_normal(lay.n_coeff).astype(np.float32)
+    f = rng.standard_normal((len(c), spec.cin)).astype(np.float32)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    if dtype == "bf16":
+        f = torch.from_numpy(f).to(tdt).float().numpy()
+    co = orb.output_sites(c, grid, ksize, stride, sub)
+    R = orb.rulebook(c, co, ksize, stride)
+    kap = lay.kappa(w, bf16=(dtype == "bf16"))
+    want = oc.forward(f, R, kap, len(co))
+    g = rng.standard_normal((len(co), spec.cout)).astype(np.float32)
+    if dtype == "bf16":
+        g = torch.from_numpy(g).to(tdt).float().numpy()
+    d_in = oc.grad_feats(g, R, kap, len(c))
+    dw = oc.synth_adjoint(spec, lay.basis, oc.grad_kappa(f, g, R, kap.shape))
+
+    desc = P.layer_desc(spec)
+    basis = torch.from_numpy(P.basis_build(desc)).to(DEV)
+    rb = P.Rulebook(torch.from_numpy(c).to(DEV), grid, ksize, stride, sub)
+    np.testing.assert_array_equal(rb.out_coords().cpu().numpy(), co)
+    W = P.synth_kernel(desc, basis, torch.from_numpy(w).to(DEV), tdt)
+    ft = torch.from_numpy(f).to(DEV).to(tdt)
+    out = P.forward(ft, rb, W).float().cpu().numpy()
+    gf, gc = P.backward(ft, torch.from_numpy(g).to(DEV).to(tdt), rb, W, desc, basis)
+    tol = 2e-2 if dtype == "bf16" else 1e-4
+    assert rel_err(out, want) < tol
+    assert rel_err(gf.float().cpu().numpy(), d_in) < tol
+    assert rel_err(gc.cpu().numpy(), dw) < tol
+    rb.close()
+
+
+def test_row_order_independence():
+    """Permuting the input rows permutes submanifold outputs the same way."""
+    spec = LayerSpec(3, 1, True, ((0, 4), (1, 4)), ((0, 4), (1, 4)), shells=(0.0, 1.0))
+    c = _coords(11, 2000, 20, batch=2)
+    perm = np.random.default_rng(1).permutation(len(c))
+    lay = oc.Layer(spec)
+    rng = np.random.default_rng(2)
+    w = torch.from_numpy(rng.standard_normal(lay.n_coeff).astype(np.float32)).to(DEV)
+    f = rng.standard_normal((len(c), spec.cin)).astype(np.float32)
+    desc = P.layer_desc(spec)
+    basis = torch.from_numpy(P.basis_build(desc)).to(DEV)
+    W = P.synth_kernel(desc, basis, w)
+    outs = []
+    for cc, ff in ((c, f), (c[perm], f[perm])):
+        rb = P.Rulebook(torch.from_numpy(np.ascontiguousarray(cc)).to(DEV), 20, 3)
+        outs.append(P.forward(torch.from_numpy(np.ascontiguousarray(ff)).to(DEV), rb, W).cpu().numpy())
+        rb.close()
+    assert rel_err(outs[1], outs[0][perm]) < 1e-6

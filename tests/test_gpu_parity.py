@@ -1,0 +1,139 @@
+"""GPU parity: the HIP library against the fp64 oracle on the five seeded workloads.
+
+Rule books and hash tables must match exactly (same sets, same order); fp32
+features within 1e-4 and bf16 within 2e-2, as L_inf error over the L_inf norm
+of the oracle result.  Every call goes through the C ABI.
+"""
+import numpy as np
+import pytest
+
+from cases import coords_of, features_of, layers_of, rel_err, single_layer_reference
+from workloads import CONFIGS
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+P = pytest.importorskip("paper_2111_07383_amd")
+
+DEV = "cuda:0"
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def _dt(i):
+    return torch.bfloat16 if CONFIGS[i].dtype == "bf16" else torch.float32
+
+
+def _tensor(a, dtype=None):
+    t = torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+    return t.to(dtype) if dtype is not None else t
+
+
+def _pair_keys(s, o, i):
+    return (np.asarray(s, np.int64) << 42) | (np.asarray(o, np.int64) << 21) | np.asarray(i, np.int64)
+
+
+def _check_rulebook(L, rb):
+    K = L.spec.ksize ** 3
+    assert rb.n_in == len(L.coords_in) and rb.n_out == len(L.coords_out)
+    np.testing.assert_array_equal(rb.out_coords().cpu().numpy(), L.coords_out)
+    counts = np.array([len(r) for r in L.R])
+    np.testing.assert_array_equal(rb.pair_counts, counts)
+    got = rb.pairs().cpu().numpy().astype(np.int64)
+    want = np.concatenate([r for r in L.R if len(r)] or [np.zeros((0, 2), np.int64)])
+    s_idx = np.repeat(np.arange(K), counts)
+    # same set of (s, out, in) triples, and the same order (grouped by s, out rows ascending)
+    assert np.array_equal(np.sort(_pair_keys(s_idx, got[:, 0], got[:, 1])), np.sort(_pair_keys(s_idx, want[:, 0], want[:, 1])))
+    np.testing.assert_array_equal(got, want)
+    np.testing.assert_array_equal(rb.neighbours().cpu().numpy(), L.nbr)
+
+
+def _check_hash(coords, grid, slots):
+    slots = slots.cpu().numpy().view(np.uint64)
+    occ = slots != np.uint64(0xFFFFFFFFFFFFFFFF)
+    keys = (slots[occ] >> np.uint64(32)).astype(np.int64)
+    rows = (slots[occ] & np.uint64(0xFFFFFFFF)).astype(np.int64)
+    c = coords.astype(np.int64)
+    want = ((c[:, 0] * grid + c[:, 1]) * grid + c[:, 2]) * grid + c[:, 3]
+    got = np.zeros(len(c), np.int64) - 1
+    assert len(rows) == len(c) and len(np.unique(rows)) == len(c)
+    got[rows] = keys
+    np.testing.assert_array_equal(got, want)
+
+
+@pytest.mark.parametrize("i", [1, 2, 3, 4, 5])
+def test_rulebook_and_hash_exact(i):
+    spec = CONFIGS[i]
+    for L in layers_of(i):
+        print(f"rulebook config {i} grid {L.grid} k{L.spec.ksize} s{L.spec.stride} n={len(L.coords_in)}", flush=True)
+        rb = P.Rulebook(_tensor(L.coords_in), L.grid, L.spec.ksize, L.spec.stride, L.spec.submanifold)
+        _check_rulebook(L, rb)
+        _check_hash(L.coords_in, L.grid, rb.hash_slots(0))
+        if not L.spec.submanifold:
+            _check_hash(L.coords_out, -(-L.grid // L.spec.stride), rb.hash_slots(1))
+        rb.close()
+
+
+@pytest.mark.parametrize("i", [1, 2, 3, 4, 5])
+def test_synth_matches_oracle(i):
+    spec = CONFIGS[i]
+    for L in layers_of(i):
+        desc = P.layer_desc(L.spec)
+        basis = _tensor(P.basis_build(desc))
+        W = P.synth_kernel(desc, basis, _tensor(L.coeffs), torch.float32).cpu().numpy()
+        kap = L.lay.kappa(L.coeffs)                      # fp64, unrounded
+        assert rel_err(W, kap) < 1e-6
+        if spec.dtype == "bf16":
+            Wb = P.synth_kernel(desc, basis, _tensor(L.coeffs), torch.bfloat16).float().cpu().numpy()
+            assert rel_err(Wb, L.kappa) < 2e-2
+            assert np.abs(Wb - L.kappa).max() <= 2.0 ** -8 * np.abs(L.kappa).max()
+
+
+def _layer_io(i):
+    L = layers_of(i)[0]
+    dt = _dt(i)
+    desc = P.layer_desc(L.spec)
+    basis = _tensor(P.basis_build(desc))
+    coeffs = _tensor(L.coeffs)
+    rb = P.Rulebook(_tensor(L.coords_in), L.grid, L.spec.ksize, L.spec.stride, L.spec.submanifold)
+    W = P.synth_kernel(desc, basis, coeffs, dt)
+    feats = _tensor(features_of(i), dt)
+    return L, dt, desc, basis, rb, W, feats
+
+
+@pytest.mark.parametrize("i", [1, 2, 3, 4])
+def test_forward_matches_oracle(i):
+    print(f"forward config {i}", flush=True)
+    L, dt, desc, basis, rb, W, feats = _layer_io(i)
+    out = P.forward(feats, rb, W).float().cpu().numpy()
+    want, *_ = single_layer_reference(i)
+    err = rel_err(out, want)
+    print(f"config {i} forward rel err {err:.3e}", flush=True)
+    assert err < TOL[CONFIGS[i].dtype]
+    rb.close()
+
+
+@pytest.mark.parametrize("i", [1, 2, 3, 4])
+def test_backward_matches_oracle(i):
+    print(f"backward config {i}", flush=True)
+    L, dt, desc, basis, rb, W, feats = _layer_io(i)
+    _, g, d_in, dw = single_layer_reference(i)
+    gf, gc = P.backward(feats, _tensor(g, dt), rb, W, desc, basis)
+    e1, e2 = rel_err(gf.float().cpu().numpy(), d_in), rel_err(gc.cpu().numpy(), dw)
+    print(f"config {i} grad_feats rel err {e1:.3e} grad_coeffs rel err {e2:.3e}", flush=True)
+    tol = TOL[CONFIGS[i].dtype]
+    assert e1 < tol and e2 < tol
+    rb.close()
+
+
+def test_forward_backward_deterministic():
+    L, dt, desc, basis, rb, W, feats = _layer_io(2)
+    g = torch.randn(rb.n_out, L.spec.cout, device=DEV, generator=torch.Generator(DEV).manual_seed(0))
+    o1 = P.forward(feats, rb, W)
+    o2 = P.forward(feats, rb, W)
+    a1, b1 = P.backward(feats, g, rb, W, desc, basis)
+    a2, b2 = P.backward(feats, g, rb, W, desc, basis)
+    assert torch.equal(o1, o2) and torch.equal(a1, a2) and torch.equal(b1, b2)
+    rb2 = P.Rulebook(_tensor(L.coords_in), L.grid, L.spec.ksize, 1, True)
+    assert torch.equal(rb2.pairs(), rb.pairs())
+    rb.close()
+    rb2.close()
