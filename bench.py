@@ -41,6 +41,11 @@ def parse():
     ap.add_argument("--config", type=int, default=2, help="workload index 1..5 (default: the 64^3 5x5x5 layer)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work to aim for")
+    ap.add_argument("--only", choices=["step", "forward"], default="step",
+                    help="'forward' times the forward gather-GEMM alone over one prebuilt rule book")
+    ap.add_argument("--variant", type=int, default=0, help="gather-GEMM tile-configuration override (tuning)")
+    ap.add_argument("--copy-mb", type=int, default=0,
+                    help="instead of the benchmark, run plain device copies of this many MiB (counter calibration)")
     return ap.parse_args()
 
 
@@ -75,6 +80,21 @@ class SingleLayer:
         rb.close()
         self.ws = torch.empty((ws,), dtype=torch.uint8, device=dev)
         self.fwd_ms = []
+
+    def forward_only(self, timed=False):
+        P, torch = self.P, self.torch
+        if not hasattr(self, "_rb"):
+            L = self.L
+            self._rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, L.stride, L.submanifold)
+            self._W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt)
+            self._out = torch.empty((self.n_out, L.cout), dtype=self.dt, device=self.feats.device)
+        if timed:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+        P.forward(self.feats, self._rb, self._W, out=self._out)
+        if timed:
+            e1.record()
+            self.fwd_events.append((e0, e1))
 
     def step(self, timed=False):
         P, torch, L = self.P, self.torch, self.L
@@ -197,20 +217,35 @@ def main():
         sys.exit(1)
     dev = "cuda:0"
     torch.cuda.set_device(0)
+    if args.copy_mb:
+        n = args.copy_mb * (1 << 20) // 4
+        x = torch.ones(n, device=dev)
+        y = torch.empty_like(x)
+        for _ in range(max(args.steps, 1)):
+            y.copy_(x)
+        torch.cuda.synchronize()
+        log(f"copied {args.copy_mb} MiB x {max(args.steps, 1)}")
+        return
     from workloads import CONFIGS
     spec = CONFIGS[args.config]
+    if args.variant:
+        import paper_2111_07383_amd as P
+        P.debug_set(3, args.variant)
     log(f"setting up {spec.name}")
     b = StackBench(dev) if args.config == 5 else SingleLayer(args.config, dev)
+    if args.only == "forward" and args.config == 5:
+        raise SystemExit("--only forward applies to the single-layer workloads 1-4")
+    run = b.forward_only if args.only == "forward" else b.step
     b.fwd_events = []
     for _ in range(args.warmup):
-        b.step()
+        run()
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} steps); timing {args.steps} steps")
     b.fwd_events = []
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        b.step(timed=True)
+        run(timed=True)
     torch.cuda.synchronize()
     t = time.perf_counter() - t0
     ms = t / args.steps * 1e3
@@ -220,6 +255,9 @@ def main():
     out = {"metric": METRIC, "value": value, "unit": "M active output sites/s", "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": spec.dtype, "data": "synthetic", "config": b.config()}
+    if args.only == "forward":
+        out["metric"] = METRIC + " (forward gather-GEMM only)"
+        out["config"]["step"] = "forward gather-MFMA only (rule book and kernel prebuilt)"
     if b.fwd_events:
         fwd_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in b.fwd_events]))
         flops = b.flops()

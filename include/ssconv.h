@@ -194,7 +194,9 @@ int ssconv_gate_backward(const ssconv_fields* fields /*host*/, const void* x, co
  * Forces failure paths from the host so they can be tested without faulting
  * a device: option 1 = hash capacity (slots) used by the next rule book builds
  * (0 restores automatic sizing); option 2 = make the N-th following device
- * allocation fail (0 disables).  Returns E_INVALID for unknown options. */
+ * allocation fail (0 disables); option 3 = tile-configuration override of the
+ * gather-GEMM kernel for tuning sweeps (0 = automatic choice; results are
+ * identical for every value).  Returns E_INVALID for unknown options. */
 int ssconv_debug_set(int option, int64_t value);
 
 #ifdef __cplusplus

@@ -9,6 +9,7 @@ namespace {
 thread_local std::string g_error;
 std::atomic<int64_t> g_debug_hash_cap{0};
 std::atomic<int64_t> g_debug_fail_alloc{0};
+std::atomic<int64_t> g_debug_gather_variant{0};
 }  // namespace
 
 void set_error(const char* fmt, ...) {
@@ -55,6 +56,7 @@ void dev_free(void* p, hipStream_t stream) {
 }
 
 int64_t debug_hash_capacity() { return g_debug_hash_cap.load(); }
+int64_t debug_gather_variant() { return g_debug_gather_variant.load(); }
 
 int make_fieldtab(const ssconv_fields* f, FieldTab* t) {
   if (!f || f->n < 1 || f->n > SSCONV_MAX_ENTRIES) return fail(SSCONV_E_INVALID, "bad field list");
@@ -90,6 +92,10 @@ extern "C" int ssconv_debug_set(int option, int64_t value) {
   }
   if (option == 2) {
     ssconv::g_debug_fail_alloc.store(value < 0 ? 0 : value);
+    return SSCONV_OK;
+  }
+  if (option == 3) {
+    ssconv::g_debug_gather_variant.store(value < 0 ? 0 : value);
     return SSCONV_OK;
   }
   return ssconv::fail(SSCONV_E_INVALID, "unknown debug option %d", option);

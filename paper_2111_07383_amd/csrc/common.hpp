@@ -37,6 +37,7 @@ int fail(int code, const char* fmt, ...);
 int dev_alloc(void** p, size_t bytes, hipStream_t stream);
 void dev_free(void* p, hipStream_t stream);
 int64_t debug_hash_capacity();
+int64_t debug_gather_variant();
 
 // ---------------------------------------------------------------------------
 // field tables (channel -> field, order, component) passed by value to kernels

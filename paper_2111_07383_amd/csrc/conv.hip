@@ -22,6 +22,7 @@
 #include <algorithm>
 
 #include "conv.hpp"
+#include "gather_mfma.hpp"
 
 namespace ssconv {
 
@@ -284,6 +285,8 @@ int pick_wnb(int cb) {
 template <typename T>
 int dispatch_gg(const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, int64_t n_rows, int K, void* out,
                 hipStream_t st) {
+  const ssconv_dtype dt = sizeof(T) == 4 ? SSCONV_F32 : SSCONV_BF16;
+  if (gather_mfma_supported(dt, ca, cb, K)) return gather_mfma(src, dt, ca, Bt, cb, nbr, nullptr, n_rows, K, out, st);
   switch (pick_wnb(cb)) {
     case 1: launch_gg<T, 1>(src, ca, Bt, cb, nbr, n_rows, K, out, st); break;
     case 2: launch_gg<T, 2>(src, ca, Bt, cb, nbr, n_rows, K, out, st); break;

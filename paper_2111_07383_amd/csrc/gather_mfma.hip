@@ -1,0 +1,367 @@
+// Output-stationary gather -> MFMA GEMM with the reduction dimension flattened over
+// the tile's active kernel offsets (Sec. 3.2.3, Alg. 1 feature update).
+//
+//   out[x] = sum_s kappa(s) in[nbr[s][x]]   for the output rows x of a tile
+//
+// A workgroup of four wavefronts owns BM = 4*WMB*16 output rows and BN = WNB*16
+// output channels.  Its reduction dimension is the concatenation, over the
+// offsets present in its rows, of the Cin input channels of each offset, cut
+// into 32-wide chunks; a chunk may straddle two offsets, so no channel padding
+// is paid per offset.
+//
+// Data movement (gfx950):
+//   * the tile's neighbour indices for every offset are staged in LDS once;
+//   * each chunk of gathered feature rows and of kappa(s) is fetched with
+//     16-byte global->LDS DMA loads (global_load_lds_dwordx4) straight into
+//     MFMA fragment order: lane l of a load lands at byte 16*l of a 1 KB
+//     block, which is exactly the 16 bytes that lane l later feeds the MFMA;
+//   * S stages are in flight; a stage is waited for with s_waitcnt on the
+//     wavefront's own DMA count (every wavefront issues the same number per
+//     stage: absent rows read a zero line, surplus kappa slots load into a
+//     junk block) and published with one barrier per chunk;
+//   * rows without a neighbour at an offset contribute zeros (measured on the
+//     benchmark surfaces, skipping at 16-row granularity would save ~1% of the
+//     MFMA work but costs branches around every MFMA).
+// Every output element is written once (fp32, or rounded to bf16).
+// fp32 uses v_mfma_f32_16x16x4f32 (8 steps per chunk; lane group g = lane/16
+// takes channels 8g..8g+7, one per step), bf16 v_mfma_f32_16x16x32_bf16 (one
+// step; lane group g supplies channels 8g..8g+7).
+#include "gather_mfma.hpp"
+
+namespace ssconv {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+constexpr int kNT = 256;
+constexpr int kBK = 32;
+constexpr int kMaxK = 128;
+constexpr int kLdsLimit = 160 * 1024;
+
+__device__ __attribute__((aligned(64))) const uint4 g_zero_line[4] = {};
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// 16 bytes per lane from global address g into LDS at byte lds + 16 * lane.
+__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane(lds);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(l), "v"(g) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// s_waitcnt vmcnt(n) for a runtime n in [0, 30] (larger n waits for everything).
+__device__ __forceinline__ void wait_vmcnt(int n) {
+#define SSC_W(k) \
+  case k: asm volatile("s_waitcnt vmcnt(" #k ")" ::: "memory"); break;
+  switch (n) {
+    SSC_W(1) SSC_W(2) SSC_W(3) SSC_W(4) SSC_W(5) SSC_W(6) SSC_W(7) SSC_W(8)
+    SSC_W(9) SSC_W(10) SSC_W(11) SSC_W(12) SSC_W(13) SSC_W(14) SSC_W(15) SSC_W(16)
+    SSC_W(17) SSC_W(18) SSC_W(19) SSC_W(20) SSC_W(21) SSC_W(22) SSC_W(23) SSC_W(24)
+    SSC_W(25) SSC_W(26) SSC_W(27) SSC_W(28) SSC_W(29) SSC_W(30)
+    default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+  }
+#undef SSC_W
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt_const() {
+  static_assert(N >= 0 && N <= 30, "vmcnt range");
+  if constexpr (N == 0)
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else
+    wait_vmcnt(N);
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
+
+// acc += A x B for one 32-wide chunk; a and b are this lane's fragment vectors.
+__device__ __forceinline__ void mma_frag(f4& acc, const uint4 (&a)[2], const uint4 (&b)[2]) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[0].x), __uint_as_float(b[0].x), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[0].y), __uint_as_float(b[0].y), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[0].z), __uint_as_float(b[0].z), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[0].w), __uint_as_float(b[0].w), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[1].x), __uint_as_float(b[1].x), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[1].y), __uint_as_float(b[1].y), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[1].z), __uint_as_float(b[1].z), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[1].w), __uint_as_float(b[1].w), acc, 0, 0, 0);
+}
+__device__ __forceinline__ void mma_frag(f4& acc, const uint4 (&a)[1], const uint4 (&b)[1]) {
+  bf16x8 av, bv;
+  __builtin_memcpy(&av, &a[0], 16);
+  __builtin_memcpy(&bv, &b[0], 16);
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc, 0, 0, 0);
+}
+
+template <typename T, int WMB, int WNB, int S>
+struct Shape {
+  static constexpr int BM = 4 * WMB * 16;
+  static constexpr int BN = WNB * 16;
+  static constexpr int VE = 16 / (int)sizeof(T);         // elements per 16-byte vector
+  static constexpr int RV = 8 / VE;                      // 16-byte vectors per lane per chunk
+  static constexpr int BJ = (WNB + 3) / 4;               // kappa blocks loaded per wavefront per chunk
+  static constexpr int ABYTES = 4 * WMB * RV * 1024;     // gathered rows of one stage
+  static constexpr int BBYTES = WNB * RV * 1024;         // kappa chunk of one stage
+  static constexpr int STAGE = ABYTES + BBYTES;
+  static constexpr int L = (WMB + BJ) * RV;              // DMA loads per wavefront per stage
+};
+
+template <typename T, int WMB, int WNB, int S>
+__global__ __launch_bounds__(kNT) void gather_mfma_kernel(const T* __restrict__ src, int ca,
+                                                          const T* __restrict__ Bt, int cb,
+                                                          const int32_t* __restrict__ nbr,
+                                                          const int32_t* __restrict__ order, int64_t n_pos, int K,
+                                                          T* __restrict__ out) {
+  using SH = Shape<T, WMB, WNB, S>;
+  constexpr int BM = SH::BM, RV = SH::RV, VE = SH::VE, BJ = SH::BJ, L = SH::L;
+  // dynamic LDS only (base at LDS address 0): stages | junk | bmask | act | count | index table
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  char* stages = smem;                                                         // S * STAGE bytes
+  char* junk = smem + S * SH::STAGE;                                           // 1 KB sink
+  uint32_t* bmask = reinterpret_cast<uint32_t*>(junk + 1024);                  // [kMaxK]
+  uint8_t* act = reinterpret_cast<uint8_t*>(bmask + kMaxK);                    // [kMaxK]
+  int* n_act_p = reinterpret_cast<int*>(act + kMaxK);                          // [4]
+  int32_t* idx_tab = n_act_p + 4;                                              // [K][BM]
+
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, r16 = lane & 15;
+  const int64_t p0 = (int64_t)blockIdx.x * BM;
+  const int n0 = blockIdx.y * SH::BN;
+
+  // 1. neighbour indices of the tile (all offsets) and the 16-row blocks each offset touches
+  for (int s = w; s < K; s += 4) {
+    uint32_t m = 0;
+#pragma unroll
+    for (int j = 0; j < BM / 64; ++j) {
+      const int64_t p = p0 + 64 * j + lane;
+      const int idx = p < n_pos ? nbr[(int64_t)s * n_pos + p] : -1;
+      idx_tab[s * BM + 64 * j + lane] = idx;
+      const uint64_t b = __ballot(idx >= 0);
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if ((b >> (16 * q)) & 0xffffull) m |= 1u << (4 * j + q);
+    }
+    if (lane == 0) bmask[s] = m;
+  }
+  __syncthreads();
+  // 2. ordered list of the offsets present in the tile
+  if (w == 0) {
+    int base = 0;
+    for (int s0 = 0; s0 < K; s0 += 64) {
+      const int s = s0 + lane;
+      const bool a = s < K && bmask[s] != 0;
+      const uint64_t b = __ballot(a);
+      if (a) act[base + __popcll(b & ((1ull << lane) - 1ull))] = (uint8_t)s;
+      base += __popcll(b);
+    }
+    if (lane == 0) n_act_p[0] = base;
+  }
+  __syncthreads();
+  const int n_act = n_act_p[0];
+  const int total = n_act * ca;
+  const int nchunk = (total + kBK - 1) / kBK;
+
+  // Gather state of this lane group's 8-channel run (flat position c*32 + 8g -> slot, channel):
+  // per 16-row block a source pointer, per kappa slot a source pointer.  They advance by one
+  // chunk per issue and are recomputed only when the run crosses into the next offset.
+  int r_slot = 0, r_ch = 8 * g;
+  while (r_ch >= ca && r_slot < n_act) r_ch -= ca, ++r_slot;
+  const uint32_t stage0 = lds_addr(stages), junk_a = lds_addr(junk);
+  const T* const zero = reinterpret_cast<const T*>(g_zero_line);
+  const T* ap[WMB];
+  const T* bp[BJ];
+  bool alive[WMB], bok[BJ];
+
+#define SSC_REFRESH()                                                                               \
+  do {                                                                                              \
+    const bool live_ = r_slot < n_act;                                                              \
+    const int s_ = live_ ? act[r_slot] : 0;                                                         \
+    _Pragma("unroll") for (int mb = 0; mb < WMB; ++mb) {                                            \
+      const int idx_ = live_ ? idx_tab[s_ * BM + 16 * (w * WMB + mb) + r16] : -1;                   \
+      alive[mb] = idx_ >= 0;                                                                        \
+      ap[mb] = alive[mb] ? src + (int64_t)idx_ * ca + r_ch : zero;                                  \
+    }                                                                                               \
+    _Pragma("unroll") for (int j = 0; j < BJ; ++j) {                                                \
+      const int nb_ = w + 4 * j;                                                                    \
+      const int n_ = n0 + 16 * nb_ + r16;                                                           \
+      bok[j] = nb_ < WNB && live_ && n_ < cb;                                                       \
+      bp[j] = bok[j] ? Bt + ((int64_t)s_ * cb + n_) * ca + r_ch : zero;                             \
+    }                                                                                               \
+  } while (0)
+
+#define SSC_ISSUE(c_)                                                                               \
+  do {                                                                                              \
+    const int st_ = (c_) % S;                                                                       \
+    const uint32_t abase_ = stage0 + st_ * SH::STAGE;                                               \
+    _Pragma("unroll") for (int mb = 0; mb < WMB; ++mb) {                                            \
+      _Pragma("unroll") for (int q = 0; q < RV; ++q)                                                \
+        dma16(ap[mb] + (alive[mb] ? q * VE : 0), abase_ + ((w * WMB + mb) * RV + q) * 1024);        \
+    }                                                                                               \
+    const uint32_t bbase_ = abase_ + SH::ABYTES;                                                    \
+    _Pragma("unroll") for (int j = 0; j < BJ; ++j) {                                                \
+      const int nb_ = w + 4 * j;                                                                    \
+      _Pragma("unroll") for (int q = 0; q < RV; ++q)                                                \
+        dma16(bp[j] + (bok[j] ? q * VE : 0), nb_ < WNB ? bbase_ + (nb_ * RV + q) * 1024 : junk_a);  \
+    }                                                                                               \
+    r_ch += kBK;                                                                                    \
+    if (r_ch >= ca) {                                                                               \
+      while (r_ch >= ca) r_ch -= ca, ++r_slot;                                                      \
+      SSC_REFRESH();                                                                                \
+    } else {                                                                                        \
+      _Pragma("unroll") for (int mb = 0; mb < WMB; ++mb) ap[mb] += alive[mb] ? kBK : 0;             \
+      _Pragma("unroll") for (int j = 0; j < BJ; ++j) bp[j] += bok[j] ? kBK : 0;                     \
+    }                                                                                               \
+  } while (0)
+
+  SSC_REFRESH();
+
+  f4 acc[WMB][WNB];
+#pragma unroll
+  for (int mb = 0; mb < WMB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < WNB; ++nb) acc[mb][nb] = f4{0.f, 0.f, 0.f, 0.f};
+
+  for (int c = 0; c < S - 1 && c < nchunk; ++c) SSC_ISSUE(c);
+  for (int c = 0; c < nchunk; ++c) {
+    // own DMAs of stage c done: later stages may stay in flight (all of them in steady state)
+    if (c + S - 2 < nchunk)
+      wait_vmcnt_const<L * (S - 2)>();
+    else
+      wait_vmcnt_const<0>();
+    __syncthreads();
+    if (c + S - 1 < nchunk) SSC_ISSUE(c + S - 1);
+    const char* sb = stages + (c % S) * SH::STAGE;
+    // every fragment of the chunk is read before the first MFMA, so one LDS round trip
+    // covers the whole chunk; the MFMAs then run back to back on in-place accumulators
+    uint4 af[WMB][RV], bf[WNB][RV];
+#pragma unroll
+    for (int mb = 0; mb < WMB; ++mb)
+#pragma unroll
+      for (int q = 0; q < RV; ++q)
+        af[mb][q] = *reinterpret_cast<const uint4*>(sb + ((w * WMB + mb) * RV + q) * 1024 + 16 * lane);
+#pragma unroll
+    for (int nb = 0; nb < WNB; ++nb)
+#pragma unroll
+      for (int q = 0; q < RV; ++q)
+        bf[nb][q] = *reinterpret_cast<const uint4*>(sb + SH::ABYTES + (nb * RV + q) * 1024 + 16 * lane);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int nb = 0; nb < WNB; ++nb)
+#pragma unroll
+      for (int mb = 0; mb < WMB; ++mb) mma_frag(acc[mb][nb], af[mb], bf[nb]);
+  }
+#undef SSC_ISSUE
+#undef SSC_REFRESH
+
+#pragma unroll
+  for (int mb = 0; mb < WMB; ++mb) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t p = p0 + 16 * (w * WMB + mb) + 4 * g + i;
+      if (p >= n_pos) continue;
+      const int64_t row = order ? order[p] : p;
+      T* orow = out + row * cb;
+#pragma unroll
+      for (int nb = 0; nb < WNB; ++nb) {
+        const int col = n0 + 16 * nb + r16;
+        if (col < cb) orow[col] = DT<T>::from_f(acc[mb][nb][i]);
+      }
+    }
+  }
+}
+
+template <typename T, int WMB, int WNB, int S>
+size_t smem_bytes(int K) {
+  using SH = Shape<T, WMB, WNB, S>;
+  return (size_t)S * SH::STAGE + 1024 + kMaxK * 5 + 16 + (size_t)K * SH::BM * 4;
+}
+
+template <typename T, int WMB, int WNB, int S>
+int launch(const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, const int32_t* order, int64_t n_pos,
+           int K, void* out, hipStream_t st) {
+  using SH = Shape<T, WMB, WNB, S>;
+  const size_t smem = smem_bytes<T, WMB, WNB, S>(K);
+  auto kern = gather_mfma_kernel<T, WMB, WNB, S>;
+  SSC_HIP(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem));
+  dim3 grid(cdiv(n_pos, SH::BM), cdiv(cb, SH::BN));
+  kern<<<grid, kNT, smem, st>>>((const T*)src, ca, (const T*)Bt, cb, nbr, order, n_pos, K, (T*)out);
+  SSC_HIP(hipGetLastError());
+  return SSCONV_OK;
+}
+
+
+// Tile configurations, best first; the first whose LDS footprint fits is used.
+struct Cfg {
+  int wmb, wnb, stages;
+};
+
+template <typename T>
+size_t cfg_smem(const Cfg& c, int K) {
+  const int VE = 16 / (int)sizeof(T), RV = 8 / VE;
+  return (size_t)c.stages * (4 * c.wmb + c.wnb) * RV * 1024 + 1024 + kMaxK * 5 + 16 + (size_t)K * 4 * c.wmb * 16 * 4;
+}
+
+int column_blocks(ssconv_dtype dt, int cb) {
+  const int blocks = (cb + 15) / 16;
+  if (dt == SSCONV_BF16) return blocks <= 4 ? 4 : blocks <= 8 ? 8 : blocks <= 13 ? 13 : 8;
+  const int tiles = (blocks + 7) / 8;
+  return (blocks + tiles - 1) / tiles;  // fp32: at most 8 column blocks per tile
+}
+
+bool pick_cfg(ssconv_dtype dt, int cb, int K, Cfg* out) {
+  const int wnb = column_blocks(dt, cb);
+  const Cfg f32[] = {{2, wnb, 3}, {1, wnb, 2}, {1, wnb, 3}};
+  const Cfg b16[] = {{2, wnb, 3}, {1, wnb, 3}};
+  const Cfg* list = dt == SSCONV_F32 ? f32 : b16;
+  const int n = dt == SSCONV_F32 ? 3 : 2;
+  for (int i = 0; i < n; ++i) {
+    const size_t need = dt == SSCONV_F32 ? cfg_smem<float>(list[i], K) : cfg_smem<uint16_t>(list[i], K);
+    if (need <= (size_t)kLdsLimit) {
+      *out = list[i];
+      return true;
+    }
+  }
+  return false;
+}
+
+template <typename T, int WMB, int S>
+int launch_wnb(int wnb, const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, const int32_t* order,
+               int64_t n_pos, int K, void* out, hipStream_t st) {
+  switch (wnb) {
+    case 1: return launch<T, WMB, 1, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 2: return launch<T, WMB, 2, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 3: return launch<T, WMB, 3, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 4: return launch<T, WMB, 4, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 5: return launch<T, WMB, 5, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 6: return launch<T, WMB, 6, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 7: return launch<T, WMB, 7, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 8: return launch<T, WMB, 8, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    default: return launch<T, WMB, 13, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+  }
+}
+
+}  // namespace
+
+bool gather_mfma_supported(ssconv_dtype dt, int ca, int cb, int K) {
+  Cfg c;
+  return ca % 8 == 0 && ca >= 8 && K <= kMaxK && pick_cfg(dt, cb, K, &c);
+}
+
+int gather_mfma(const void* src, ssconv_dtype dt, int ca, const void* Bt, int cb, const int32_t* nbr,
+                const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st) {
+  if (n_pos == 0) return SSCONV_OK;
+  Cfg c;
+  if (!pick_cfg(dt, cb, K, &c)) return fail(SSCONV_E_INVALID, "no gather tile fits the LDS for K=%d", K);
+  const int64_t variant = debug_gather_variant();
+  if (variant == 1) c.wmb = 1, c.stages = 2;   // tuning override: one row block per wavefront, double buffer
+  if (variant == 2) c.wmb = 1, c.stages = 3;   // tuning override: one row block per wavefront, three stages
+  if (dt == SSCONV_F32) {
+    if (c.wmb == 2) return launch_wnb<float, 2, 3>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    if (c.stages == 2) return launch_wnb<float, 1, 2>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    return launch_wnb<float, 1, 3>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+  }
+  if (c.wmb == 2) return launch_wnb<uint16_t, 2, 3>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+  if (c.stages == 2) return launch_wnb<uint16_t, 1, 2>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+  return launch_wnb<uint16_t, 1, 3>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+}
+
+}  // namespace ssconv

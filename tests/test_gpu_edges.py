@@ -48,7 +48,7 @@ def test_error_codes():
     assert _code(lambda: P.Rulebook(c, 8, 4)) == E_INVALID
     assert _code(lambda: P.Rulebook(c, 8, 3, stride=3, submanifold=False)) == E_INVALID
     big = c.clone()
-    big[:, 0] = 70000                                   # (b+1) * 8^3 exceeds 32 bits
+    big[:, 0] = 9_000_000                               # (b+1) * 8^3 exceeds 2^32
     assert _code(lambda: P.Rulebook(big, 8, 3)) == E_BOUNDS
     P.debug_set(1, 16)                                  # 16 slots for 50 sites
     try:
