@@ -23,6 +23,7 @@
 
 #include "conv.hpp"
 #include "gather_mfma.hpp"
+#include "kgrad_mfma.hpp"
 
 namespace ssconv {
 
@@ -349,7 +350,7 @@ static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout) {
   BwdLayout L;
   const size_t K = rb->K, sz = dtype_bytes(dt);
-  L.nsplit = dw_nsplit(rb);
+  L.nsplit = kgrad_supported(dt, cin, cout) ? kgrad_plan(rb, dt, cin, cout).nsplit : dw_nsplit(rb);
   size_t o = 0;
   L.nbrT = o;
   o += align256(K * (size_t)rb->n_in * 4);
@@ -393,7 +394,9 @@ int conv_backward_dw(const void* feats, const void* grad_out, ssconv_dtype dt, i
   *dW_out = dW;
   const int K = rb->K;
   const int64_t n = (int64_t)K * cin * cout;
-  if (dt == SSCONV_F32)
+  if (kgrad_supported(dt, cin, cout))
+    SSC_TRY(kgrad_partials(grad_out, feats, dt, cin, cout, rb, kgrad_plan(rb, dt, cin, cout), part, st));
+  else if (dt == SSCONV_F32)
     SSC_TRY(dispatch_dw<float>(grad_out, cout, feats, cin, rb->pairs, rb->pair_off_dev, K, L.nsplit, part, st));
   else
     SSC_TRY(dispatch_dw<uint16_t>(grad_out, cout, feats, cin, rb->pairs, rb->pair_off_dev, K, L.nsplit, part, st));
