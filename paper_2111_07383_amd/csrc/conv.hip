@@ -329,10 +329,23 @@ int dispatch_dw(const void* G, int cout, const void* F, int cin, const int32_t* 
 
 }  // namespace
 
+static bool use_bf16_kernel(ssconv_dtype dt, int64_t n_src, int ca, int cb, int K) {
+  return dt == SSCONV_BF16 && debug_gather_variant() != 5 && gather_bf16_supported(n_src, ca, cb, K);
+}
+
 int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_rulebook* rb, const void* W, int cout,
                  void* out, hipStream_t st) {
   if (rb->n_out == 0) return SSCONV_OK;
   if (dt == SSCONV_F32) return dispatch_gg<float>(feats, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st);
+  if (use_bf16_kernel(dt, rb->n_in, cin, cout, rb->K)) {
+    // kappa packed for the bf16 kernel in a stream-ordered scratch buffer
+    void* Bp = nullptr;
+    SSC_TRY(dev_alloc(&Bp, (size_t)rb->K * cin * cout * 2, st));
+    int rc = pack_b_bf16(W, rb->K, cin, cout, false, Bp, st);
+    if (rc == SSCONV_OK) rc = gather_bf16(feats, rb->n_in, cin, Bp, cout, rb->nbr, nullptr, rb->n_out, rb->K, out, st);
+    dev_free(Bp, st);
+    return rc;
+  }
   return dispatch_gg<uint16_t>(feats, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st);
 }
 
@@ -381,6 +394,11 @@ int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout
     transpose_kernel<float><<<cdiv(nw, 256), 256, 0, st>>>((const float*)W, K, cout, cin, (float*)Wt);
     SSC_HIP(hipGetLastError());
     return dispatch_gg<float>(grad_out, cout, Wt, cin, nbrT, rb->n_in, K, grad_feats, st);
+  }
+  if (use_bf16_kernel(dt, rb->n_out, cout, cin, K)) {
+    // kappa^T packed for the bf16 kernel: Bp[s][o/8][i][o%8] = W[s][o][i]
+    SSC_TRY(pack_b_bf16(W, K, cout, cin, true, Wt, st));
+    return gather_bf16(grad_out, rb->n_out, cout, Wt, cin, nbrT, nullptr, rb->n_in, K, grad_feats, st);
   }
   transpose_kernel<uint16_t><<<cdiv(nw, 256), 256, 0, st>>>((const uint16_t*)W, K, cout, cin, (uint16_t*)Wt);
   SSC_HIP(hipGetLastError());

@@ -27,6 +27,7 @@
 // takes channels 8g..8g+7, one per step), bf16 v_mfma_f32_16x16x32_bf16 (one
 // step; lane group g supplies channels 8g..8g+7).
 #include "gather_mfma.hpp"
+#include "lds_dma.hpp"
 
 namespace ssconv {
 namespace {
@@ -41,39 +42,6 @@ constexpr int kLdsLimit = 160 * 1024;
 
 __device__ __attribute__((aligned(64))) const uint4 g_zero_line[4] = {};
 
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-// 16 bytes per lane from global address g into LDS at byte lds + 16 * lane.
-__device__ __forceinline__ void dma16(const void* g, uint32_t lds) {
-  const uint32_t l = __builtin_amdgcn_readfirstlane(lds);
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(l), "v"(g) : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-// s_waitcnt vmcnt(n) for a runtime n in [0, 30] (larger n waits for everything).
-__device__ __forceinline__ void wait_vmcnt(int n) {
-#define SSC_W(k) \
-  case k: asm volatile("s_waitcnt vmcnt(" #k ")" ::: "memory"); break;
-  switch (n) {
-    SSC_W(1) SSC_W(2) SSC_W(3) SSC_W(4) SSC_W(5) SSC_W(6) SSC_W(7) SSC_W(8)
-    SSC_W(9) SSC_W(10) SSC_W(11) SSC_W(12) SSC_W(13) SSC_W(14) SSC_W(15) SSC_W(16)
-    SSC_W(17) SSC_W(18) SSC_W(19) SSC_W(20) SSC_W(21) SSC_W(22) SSC_W(23) SSC_W(24)
-    SSC_W(25) SSC_W(26) SSC_W(27) SSC_W(28) SSC_W(29) SSC_W(30)
-    default: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-  }
-#undef SSC_W
-}
-
-template <int N>
-__device__ __forceinline__ void wait_vmcnt_const() {
-  static_assert(N >= 0 && N <= 30, "vmcnt range");
-  if constexpr (N == 0)
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  else
-    wait_vmcnt(N);
-}
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) { return (uint32_t)(uintptr_t)p; }
 
 // acc += A x B for one 32-wide chunk; a and b are this lane's fragment vectors.
 __device__ __forceinline__ void mma_frag(f4& acc, const uint4 (&a)[2], const uint4 (&b)[2]) {
@@ -224,9 +192,9 @@ __global__ __launch_bounds__(kNT) void gather_mfma_kernel(const T* __restrict__ 
   for (int c = 0; c < nchunk; ++c) {
     // own DMAs of stage c done: later stages may stay in flight (all of them in steady state)
     if (c + S - 2 < nchunk)
-      wait_vmcnt_const<L * (S - 2)>();
+      wait_vm<L * (S - 2)>();
     else
-      wait_vmcnt_const<0>();
+      wait_vm<0>();
     __syncthreads();
     if (c + S - 1 < nchunk) SSC_ISSUE(c + S - 1);
     const char* sb = stages + (c % S) * SH::STAGE;

@@ -13,4 +13,16 @@ bool gather_mfma_supported(ssconv_dtype dt, int ca, int cb, int K);
 int gather_mfma(const void* src, ssconv_dtype dt, int ca, const void* Bt, int cb, const int32_t* nbr,
                 const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st);
 
+// bf16 kernel with 256-row tiles and packed kappa (gather_bf16.hip).
+bool gather_bf16_supported(int64_t n_src, int ca, int cb, int K);
+
+// Bp[s][k/8][n][k%8] (bf16) from Bt[s][n][k] (transposed = false) or from W[s][k][n]
+// (transposed = true), for k < ca, n < cb; ca a multiple of 8.
+int pack_b_bf16(const void* W, int K, int ca, int cb, bool transposed, void* Bp, hipStream_t st);
+
+// out[order ? order[p] : p][:] = sum_s Bt[s] (cb x ca) . src[nbr[s][p]] with Bt given packed as above;
+// src holds n_src rows.
+int gather_bf16(const void* src, int64_t n_src, int ca, const void* Bp, int cb, const int32_t* nbr,
+                const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st);
+
 }  // namespace ssconv

@@ -24,6 +24,7 @@
 #include <algorithm>
 
 #include "kgrad_mfma.hpp"
+#include "lds_dma.hpp"
 
 namespace ssconv {
 namespace {
@@ -34,50 +35,6 @@ typedef short s4 __attribute__((ext_vector_type(4)));
 
 __device__ __attribute__((aligned(64))) const uint4 g_zero16[4] = {};
 
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-__device__ __forceinline__ void dma16(const void* gp, uint32_t lds) {
-  const uint32_t l = __builtin_amdgcn_readfirstlane(lds);
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(l), "v"(gp) : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-// s_waitcnt vmcnt(N) for a compile-time N in [0, 30].
-template <int N>
-__device__ __forceinline__ void wait_vm() {
-  static_assert(N >= 0 && N <= 30, "vmcnt range");
-  if constexpr (N == 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  else if constexpr (N == 1) asm volatile("s_waitcnt vmcnt(1)" ::: "memory");
-  else if constexpr (N == 2) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
-  else if constexpr (N == 3) asm volatile("s_waitcnt vmcnt(3)" ::: "memory");
-  else if constexpr (N == 4) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-  else if constexpr (N == 5) asm volatile("s_waitcnt vmcnt(5)" ::: "memory");
-  else if constexpr (N == 6) asm volatile("s_waitcnt vmcnt(6)" ::: "memory");
-  else if constexpr (N == 7) asm volatile("s_waitcnt vmcnt(7)" ::: "memory");
-  else if constexpr (N == 8) asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
-  else if constexpr (N == 9) asm volatile("s_waitcnt vmcnt(9)" ::: "memory");
-  else if constexpr (N == 10) asm volatile("s_waitcnt vmcnt(10)" ::: "memory");
-  else if constexpr (N == 11) asm volatile("s_waitcnt vmcnt(11)" ::: "memory");
-  else if constexpr (N == 12) asm volatile("s_waitcnt vmcnt(12)" ::: "memory");
-  else if constexpr (N == 13) asm volatile("s_waitcnt vmcnt(13)" ::: "memory");
-  else if constexpr (N == 14) asm volatile("s_waitcnt vmcnt(14)" ::: "memory");
-  else if constexpr (N == 15) asm volatile("s_waitcnt vmcnt(15)" ::: "memory");
-  else if constexpr (N == 16) asm volatile("s_waitcnt vmcnt(16)" ::: "memory");
-  else if constexpr (N == 17) asm volatile("s_waitcnt vmcnt(17)" ::: "memory");
-  else if constexpr (N == 18) asm volatile("s_waitcnt vmcnt(18)" ::: "memory");
-  else if constexpr (N == 19) asm volatile("s_waitcnt vmcnt(19)" ::: "memory");
-  else if constexpr (N == 20) asm volatile("s_waitcnt vmcnt(20)" ::: "memory");
-  else if constexpr (N == 21) asm volatile("s_waitcnt vmcnt(21)" ::: "memory");
-  else if constexpr (N == 22) asm volatile("s_waitcnt vmcnt(22)" ::: "memory");
-  else if constexpr (N == 23) asm volatile("s_waitcnt vmcnt(23)" ::: "memory");
-  else if constexpr (N == 24) asm volatile("s_waitcnt vmcnt(24)" ::: "memory");
-  else if constexpr (N == 25) asm volatile("s_waitcnt vmcnt(25)" ::: "memory");
-  else if constexpr (N == 26) asm volatile("s_waitcnt vmcnt(26)" ::: "memory");
-  else if constexpr (N == 27) asm volatile("s_waitcnt vmcnt(27)" ::: "memory");
-  else if constexpr (N == 28) asm volatile("s_waitcnt vmcnt(28)" ::: "memory");
-  else if constexpr (N == 29) asm volatile("s_waitcnt vmcnt(29)" ::: "memory");
-  else if constexpr (N == 30) asm volatile("s_waitcnt vmcnt(30)" ::: "memory");
-}
 
 __device__ __forceinline__ s4 tr_read(uint32_t lds_byte) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(uintptr_t)lds_byte);
