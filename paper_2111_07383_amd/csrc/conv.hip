@@ -360,17 +360,31 @@ int dw_nsplit(const ssconv_rulebook* rb) {
 
 static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
+// The bf16 kernel gradient cuts the pair lists into work units (about two per compute unit).
+constexpr int kKgradUnits = 512;
+
+static bool use_kgrad_units(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout) {
+  return dt == SSCONV_BF16 && debug_gather_variant() != 6 && kgrad_supported(dt, cin, cout) && rb->K <= kKgradMaxK &&
+         (int64_t)rb->n_in * cin * 2 < ((int64_t)1 << 31) && (int64_t)rb->n_out * cout * 2 < ((int64_t)1 << 31);
+}
+
 BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout) {
   BwdLayout L;
   const size_t K = rb->K, sz = dtype_bytes(dt);
-  L.nsplit = kgrad_supported(dt, cin, cout) ? kgrad_plan(rb, dt, cin, cout).nsplit : dw_nsplit(rb);
+  size_t nparts;  // fp32 partial tiles of cout x cin
+  if (use_kgrad_units(rb, dt, cin, cout)) {
+    nparts = (size_t)kgrad_units(rb, kKgradUnits).nunits;
+  } else {
+    L.nsplit = kgrad_supported(dt, cin, cout) ? kgrad_plan(rb, dt, cin, cout).nsplit : dw_nsplit(rb);
+    nparts = (size_t)L.nsplit * K;
+  }
   size_t o = 0;
   L.nbrT = o;
   o += align256(K * (size_t)rb->n_in * 4);
   L.Wt = o;
   o += align256(K * (size_t)cin * cout * sz);
   L.part = o;
-  o += align256((size_t)L.nsplit * K * cin * cout * 4);
+  o += align256(nparts * cin * cout * 4);
   L.dW = o;
   o += align256(K * (size_t)cin * cout * 4);
   L.total = o;
@@ -412,6 +426,11 @@ int conv_backward_dw(const void* feats, const void* grad_out, ssconv_dtype dt, i
   *dW_out = dW;
   const int K = rb->K;
   const int64_t n = (int64_t)K * cin * cout;
+  if (use_kgrad_units(rb, dt, cin, cout)) {
+    const KgradUnits units = kgrad_units(rb, kKgradUnits);
+    SSC_TRY(kgrad_bf16(grad_out, rb->n_out, feats, rb->n_in, cin, cout, rb, units, part, st));
+    return reduce_units(part, units, (int64_t)cin * cout, dW, st);
+  }
   if (kgrad_supported(dt, cin, cout))
     SSC_TRY(kgrad_partials(grad_out, feats, dt, cin, cout, rb, kgrad_plan(rb, dt, cin, cout), part, st));
   else if (dt == SSCONV_F32)

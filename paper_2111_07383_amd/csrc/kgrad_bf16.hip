@@ -1,0 +1,343 @@
+// bf16 gradient of the kernel tensor (the adjoint of Alg. 1's feature update):
+//
+//   dkappa(s)[o][i] = sum_{(x, y) in R_s} grad_out[x][o] * feats[y][i]
+//
+// a GEMM per offset whose reduction runs over the compact pair list R_s.  The pair lists of
+// all offsets are cut into work units of about equal length (several per offset, so that the
+// units fill the chip evenly); each workgroup computes one (32W x 32W) tile of one offset over
+// one unit and writes its own fp32 partial, and the partials of an offset are summed in a
+// fixed order afterwards (deterministic, no atomics).
+//
+// v_mfma_f32_16x16x32_bf16 takes 8 consecutive PAIRS of one channel per lane, the transpose of
+// the row layout.  Rows of 32 pairs are DMA'd into LDS row-major (buffer_load ... lds on 32-bit
+// row offsets: the tail of a unit reads past the end of the buffer, which writes zeros) and the
+// operands are read with ds_read_b64_tr_b16: within a 16-lane group, output lane i / slot j
+// receives element i%4 of the 8 bytes addressed by source lane 4j + i/4, so source lane L
+// pointing at row (base + L/4), channel (c0 + 4*(L%4)) delivers pairs base..base+3 of channel
+// c0 + i; two such reads form one operand.  Rows are padded by one 16-byte granule so that the
+// four rows of a read fall in different banks.
+//
+// Pipeline (four LDS stages): iteration c waits for its own DMAs of chunk c+1, publishes them
+// with one barrier, then runs the MFMAs of chunk c with the transpose reads of chunk c+1, the
+// pair-table reads and the DMAs of chunk c+3 spread between them.  The unit's pair indices are
+// staged in LDS in blocks of 1024, double-buffered and DMA'd one block ahead.
+#include <algorithm>
+
+#include "kgrad_mfma.hpp"
+#include "lds_dma.hpp"
+
+namespace ssconv {
+namespace {
+
+typedef float f4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short s4 __attribute__((ext_vector_type(4)));
+
+constexpr uint32_t kAbsent = 0x80000000u;  // row offset past any buffer: the DMA writes zeros
+constexpr int kBufferWord3 = 0x00020000;   // buffer descriptor word 3 for gfx9-family raw loads
+constexpr int kS = 4;                      // LDS stages
+constexpr int kPBLK = 1024;                // pair indices per staged block
+
+template <int W>
+struct KB {
+  static constexpr int TW = 32 * W;                 // tile width in channels (each side)
+  static constexpr int GR = TW / 8;                 // 16-byte granules of one row segment
+  static constexpr int RS = GR + 1;                 // granules per LDS row (one pad granule)
+  static constexpr int NDMA = (32 * RS + 63) / 64;  // DMA instructions per operand per stage
+  static constexpr int OPB = NDMA * 1024;           // bytes per operand per stage
+  static constexpr int STAGE = 2 * OPB;
+  static constexpr int PW = (2 * NDMA + 3) / 4;     // row DMAs per wavefront per stage
+  static constexpr int SMEM = kS * STAGE + 1024 + 2 * kPBLK * 8;
+};
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void dma16_buf(__amdgpu_buffer_rsrc_t rsrc, uint32_t off, uint32_t lds) {
+  const uint32_t l = __builtin_amdgcn_readfirstlane(lds);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(l), "v"(off), "s"(rsrc)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+__device__ __forceinline__ s4 tr_read(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) s4*)(uintptr_t)lds_addr(p));
+}
+
+template <int W>
+__global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restrict__ G, int64_t g_rows, int cout,
+                                                         const uint16_t* __restrict__ F, int64_t f_rows, int cin,
+                                                         const int2* __restrict__ pairs,
+                                                         const int64_t* __restrict__ pair_off, KgradUnits units,
+                                                         int mtiles, int ntiles, float* __restrict__ part) {
+  using C = KB<W>;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  char* stages = smem;
+  char* junk = smem + kS * C::STAGE;
+  int2* pblk = reinterpret_cast<int2*>(junk + 1024);  // [2][kPBLK]
+  const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, r16 = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = w >> 1, wn = w & 1;
+
+  // work unit -> (offset s, slice of R_s), tile (mt, nt)
+  const int tile = blockIdx.x % (mtiles * ntiles);
+  const int u = blockIdx.x / (mtiles * ntiles);
+  int s = 0;
+  while (s + 1 < units.K && units.uoff[s + 1] <= u) ++s;
+  const int j = u - units.uoff[s], ns = units.uoff[s + 1] - units.uoff[s];
+  const int nt = tile % ntiles, mt = tile / ntiles;
+  const int m0 = mt * C::TW, n0 = nt * C::TW;
+  const int64_t off = pair_off[s], cnt = pair_off[s + 1] - off;
+  const int64_t beg = off + cnt * j / ns, end = off + cnt * (j + 1) / ns;
+  const int npairs = (int)(end - beg);
+  const int nchunk = (npairs + 31) / 32;
+
+  const __amdgpu_buffer_rsrc_t g_rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(G), (short)0, (int)(g_rows * cout * 2), kBufferWord3);
+  const __amdgpu_buffer_rsrc_t f_rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(F), (short)0, (int)(f_rows * cin * 2), kBufferWord3);
+  // the unit's pair list as a byte buffer (past its end: zeros, i.e. row 0 -- masked below)
+  const __amdgpu_buffer_rsrc_t p_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int2*>(pairs + beg), (short)0, npairs * 8, kBufferWord3);
+  const uint32_t stage0 = lds_addr(stages), junk_a = lds_addr(junk), pblk_a = lds_addr(pblk);
+
+  // Row-DMA duty of this wavefront (q < PW): DMA d = w + 4q of the stage covers operand
+  // d / NDMA (0: grad_out, 1: feats) slots (d % NDMA) * 64 + lane = row * RS + granule.
+  int rowq[C::PW];
+  uint32_t goff[C::PW], pent[C::PW];
+  bool liveq[C::PW];
+#pragma unroll
+  for (int q = 0; q < C::PW; ++q) {
+    const int d = w + 4 * q;
+    const bool isF = d >= C::NDMA;
+    const int slot = (isF ? d - C::NDMA : d) * 64 + lane;
+    const int row = slot / C::RS, gran = slot % C::RS;
+    rowq[q] = row < 32 ? row : 0;
+    liveq[q] = d < 2 * C::NDMA && row < 32 && gran < C::GR;
+    pent[q] = (uint32_t)rowq[q] * 8u + (isF ? 4u : 0u);  // byte offset of this lane's index in a chunk's 32 pairs
+    goff[q] = (uint32_t)((isF ? n0 : m0) + 8 * gran) * 2u;
+  }
+
+  // pair block b (slice pairs [b*kPBLK, (b+1)*kPBLK)) into buffer b % 2: 8 KB per block, two
+  // 1 KB DMAs per wavefront
+#define SSK_PAIRS(b_)                                                                               \
+  do {                                                                                              \
+    _Pragma("unroll") for (int i_ = 0; i_ < 2; ++i_) {                                              \
+      const int blk_ = w + 4 * i_;                                                                  \
+      dma16_buf(p_rsrc, (uint32_t)((b_) * kPBLK * 8 + blk_ * 1024 + 16 * lane),                     \
+                pblk_a + ((b_) & 1) * kPBLK * 8 + blk_ * 1024);                                     \
+    }                                                                                               \
+  } while (0)
+
+  // row index (into grad_out or feats, -1: none) of row DMA q of chunk c_, from the pair table.
+  // Pair k = c_*32 + row of the slice sits in buffer (c_ / 32) % 2 at entry (c_ % 32)*32 + row
+  // (32 chunks per block): a wave-uniform base plus this lane's constant pent[q].
+#define SSK_PAIR(dst_, q_, c_)                                                                      \
+  do {                                                                                              \
+    const uint32_t pb_ = pblk_a + ((uint32_t)(c_) >> 5 & 1u) * (kPBLK * 8) + ((uint32_t)(c_) & 31u) * 256u; \
+    const int v_ = *reinterpret_cast<const int*>(smem + (pb_ - lds_addr(smem)) + pent[q_]);         \
+    dst_ = (liveq[q_] && rowq[q_] < npairs - (c_) * 32) ? v_ : -1;                                  \
+  } while (0)
+
+  // row DMA q into stage k_ of the row pr_ (from SSK_PAIR)
+#define SSK_DMA(q_, pr_, k_)                                                                        \
+  do {                                                                                              \
+    const int d_ = w + 4 * (q_);                                                                    \
+    const bool isF_ = d_ >= C::NDMA;                                                                \
+    const int dd_ = isF_ ? d_ - C::NDMA : d_;                                                       \
+    const uint32_t o_ = (pr_) >= 0 ? (uint32_t)(pr_) * (uint32_t)((isF_ ? cin : cout) * 2) + goff[q_] : kAbsent; \
+    dma16_buf(isF_ ? f_rsrc : g_rsrc, o_,                                                           \
+              d_ < 2 * C::NDMA ? stage0 + (k_) * C::STAGE + (isF_ ? C::OPB : 0) + dd_ * 1024 : junk_a); \
+  } while (0)
+
+  // operands of the chunk in stage k_ via transpose reads: row base 8g + 4h + L/4, column 4(L%4)
+  const int rsel = 8 * g + (r16 >> 2), csel = 4 * (r16 & 3);
+#define SSK_READ(da_, db_, i_, k_)                                                                  \
+  do {                                                                                              \
+    const char* sb_ = stages + (k_) * C::STAGE;                                                     \
+    const int ca_ = (wm * W + (i_)) * 16 + csel, cb_ = (wn * W + (i_)) * 16 + csel;                 \
+    const s4 a0_ = tr_read(sb_ + (rsel * C::RS) * 16 + ca_ * 2);                                    \
+    const s4 a1_ = tr_read(sb_ + ((rsel + 4) * C::RS) * 16 + ca_ * 2);                              \
+    const s4 b0_ = tr_read(sb_ + C::OPB + (rsel * C::RS) * 16 + cb_ * 2);                           \
+    const s4 b1_ = tr_read(sb_ + C::OPB + ((rsel + 4) * C::RS) * 16 + cb_ * 2);                     \
+    da_[i_] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0_, a1_, 0, 1, 2, 3, 4, 5, 6, 7)); \
+    db_[i_] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(b0_, b1_, 0, 1, 2, 3, 4, 5, 6, 7)); \
+  } while (0)
+
+  // Accumulators start at zero through a value the compiler cannot fold (npairs >= 0), each from
+  // its own expression: a single shared zero makes the register allocator merge the initial
+  // accumulators and then copy them apart on every path into the chunk loop.
+  f4 acc[W][W];
+  {
+    const float z = __uint_as_float((uint32_t)__builtin_amdgcn_readfirstlane(npairs < 0 ? 1 : 0));
+#pragma unroll
+    for (int i = 0; i < W; ++i)
+#pragma unroll
+      for (int jj = 0; jj < W; ++jj) {
+        const float zi = z * (float)(i * W + jj + 1);
+        acc[i][jj] = f4{zi, zi, zi, zi};
+      }
+  }
+
+  constexpr int L = C::PW;  // row DMAs per wavefront per chunk (pair-block DMAs only add to waits)
+  const int nblk = (npairs + kPBLK - 1) / kPBLK;
+  // prologue: pair blocks 0 and 1, then the rows of chunks 0..2
+  if (nblk > 0) SSK_PAIRS(0);
+  if (nblk > 1) SSK_PAIRS(1);
+  wait_vm<0>();
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < kS - 1; ++c)
+    if (c < nchunk) {
+#pragma unroll
+      for (int q = 0; q < L; ++q) {
+        int pr;
+        SSK_PAIR(pr, q, c);
+        SSK_DMA(q, pr, c);
+      }
+    }
+
+#define SSK_BODY(k_, AC, BC, AN, BN)                                                                \
+  if (c + (k_) < nchunk) {                                                                          \
+    const int cc_ = c + (k_);                                                                       \
+    if (cc_ + kS - 2 < nchunk)                                                                      \
+      wait_vm<(kS - 3) * L>();                                                                      \
+    else                                                                                            \
+      wait_vm<0>();                                                                                 \
+    __syncthreads();                                                                                \
+    const bool rd_ = cc_ + 1 < nchunk;                                                              \
+    const int ci_ = cc_ + kS - 1; /* chunk whose rows are issued now */                             \
+    const bool iss_ = ci_ < nchunk;                                                                 \
+    /* entering pair block b at the issue side: block b+1 goes into the other buffer, whose */      \
+    /* entries (block b-1) were all read by issues before this iteration's barrier */               \
+    if (iss_ && (ci_ % (kPBLK / 32)) == 0 && ci_ / (kPBLK / 32) + 1 < nblk)                         \
+      SSK_PAIRS(ci_ / (kPBLK / 32) + 1);                                                            \
+    constexpr int ks_ = ((k_) + kS - 1) % kS, kr_ = ((k_) + 1) % kS;                                \
+    int prq_[L];                                                                                    \
+    _Pragma("unroll") for (int q = 0; q < L; ++q) SSK_PAIR(prq_[q], q, ci_);                        \
+    __builtin_amdgcn_sched_barrier(0);                                                              \
+    _Pragma("unroll") for (int i = 0; i < W; ++i) {                                                 \
+      _Pragma("unroll") for (int jj = 0; jj < W; ++jj)                                              \
+        acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(AC[i], BC[jj], acc[i][jj], 0, 0, 0);   \
+      __builtin_amdgcn_sched_barrier(0);                                                            \
+      if (rd_) SSK_READ(AN, BN, i, kr_);                                                            \
+      _Pragma("unroll") for (int q = (i * L) / W; q < ((i + 1) * L) / W; ++q)                       \
+        if (iss_) SSK_DMA(q, prq_[q], ks_);                                                         \
+      __builtin_amdgcn_sched_barrier(0);                                                            \
+    }                                                                                               \
+  }
+
+  bf16x8 a0[W], b0[W], a1[W], b1[W];
+  if (nchunk > 0) {
+    if (nchunk > 2) wait_vm<2 * L>(); else wait_vm<0>();
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < W; ++i) SSK_READ(a0, b0, i, 0);
+  }
+  static_assert(kS == 4, "the unrolled chunk loop is written for four stages");
+  for (int c = 0; c < nchunk; c += kS) {
+    SSK_BODY(0, a0, b0, a1, b1)
+    SSK_BODY(1, a1, b1, a0, b0)
+    SSK_BODY(2, a0, b0, a1, b1)
+    SSK_BODY(3, a1, b1, a0, b0)
+  }
+#undef SSK_BODY
+#undef SSK_READ
+#undef SSK_DMA
+#undef SSK_PAIR
+#undef SSK_PAIRS
+
+  float* dst = part + (int64_t)u * cout * cin;
+#pragma unroll
+  for (int i = 0; i < W; ++i)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int m = m0 + (wm * W + i) * 16 + 4 * g + e;
+      if (m >= cout) continue;
+#pragma unroll
+      for (int jj = 0; jj < W; ++jj) {
+        const int n = n0 + (wn * W + jj) * 16 + r16;
+        if (n < cin) dst[(int64_t)m * cin + n] = acc[i][jj][e];
+      }
+    }
+}
+
+__global__ void reduce_units_kernel(const float* __restrict__ part, KgradUnits units, int64_t n,
+                                    float* __restrict__ dW) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int s = blockIdx.y;
+  if (e >= n) return;
+  float acc = 0.f;
+  for (int u = units.uoff[s]; u < units.uoff[s + 1]; ++u) acc += part[(int64_t)u * n + e];
+  dW[(int64_t)s * n + e] = acc;
+}
+
+}  // namespace
+
+KgradUnits kgrad_units(const ssconv_rulebook* rb, int want) {
+  KgradUnits u;
+  u.K = rb->K;
+  const int K = rb->K;
+  int64_t total = 0;
+  for (int s = 0; s < K; ++s) total += rb->pair_off[s + 1] - rb->pair_off[s];
+  want = std::max(want, K);
+  int n[kKgradMaxK];
+  double rem[kKgradMaxK];
+  int sum = 0;
+  for (int s = 0; s < K; ++s) {
+    const double quota = total > 0 ? (double)(rb->pair_off[s + 1] - rb->pair_off[s]) * want / (double)total : 0.0;
+    n[s] = std::max(1, (int)quota);
+    rem[s] = quota - n[s];
+    sum += n[s];
+  }
+  while (sum < want) {  // largest remainders first
+    int best = 0;
+    for (int s = 1; s < K; ++s)
+      if (rem[s] > rem[best]) best = s;
+    if (rem[best] <= 0.0) break;
+    ++n[best];
+    rem[best] -= 1.0;
+    ++sum;
+  }
+  u.uoff[0] = 0;
+  for (int s = 0; s < K; ++s) u.uoff[s + 1] = u.uoff[s] + n[s];
+  u.nunits = u.uoff[K];
+  return u;
+}
+
+int reduce_units(const float* part, const KgradUnits& units, int64_t n, float* dW, hipStream_t st) {
+  if (n == 0 || units.K == 0) return SSCONV_OK;
+  dim3 grid(cdiv(n, 256), units.K);
+  reduce_units_kernel<<<grid, 256, 0, st>>>(part, units, n, dW);
+  SSC_HIP(hipGetLastError());
+  return SSCONV_OK;
+}
+
+int kgrad_bf16_tile(int cin, int cout) {
+  const int need = (std::max(cout, cin) + 31) / 32;
+  return need <= 2 ? 2 : need <= 4 ? 4 : 7;
+}
+
+int kgrad_bf16(const void* grad_out, int64_t n_out, const void* feats, int64_t n_in, int cin, int cout,
+               const ssconv_rulebook* rb, const KgradUnits& units, float* part, hipStream_t st) {
+  if (units.nunits == 0) return SSCONV_OK;
+  const int W = kgrad_bf16_tile(cin, cout);
+  const int mtiles = (cout + 32 * W - 1) / (32 * W), ntiles = (cin + 32 * W - 1) / (32 * W);
+  dim3 grid((unsigned)(units.nunits * mtiles * ntiles));
+  const int2* pairs = reinterpret_cast<const int2*>(rb->pairs);
+#define SSK_LAUNCH(Wv)                                                                              \
+  do {                                                                                              \
+    auto kern = kgrad_bf16_kernel<Wv>;                                                              \
+    SSC_HIP(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, KB<Wv>::SMEM)); \
+    kern<<<grid, 256, KB<Wv>::SMEM, st>>>((const uint16_t*)grad_out, n_out, cout, (const uint16_t*)feats, n_in, \
+                                          cin, pairs, rb->pair_off_dev, units, mtiles, ntiles, part);  \
+  } while (0)
+  if (W == 2) SSK_LAUNCH(2);
+  else if (W == 4) SSK_LAUNCH(4);
+  else SSK_LAUNCH(7);
+#undef SSK_LAUNCH
+  SSC_HIP(hipGetLastError());
+  return SSCONV_OK;
+}
+
+}  // namespace ssconv

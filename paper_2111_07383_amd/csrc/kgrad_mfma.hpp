@@ -18,6 +18,29 @@ inline bool kgrad_supported(ssconv_dtype dt, int cin, int cout) {
 
 KgradPlan kgrad_plan(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout);
 
+// Work units of the bf16 kernel gradient: offset s owns units uoff[s] .. uoff[s+1]-1, which cut
+// its pair list R_s into near-equal slices (passed to the kernels by value).
+constexpr int kKgradMaxK = 125;  // ksize <= 5
+struct KgradUnits {
+  int K = 0, nunits = 0;
+  int uoff[kKgradMaxK + 1] = {};
+};
+
+// Units for the rule book: about `want` in total (at least one per offset), distributed over the
+// offsets in proportion to their pair counts (largest remainders).
+KgradUnits kgrad_units(const ssconv_rulebook* rb, int want);
+
+// bf16 tile width (in 32-channel steps of the 2x2 wavefront grid) for cin x cout.
+int kgrad_bf16_tile(int cin, int cout);
+
+// part[u][o][i] (fp32) = sum over unit u's slice of R_s of grad_out[x][o] feats[y][i]; grad_out
+// holds n_out rows, feats n_in rows.
+int kgrad_bf16(const void* grad_out, int64_t n_out, const void* feats, int64_t n_in, int cin, int cout,
+               const ssconv_rulebook* rb, const KgradUnits& units, float* part, hipStream_t st);
+
+// dW[s][:] = sum over the units of offset s of part[u][:] (n = cout * cin per unit), fixed order.
+int reduce_units(const float* part, const KgradUnits& units, int64_t n, float* dW, hipStream_t st);
+
 // part[split][s][o][i] (fp32) = sum over the split's slice of R_s of grad_out[x][o] feats[y][i].
 int kgrad_partials(const void* grad_out, const void* feats, ssconv_dtype dt, int cin, int cout,
                    const ssconv_rulebook* rb, const KgradPlan& p, float* part, hipStream_t st);

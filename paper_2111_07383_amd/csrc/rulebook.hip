@@ -11,6 +11,8 @@
 //               is deterministic: grouped by s, output rows ascending.
 // Dilated / strided output sets are marked in a bitmap over the output grid
 // and emitted in lexicographic (b, x, y, z) order by a scan of popcounts.
+#include <algorithm>
+
 #include "scan.hpp"
 
 namespace ssconv {
@@ -69,11 +71,21 @@ __global__ void fill_u64(uint64_t* __restrict__ p, int64_t n, uint64_t v) {
   if (i < n) p[i] = v;
 }
 
-__global__ void hash_insert_kernel(const int32_t* __restrict__ c, int64_t n, int g0, int g1, int g2,
+// Inserts every site; a site outside the grid, with b < 0 or with b > bmax (the largest batch
+// index whose keys fit 32 bits) is not inserted and raises kFlagBounds (one atomic per
+// wavefront that holds such a site).
+__global__ void hash_insert_kernel(const int32_t* __restrict__ c, int64_t n, int g0, int g1, int g2, int bmax,
                                    uint64_t* __restrict__ slots, uint64_t mask, int* __restrict__ flags) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
-  int4 v = reinterpret_cast<const int4*>(c)[i];
+  int4 v = make_int4(0, 0, 0, 0);
+  bool bad = false;
+  if (i < n) {
+    v = reinterpret_cast<const int4*>(c)[i];
+    bad = (v.x < 0) | (v.x > bmax) | (v.y < 0) | (v.y >= g0) | (v.z < 0) | (v.z >= g1) | (v.w < 0) | (v.w >= g2);
+  }
+  const uint64_t any_bad = __ballot(bad);
+  if (any_bad && (threadIdx.x & 63) == __ffsll((unsigned long long)any_bad) - 1) atomicOr(flags, kFlagBounds);
+  if (i >= n || bad) return;
   uint32_t key = site_key(v.x, v.y, v.z, v.w, g0, g1, g2);
   uint64_t item = ((uint64_t)key << 32) | (uint32_t)i;
   uint64_t pos = mix32(key) & mask;
@@ -236,6 +248,13 @@ struct Scratch {
   }
 };
 
+// largest batch index whose site keys ((b*G0 + x)*G1 + y)*G2 + z fit in 32 bits (key ~0 is reserved)
+static int max_batch(const int* g) {
+  const int64_t cells = (int64_t)g[0] * g[1] * g[2];
+  const int64_t m = 0xFFFFFFFFll / cells - 1;
+  return (int)std::min<int64_t>(m, 0x7fffffff);
+}
+
 static int build_hash(const int32_t* coords, int64_t n, const int* g, hipStream_t st, uint64_t** slots,
                       int64_t* cap, int* flags) {
   int64_t c = debug_hash_capacity();
@@ -244,7 +263,9 @@ static int build_hash(const int32_t* coords, int64_t n, const int* g, hipStream_
   *cap = c;
   SSC_TRY(dev_alloc((void**)slots, (size_t)c * 8, st));
   fill_u64<<<cdiv(c, 256), 256, 0, st>>>(*slots, c, kEmpty);
-  if (n > 0) hash_insert_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, g[0], g[1], g[2], *slots, (uint64_t)(c - 1), flags);
+  if (n > 0)
+    hash_insert_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, g[0], g[1], g[2], max_batch(g), *slots,
+                                                     (uint64_t)(c - 1), flags);
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;
 }
@@ -271,16 +292,17 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
   SSC_TRY(tmp.alloc((void**)&dflags, 64));
   SSC_HIP(hipMemsetAsync(dflags, 0, 4, st));
   SSC_HIP(hipMemsetAsync(dflags + 1, 0xff, 4, st));  // max b = -1
-  if (n > 0) validate_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, grid[0], grid[1], grid[2], dflags, dflags + 1);
-  SSC_HIP(hipGetLastError());
-  SSC_HIP(hipMemcpyAsync(host, dflags, 8, hipMemcpyDeviceToHost, st));
-  SSC_HIP(hipStreamSynchronize(st));
-  const int flags0 = ((int*)host)[0], maxb = ((int*)host)[1];
-  if (flags0 & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid or has b < 0");
-  const int64_t cells = (int64_t)grid[0] * grid[1] * grid[2];
-  if ((int64_t)(maxb + 1) * cells > 0xFFFFFFFFll)
-    return fail(SSCONV_E_BOUNDS, "(max b + 1) * grid volume exceeds the 32-bit key space");
-  rb->nbatch = maxb + 1;
+  if (!submanifold) {
+    // the output bitmap spans the batch: its extent is needed on the host before the next launch
+    if (n > 0) validate_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, grid[0], grid[1], grid[2], dflags, dflags + 1);
+    SSC_HIP(hipGetLastError());
+    SSC_HIP(hipMemcpyAsync(host, dflags, 8, hipMemcpyDeviceToHost, st));
+    SSC_HIP(hipStreamSynchronize(st));
+    const int flags0 = ((int*)host)[0], maxb = ((int*)host)[1];
+    if (flags0 & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid or has b < 0");
+    if (maxb > max_batch(grid)) return fail(SSCONV_E_BOUNDS, "(max b + 1) * grid volume exceeds the 32-bit key space");
+    rb->nbatch = maxb + 1;
+  }
 
   SSC_TRY(build_hash(coords, n, rb->grid, st, &rb->hash_in, &rb->cap_in, dflags));
 
@@ -342,23 +364,35 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     SSC_HIP(hipGetLastError());
     SSC_TRY(exclusive_scan(counts, ncnt, offs, dtotal, stmp, st));
     gather_offsets<<<1, 256, 0, st>>>(offs, K, nblk, dtotal, rb->pair_off_dev);
+    // the pair lists are written at their upper bound (every output has at most K neighbours), so
+    // the write pass follows without a round trip to the host and the counts come back once,
+    // below; past 1 GB the exact size is read back first
+    const size_t bound = (size_t)K * n_out * 8;
+    if (bound <= ((size_t)1 << 30)) {
+      SSC_TRY(dev_alloc((void**)&rb->pairs, bound, st));
+    } else {
+      SSC_HIP(hipMemcpyAsync(host, dtotal, 8, hipMemcpyDeviceToHost, st));
+      SSC_HIP(hipStreamSynchronize(st));
+      SSC_TRY(dev_alloc((void**)&rb->pairs, (size_t)host[0] * 8, st));
+    }
+    probe_kernel<false><<<gp, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0], grid[1], grid[2],
+                                           rb->hash_in, (uint64_t)(rb->cap_in - 1), rb->nbr, nullptr, offs, rb->pairs);
+    SSC_HIP(hipGetLastError());
     SSC_HIP(hipMemcpyAsync(host, rb->pair_off_dev, (size_t)(K + 1) * 8, hipMemcpyDeviceToHost, st));
     SSC_HIP(hipMemcpyAsync(host + K + 1, dflags, 4, hipMemcpyDeviceToHost, st));
     SSC_HIP(hipStreamSynchronize(st));
     for (int s = 0; s <= K; ++s) rb->pair_off[s] = host[s];
     rb->n_pairs = host[K];
     const int fl = (int)(host[K + 1] & 0xffffffff);
+    if (fl & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid, has b < 0, or (max b + 1) * grid volume exceeds the 32-bit key space");
     if (fl & kFlagDup) return fail(SSCONV_E_DUPLICATE, "duplicate input site");
     if (fl & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
-    SSC_TRY(dev_alloc((void**)&rb->pairs, (size_t)rb->n_pairs * 8, st));
-    probe_kernel<false><<<gp, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0], grid[1], grid[2],
-                                           rb->hash_in, (uint64_t)(rb->cap_in - 1), rb->nbr, nullptr, offs, rb->pairs);
-    SSC_HIP(hipGetLastError());
   } else {
     SSC_HIP(hipMemsetAsync(rb->pair_off_dev, 0, (size_t)(K + 1) * 8, st));
     SSC_HIP(hipMemcpyAsync(host, dflags, 4, hipMemcpyDeviceToHost, st));
     SSC_HIP(hipStreamSynchronize(st));
     const int fl = (int)(host[0] & 0xffffffff);
+    if (fl & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid, has b < 0, or (max b + 1) * grid volume exceeds the 32-bit key space");
     if (fl & kFlagDup) return fail(SSCONV_E_DUPLICATE, "duplicate input site");
     if (fl & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
     SSC_TRY(dev_alloc((void**)&rb->pairs, 8, st));
