@@ -33,6 +33,117 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+# ---------------------------------------------------------------------------
+# HBM traffic of the gather-GEMM kernel from rocprofv3 counter runs
+# ---------------------------------------------------------------------------
+CSRC = os.path.join(ROOT, "paper_2111_07383_amd", "csrc")
+# kernel symbol and the source files that decide its device code, per compute dtype
+GATHER_KERNEL = {"bf16": ("gather_bf16_kernel", ["gather_bf16.hip", "lds_dma.hpp", "gather_mfma.hpp", "common.hpp"]),
+                 "f32": ("gather_mfma_kernel", ["gather_mfma.hip", "lds_dma.hpp", "gather_mfma.hpp", "common.hpp"])}
+COPY_KERNEL = "__amd_rocclr_copyBuffer"
+
+
+def kernel_name(dtype):
+    return GATHER_KERNEL[dtype][0]
+
+
+def kernel_source_hash(dtype):
+    import hashlib
+    h = hashlib.sha256()
+    for f in GATHER_KERNEL[dtype][1]:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_path(spec):
+    return os.path.join(ROOT, "profiles", f"traffic_{kernel_name(spec.dtype)}_{spec.name}.txt")
+
+
+def traffic_from_summary(spec):
+    """HBM bytes per gather-GEMM launch from the committed counter summary, or None when
+    there is none or the kernel's sources changed since the counters were taken."""
+    path = traffic_path(spec)
+    if not os.path.exists(path):
+        return None, "no counter summary"
+    kv = {}
+    for line in open(path):
+        if ":" in line and not line.startswith(" "):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("source_sha256") != kernel_source_hash(spec.dtype):
+        return None, f"{os.path.relpath(path, ROOT)} predates the current kernel source"
+    return float(kv["traffic_bytes_per_launch"]), os.path.relpath(path, ROOT)
+
+
+def _counter_rows(d):
+    import csv
+    import glob
+    files = glob.glob(os.path.join(d, "**", "*counter_collection.csv"), recursive=True)
+    if not files:
+        raise SystemExit(f"no counter_collection.csv under {d}")
+    rows = []
+    for f in files:
+        rows += list(csv.DictReader(open(f)))
+    return rows
+
+
+def _per_dispatch(rows, name_part, counter):
+    vals = {}
+    for r in rows:
+        if name_part in r["Kernel_Name"] and r["Counter_Name"] == counter:
+            vals[r["Dispatch_Id"]] = vals.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+    return list(vals.values())
+
+
+def write_traffic_summary(args):
+    """Turns four rocprofv3 --pmc runs into the summary that traffic_from_summary reads:
+    fetch/ and write/ under args.traffic_summary (the workload), copy_fetch/ and
+    copy_write/ under args.copy_pmc (a plain device copy of args.copy_mb MiB)."""
+    from workloads import CONFIGS
+    spec = CONFIGS[args.config]
+    d = args.traffic_summary
+    dc = args.copy_pmc or d
+    kname = kernel_name(spec.dtype)
+    mb = args.copy_mb or 256
+    fetch = _per_dispatch(_counter_rows(os.path.join(d, "fetch")), kname, "FETCH_SIZE")
+    write = _per_dispatch(_counter_rows(os.path.join(d, "write")), kname, "WRITE_SIZE")
+    cf = _per_dispatch(_counter_rows(os.path.join(dc, "copy_fetch")), COPY_KERNEL, "FETCH_SIZE")
+    cw = _per_dispatch(_counter_rows(os.path.join(dc, "copy_write")), COPY_KERNEL, "WRITE_SIZE")
+    if not (fetch and write and cf and cw):
+        raise SystemExit("missing dispatches of the kernel or of the copy in the counter runs")
+    kib = mb * 1024.0
+    ff, fw = kib / float(np.mean(cf)), kib / float(np.mean(cw))
+    fk, wk = float(np.mean(fetch)), float(np.mean(write))
+    traffic = (fk * ff + wk * fw) * 1024.0
+    run = (f"python3 bench.py --config {spec.index} --steps 3 --warmup 1 --no-cpu-baseline")
+    cmds = [f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {d}/fetch -o p -- {run}",
+            f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {d}/write -o p -- {run}",
+            f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {dc}/copy_fetch -o p -- "
+            f"python3 bench.py --copy-mb {mb} --steps 2",
+            f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {dc}/copy_write -o p -- "
+            f"python3 bench.py --copy-mb {mb} --steps 2",
+            f"python3 bench.py --config {spec.index} --copy-mb {mb} --traffic-summary {d}"
+            + (f" --copy-pmc {dc}" if dc != d else "")]
+    lines = [f"# HBM traffic of {kname} on {spec.name} (rocprofv3 counters, KiB per dispatch)",
+             "commands (from the repository root, TMPDIR=/tmp, each rocprofv3 run under timeout -s KILL 120):"]
+    lines += [f"  {c}" for c in cmds]
+    lines += [f"kernel: {kname}",
+              f"source_sha256: {kernel_source_hash(spec.dtype)}",
+              f"dispatches: {len(fetch)} (FETCH_SIZE run), {len(write)} (WRITE_SIZE run)",
+              f"fetch_kib_per_dispatch: {fk:.1f}",
+              f"write_kib_per_dispatch: {wk:.1f}",
+              f"copy_calibration: {COPY_KERNEL} of {mb} MiB reads FETCH_SIZE {np.mean(cf):.1f} KiB, "
+              f"WRITE_SIZE {np.mean(cw):.1f} KiB",
+              f"fetch_factor: {ff:.4f}",
+              f"write_factor: {fw:.4f}",
+              f"traffic_bytes_per_launch: {traffic:.0f}"]
+    path = traffic_path(spec)
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    log(f"wrote {os.path.relpath(path, ROOT)}: {traffic / 1e6:.1f} MB per launch")
+
+
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -46,6 +157,15 @@ def parse():
     ap.add_argument("--variant", type=int, default=0, help="gather-GEMM tile-configuration override (tuning)")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="instead of the benchmark, run plain device copies of this many MiB (counter calibration)")
+    ap.add_argument("--traffic-summary", default="",
+                    help="write the HBM-traffic summary under profiles/ from the rocprofv3 counter runs in this "
+                         "directory (runs on the CPU; --copy-mb gives the calibration copy size)")
+    ap.add_argument("--stats-summary", default="",
+                    help="write profiles/kernels_<workload>.txt from the rocprofv3 --kernel-trace --stats run in this "
+                         "directory (runs on the CPU)")
+    ap.add_argument("--stats-log", default="", help="stdout of that profiled run (holds the benchmark's JSON line)")
+    ap.add_argument("--copy-pmc", default="",
+                    help="directory of the copy-calibration counter runs (default: the --traffic-summary one)")
     return ap.parse_args()
 
 
@@ -73,40 +193,26 @@ class SingleLayer:
         rb = P.Rulebook(self.coords, spec.grid, self.L.ksize, self.L.stride, self.L.submanifold)
         self.n_out, self.n_pairs = rb.n_out, rb.n_pairs
         rb.close()
-        self.fwd_events = []
         self.grad = torch.from_numpy(make_grad(spec, self.n_out, self.L.cout)).to(dev).to(self.dt)
         rb = P.Rulebook(self.coords, spec.grid, self.L.ksize, self.L.stride, self.L.submanifold)
         ws = P.backward_workspace_size(rb, self.dt, self.L.cin, self.L.cout)
         rb.close()
         self.ws = torch.empty((ws,), dtype=torch.uint8, device=dev)
-        self.fwd_ms = []
 
-    def forward_only(self, timed=False):
+    def forward_only(self):
         P, torch = self.P, self.torch
         if not hasattr(self, "_rb"):
             L = self.L
             self._rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, L.stride, L.submanifold)
             self._W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt)
             self._out = torch.empty((self.n_out, L.cout), dtype=self.dt, device=self.feats.device)
-        if timed:
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
         P.forward(self.feats, self._rb, self._W, out=self._out)
-        if timed:
-            e1.record()
-            self.fwd_events.append((e0, e1))
 
-    def step(self, timed=False):
-        P, torch, L = self.P, self.torch, self.L
+    def step(self):
+        P, L = self.P, self.L
         rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, L.stride, L.submanifold)
         W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt)
-        if timed:
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
         out = P.forward(self.feats, rb, W)
-        if timed:
-            e1.record()
-            self.fwd_events.append((e0, e1))
         P.backward(self.feats, self.grad, rb, W, self.desc, self.basis, n_coeff=self.n_coeff, workspace=self.ws)
         rb.close()
         return out
@@ -114,8 +220,11 @@ class SingleLayer:
     def sites(self):
         return self.n_out
 
-    def flops(self):
-        return 2.0 * self.n_pairs * self.L.cin * self.L.cout
+    def gather_flops(self, forward_only):
+        """Algorithmic flops of the gather-GEMM launches of one step: the forward and, in a
+        full step, the input-feature gradient, each 2 * pairs * cin * cout."""
+        f = 2.0 * self.n_pairs * self.L.cin * self.L.cout
+        return (f, 1) if forward_only else (2 * f, 2)
 
     def config(self):
         L = self.L
@@ -144,17 +253,19 @@ class StackBench:
         self.n_outs = [L.rb.n_out for L in self.st.layers]
         self.pairs = [L.rb.n_pairs for L in self.st.layers]
         self.grad = torch.from_numpy(make_grad(spec, self.n_outs[-1], spec.layers[-1].cout)).to(dev)
-        self.fwd_ms = []
 
-    def step(self, timed=False):
+    def step(self):
         self.st.forward(self.coords, self.feats)
         self.st.backward(self.grad, need_input_grad=False)
 
     def sites(self):
         return sum(self.n_outs)
 
-    def flops(self):
-        return sum(2.0 * p * L.cin * L.cout for p, L in zip(self.pairs, self.spec.layers))
+    def gather_flops(self, forward_only):
+        """Forward gather-GEMM of every layer plus the input-feature gradient of layers 2..5
+        (the stack input needs no gradient)."""
+        f = [2.0 * p * L.cin * L.cout for p, L in zip(self.pairs, self.spec.layers)]
+        return sum(f) + sum(f[1:]), 2 * len(f) - 1
 
     def config(self):
         return {"workload": self.spec.name, "grid": self.spec.grid, "batch": self.spec.batch,
@@ -182,31 +293,88 @@ def cpu_baseline(i, budget_s):
     t0 = time.perf_counter()
     co = orb.output_sites(coords, spec.grid, L.ksize, L.stride, L.submanifold)
     t_sites = time.perf_counter() - t0
-    # sample: the first m output rows, sized from a short probe to the time budget
-    probe = min(len(co), 256)
-    t0 = time.perf_counter()
-    R = orb.rulebook(coords, co[:probe], L.ksize, L.stride)
-    kap = lay.kappa(w)
-    oc.forward(f, R, kap, probe)
-    t_probe = time.perf_counter() - t0
-    m = int(min(len(co), max(probe, probe * budget_s / max(4 * t_probe, 1e-6))))
-    g = make_grad(spec, len(co), L.cout)[:m]
-    t0 = time.perf_counter()
-    R = orb.rulebook(coords, co[:m], L.ksize, L.stride)
-    kap = lay.kappa(w)
-    oc.forward(f, R, kap, m)
-    oc.grad_feats(g, R, kap, len(coords))
-    dk = oc.grad_kappa(f, g, R, kap.shape)
-    oc.synth_adjoint(L, lay.basis, dk)
-    t = time.perf_counter() - t0 + t_sites * m / max(len(co), 1)
+    # sample: the first m output rows, grown until the timed work fills about half the budget
+    m = min(len(co), 256)
+    while True:
+        g = make_grad(spec, len(co), L.cout)[:m]
+        t0 = time.perf_counter()
+        R = orb.rulebook(coords, co[:m], L.ksize, L.stride)
+        kap = lay.kappa(w)
+        oc.forward(f, R, kap, m)
+        oc.grad_feats(g, R, kap, len(coords))
+        dk = oc.grad_kappa(f, g, R, kap.shape)
+        oc.synth_adjoint(L, lay.basis, dk)
+        t = time.perf_counter() - t0 + t_sites * m / max(len(co), 1)
+        if m == len(co) or t >= 0.5 * budget_s:
+            break
+        m = int(min(len(co), max(2 * m, m * 0.8 * budget_s / max(t, 1e-3))))
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
     return {"value": m / t / 1e6, "unit": "M active output sites/s", "cores": int(threads), "kind": "oracle",
             "sample": f"{spec.name}: first {m} of {len(co)} output rows, all offsets; rulebook (dict, 1 thread) + "
                       f"synth + forward + backward (fp64 numpy), {t:.1f} s"}
 
 
+def write_stats_summary(args):
+    """Tabulates a rocprofv3 --kernel-trace --stats run of this benchmark (directory
+    args.stats_summary, with the benchmark's own JSON line in args.stats_log) into
+    profiles/kernels_<workload>.txt, next to the gather-GEMM launch time the benchmark
+    measured with its events in the same run."""
+    import csv
+    import glob
+    import re
+    from workloads import CONFIGS
+    spec = CONFIGS[args.config]
+    d = args.stats_summary
+    stats = list(csv.DictReader(open(glob.glob(os.path.join(d, "*_kernel_stats.csv"))[0])))
+    trace = list(csv.DictReader(open(glob.glob(os.path.join(d, "*_kernel_trace.csv"))[0])))
+    bench = None
+    for line in open(args.stats_log):
+        if line.startswith("{"):
+            bench = json.loads(line)
+
+    def short(n):
+        n = n.replace("(anonymous namespace)::", "").replace("void ", "").replace("ssconv::", "")
+        return re.sub(r"\(.*", "", n)[:70]
+
+    steps, warmup = (bench["steps"], bench["warmup"]) if bench else (args.steps, args.warmup)
+    run = f"python3 bench.py --config {spec.index} --steps {steps} --warmup {warmup} --no-cpu-baseline"
+    out = [f"# rocprofv3 kernel statistics: {spec.name} ({spec.dtype}), one step = rule book + synthesis + "
+           "forward + backward",
+           f"command: rocprofv3 --kernel-trace --stats --output-format csv -d {d} -o p -- {run} > {args.stats_log}",
+           f"summary: python3 bench.py --config {spec.index} --stats-summary {d} --stats-log {args.stats_log}", "",
+           f"{'kernel':70s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} {'pct':>6s}"]
+    for r in stats[:18]:
+        out.append(f"{short(r['Name']):70s} {r['Calls']:>6s} {float(r['AverageNs']) / 1e3:9.1f} "
+                   f"{float(r['MinNs']) / 1e3:9.1f} {float(r['MaxNs']) / 1e3:9.1f} {float(r['Percentage']):6.1f}")
+    kname = kernel_name(spec.dtype)
+    g = sorted((int(t["Start_Timestamp"]), int(t["End_Timestamp"])) for t in trace if kname in t["Kernel_Name"])
+    if g:
+        durs = [(e - b) / 1e3 for b, e in g]
+        n_timed = bench["roofline"]["launches_timed"] if bench else 0
+        timed = durs[len(durs) - n_timed:] if n_timed else durs
+        out += ["", f"{kname} dispatches in launch order (us): " + " ".join(f"{x:.0f}" for x in durs),
+                f"{kname} average over the {len(timed)} timed dispatches (trace): {np.mean(timed):.1f} us"]
+        if bench:
+            r = bench["roofline"]
+            out.append(f"{kname} average launch time measured by the benchmark's HIP events in the same run: "
+                       f"{r['avg_launch_ms'] * 1e3:.1f} us ({r['achieved']:.1f} {r['unit']}, "
+                       f"{100 * r['frac']:.1f}% of {r['peak']})")
+    if bench:
+        out.append(f"step: {bench['ms_per_step']:.3f} ms ({bench['value']:.2f} {bench['unit']}) under the profiler")
+    path = os.path.join(ROOT, "profiles", f"kernels_{spec.name}.txt")
+    with open(path, "w") as fh:
+        fh.write("\n".join(out) + "\n")
+    log(f"wrote {os.path.relpath(path, ROOT)}")
+
+
 def main():
     args = parse()
+    if args.stats_summary:
+        write_stats_summary(args)
+        return
+    if args.traffic_summary:
+        write_traffic_summary(args)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (got --gpus {args.gpus}); the multi-GPU sharding is a design "
               "described in DESIGN.md, not a measured path.", file=sys.stderr)
@@ -236,18 +404,19 @@ def main():
     if args.only == "forward" and args.config == 5:
         raise SystemExit("--only forward applies to the single-layer workloads 1-4")
     run = b.forward_only if args.only == "forward" else b.step
-    b.fwd_events = []
     for _ in range(args.warmup):
         run()
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} steps); timing {args.steps} steps")
-    b.fwd_events = []
+    import paper_2111_07383_amd as P
+    P.debug_set(4, 1)                 # HIP events around each gather-GEMM launch, on its stream
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        run(timed=True)
+        run()
     torch.cuda.synchronize()
     t = time.perf_counter() - t0
+    P.debug_set(4, 0)
     ms = t / args.steps * 1e3
     value = b.sites() / (ms / 1e3) / 1e6
     log(f"{ms:.3f} ms/step, {value:.2f} M sites/s")
@@ -258,13 +427,20 @@ def main():
     if args.only == "forward":
         out["metric"] = METRIC + " (forward gather-GEMM only)"
         out["config"]["step"] = "forward gather-MFMA only (rule book and kernel prebuilt)"
-    if b.fwd_events:
-        fwd_ms = float(np.mean([e0.elapsed_time(e1) for e0, e1 in b.fwd_events]))
-        flops = b.flops()
-        achieved = flops / (fwd_ms / 1e3) / 1e12
-        out["roofline"] = {"kernel": "gather_gemm (forward)", "bound": "mfma", "achieved": achieved,
-                           "peak": PEAK[spec.dtype], "unit": "TFLOP/s", "frac": achieved / PEAK[spec.dtype],
-                           "traffic": None, "avg_ms": fwd_ms, "algorithmic_flops": flops}
+    n_timed, kern_ms = P.debug_kernel_ms()
+    flops_step, launches_step = b.gather_flops(args.only == "forward")
+    if n_timed != launches_step * args.steps:
+        log(f"warning: {n_timed} gather-GEMM launches timed, expected {launches_step * args.steps}")
+    avg_ms = kern_ms / max(n_timed, 1)
+    flops_launch = flops_step / launches_step
+    achieved = flops_step * args.steps / (kern_ms / 1e3) / 1e12
+    traffic, tsrc = traffic_from_summary(spec)
+    out["roofline"] = {"kernel": kernel_name(spec.dtype), "bound": "mfma", "achieved": achieved,
+                       "peak": PEAK[spec.dtype], "unit": "TFLOP/s", "frac": achieved / PEAK[spec.dtype],
+                       "traffic": traffic, "traffic_source": tsrc, "avg_launch_ms": avg_ms,
+                       "launches_timed": n_timed, "algorithmic_flops_per_launch": flops_launch,
+                       "kernel_ms_per_step": kern_ms / args.steps}
+    log(f"gather-GEMM: {n_timed} launches, {avg_ms:.4f} ms avg, {achieved:.1f} TFLOP/s")
     if not args.no_cpu_baseline and args.config != 5:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(args.config, args.cpu_budget)

@@ -194,10 +194,25 @@ int ssconv_gate_backward(const ssconv_fields* fields /*host*/, const void* x, co
  * Forces failure paths from the host so they can be tested without faulting
  * a device: option 1 = hash capacity (slots) used by the next rule book builds
  * (0 restores automatic sizing); option 2 = make the N-th following device
- * allocation fail (0 disables); option 3 = tile-configuration override of the
- * gather-GEMM kernel for tuning sweeps (0 = automatic choice; results are
- * identical for every value).  Returns E_INVALID for unknown options. */
+ * allocation fail (0 disables); option 3 = kernel-selection override for
+ * tuning sweeps and cross-checks (0 = automatic choice; 1, 2 = tile variants
+ * of the generic gather-GEMM kernel; 5 = bf16 convolutions use the generic
+ * gather-GEMM kernel instead of the bf16 pipeline kernel; 6 = the bf16 kernel
+ * gradient uses per-offset splits instead of balanced work units; results
+ * agree within the dtype's tolerance for every value); option 4 = kernel
+ * timing: a nonzero value switches it on and clears this thread's log, 0
+ * switches it off; while on, every gather-GEMM kernel launch (the one of
+ * ssconv_forward and the input-feature gradient one of ssconv_backward) is
+ * bracketed by a pair of HIP events on its stream, up to 4096 launches per
+ * thread, and nothing else of the call is timed.  Returns E_INVALID for
+ * unknown options. */
 int ssconv_debug_set(int option, int64_t value);
+
+/* Kernel timing read-out: *count (host) = gather-GEMM launches timed on this
+ * thread since option 4 was last switched on, *total_ms (host) = the sum of
+ * their durations in milliseconds.  Waits for the last timed kernel.
+ * E_INVALID if nothing was timed, E_HIP if the events fail. */
+int ssconv_debug_kernel_ms(int64_t* count, float* total_ms);
 
 #ifdef __cplusplus
 }

@@ -12,6 +12,7 @@ from .binding import (  # noqa: F401
     basis_desc,
     basis_info,
     build_rulebook,
+    debug_kernel_ms,
     debug_set,
     forward,
     gate_backward,

@@ -6,7 +6,7 @@ missing, loading raises.
 """
 import ctypes
 import os
-from ctypes import POINTER, c_char_p, c_double, c_int, c_int64, c_size_t, c_void_p
+from ctypes import POINTER, c_char_p, c_double, c_float, c_int, c_int64, c_size_t, c_void_p
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libssconv.so")
 
@@ -49,6 +49,7 @@ SIGNATURES = {
     "ssconv_gate_forward": (c_int, [POINTER(Fields), c_void_p, c_int, c_int64, c_void_p, c_void_p]),
     "ssconv_gate_backward": (c_int, [POINTER(Fields), c_void_p, c_void_p, c_int, c_int64, c_void_p, c_void_p]),
     "ssconv_debug_set": (c_int, [c_int, c_int64]),
+    "ssconv_debug_kernel_ms": (c_int, [POINTER(c_int64), POINTER(c_float)]),
 }
 
 

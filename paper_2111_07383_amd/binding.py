@@ -6,7 +6,7 @@ etc.).  Tensors must live on the current HIP device; bf16 tensors map to
 SSCONV_BF16 and fp32 tensors to SSCONV_F32.
 """
 import ctypes
-from ctypes import byref, c_int, c_int64, c_void_p
+from ctypes import byref, c_float, c_int, c_int64, c_void_p
 from typing import Optional, Sequence, Tuple
 
 import numpy as np
@@ -247,3 +247,11 @@ def gate_backward(fields: FieldList, x: torch.Tensor, dy: torch.Tensor, stream=N
 
 def debug_set(option: int, value: int) -> None:
     check(lib().ssconv_debug_set(int(option), int(value)), "ssconv_debug_set")
+
+
+def debug_kernel_ms() -> Tuple[int, float]:
+    """(launches, total ms) of the gather-GEMM kernels timed on this thread since
+    debug_set(4, 1); waits for the last of them."""
+    n, ms = c_int64(), c_float()
+    check(lib().ssconv_debug_kernel_ms(byref(n), byref(ms)), "ssconv_debug_kernel_ms")
+    return int(n.value), float(ms.value)

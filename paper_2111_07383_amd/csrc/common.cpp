@@ -1,6 +1,9 @@
 // Error reporting, allocation and field tables shared by the SS-Conv entry points.
 #include "common.hpp"
 
+#include <utility>
+#include <vector>
+
 #include <atomic>
 
 namespace ssconv {
@@ -10,6 +13,14 @@ thread_local std::string g_error;
 std::atomic<int64_t> g_debug_hash_cap{0};
 std::atomic<int64_t> g_debug_fail_alloc{0};
 std::atomic<int64_t> g_debug_gather_variant{0};
+std::atomic<int64_t> g_debug_timing{0};
+// event pairs of the kernel timing hook, reused from call to call on this thread
+constexpr size_t kMaxTimed = 4096;
+struct TimingLog {
+  std::vector<std::pair<hipEvent_t, hipEvent_t>> ev;
+  size_t used = 0;
+};
+thread_local TimingLog g_timing;
 }  // namespace
 
 void set_error(const char* fmt, ...) {
@@ -58,6 +69,23 @@ void dev_free(void* p, hipStream_t stream) {
 int64_t debug_hash_capacity() { return g_debug_hash_cap.load(); }
 int64_t debug_gather_variant() { return g_debug_gather_variant.load(); }
 
+bool debug_timing_events(hipEvent_t* start, hipEvent_t* stop) {
+  if (g_debug_timing.load() == 0 || g_timing.used == kMaxTimed) return false;
+  if (g_timing.used == g_timing.ev.size()) {
+    hipEvent_t a = nullptr, b = nullptr;
+    if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
+      if (a) (void)hipEventDestroy(a);
+      (void)hipGetLastError();
+      return false;
+    }
+    g_timing.ev.emplace_back(a, b);
+  }
+  *start = g_timing.ev[g_timing.used].first;
+  *stop = g_timing.ev[g_timing.used].second;
+  ++g_timing.used;
+  return true;
+}
+
 int make_fieldtab(const ssconv_fields* f, FieldTab* t) {
   if (!f || f->n < 1 || f->n > SSCONV_MAX_ENTRIES) return fail(SSCONV_E_INVALID, "bad field list");
   t->n = f->n;
@@ -98,5 +126,28 @@ extern "C" int ssconv_debug_set(int option, int64_t value) {
     ssconv::g_debug_gather_variant.store(value < 0 ? 0 : value);
     return SSCONV_OK;
   }
+  if (option == 4) {
+    ssconv::g_debug_timing.store(value != 0 ? 1 : 0);
+    if (value != 0) ssconv::g_timing.used = 0;
+    return SSCONV_OK;
+  }
   return ssconv::fail(SSCONV_E_INVALID, "unknown debug option %d", option);
+}
+
+extern "C" int ssconv_debug_kernel_ms(int64_t* count, float* total_ms) {
+  using namespace ssconv;
+  if (!count || !total_ms) return fail(SSCONV_E_INVALID, "count or total_ms is NULL");
+  *count = 0;
+  *total_ms = 0.f;
+  if (g_timing.used == 0) return fail(SSCONV_E_INVALID, "no timed kernel on this thread");
+  SSC_HIP(hipEventSynchronize(g_timing.ev[g_timing.used - 1].second));
+  double sum = 0.0;
+  for (size_t i = 0; i < g_timing.used; ++i) {
+    float ms = 0.f;
+    SSC_HIP(hipEventElapsedTime(&ms, g_timing.ev[i].first, g_timing.ev[i].second));
+    sum += ms;
+  }
+  *count = (int64_t)g_timing.used;
+  *total_ms = (float)sum;
+  return SSCONV_OK;
 }

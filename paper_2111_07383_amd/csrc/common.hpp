@@ -38,6 +38,9 @@ int dev_alloc(void** p, size_t bytes, hipStream_t stream);
 void dev_free(void* p, hipStream_t stream);
 int64_t debug_hash_capacity();
 int64_t debug_gather_variant();
+// Kernel timing hook (ssconv_debug_set option 4): returns the event pair to record around the
+// next timed kernel, or false when timing is off.
+bool debug_timing_events(hipEvent_t* start, hipEvent_t* stop);
 
 // ---------------------------------------------------------------------------
 // field tables (channel -> field, order, component) passed by value to kernels

@@ -333,19 +333,39 @@ static bool use_bf16_kernel(ssconv_dtype dt, int64_t n_src, int ca, int cb, int 
   return dt == SSCONV_BF16 && debug_gather_variant() != 5 && gather_bf16_supported(n_src, ca, cb, K);
 }
 
+// Records the timing-hook events (ssconv_debug_set option 4) around one kernel launch.
+struct KernelTimer {
+  hipEvent_t start = nullptr, stop = nullptr;
+  hipStream_t st;
+  bool on;
+  explicit KernelTimer(hipStream_t s) : st(s), on(debug_timing_events(&start, &stop)) {
+    if (on) (void)hipEventRecord(start, st);
+  }
+  ~KernelTimer() {
+    if (on) (void)hipEventRecord(stop, st);
+  }
+};
+
 int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_rulebook* rb, const void* W, int cout,
                  void* out, hipStream_t st) {
   if (rb->n_out == 0) return SSCONV_OK;
-  if (dt == SSCONV_F32) return dispatch_gg<float>(feats, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st);
+  if (dt == SSCONV_F32) {
+    KernelTimer timer(st);
+    return dispatch_gg<float>(feats, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st);
+  }
   if (use_bf16_kernel(dt, rb->n_in, cin, cout, rb->K)) {
     // kappa packed for the bf16 kernel in a stream-ordered scratch buffer
     void* Bp = nullptr;
     SSC_TRY(dev_alloc(&Bp, (size_t)rb->K * cin * cout * 2, st));
     int rc = pack_b_bf16(W, rb->K, cin, cout, false, Bp, st);
-    if (rc == SSCONV_OK) rc = gather_bf16(feats, rb->n_in, cin, Bp, cout, rb->nbr, nullptr, rb->n_out, rb->K, out, st);
+    if (rc == SSCONV_OK) {
+      KernelTimer timer(st);
+      rc = gather_bf16(feats, rb->n_in, cin, Bp, cout, rb->nbr, nullptr, rb->n_out, rb->K, out, st);
+    }
     dev_free(Bp, st);
     return rc;
   }
+  KernelTimer timer(st);
   return dispatch_gg<uint16_t>(feats, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st);
 }
 
@@ -407,15 +427,18 @@ int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout
   if (dt == SSCONV_F32) {
     transpose_kernel<float><<<cdiv(nw, 256), 256, 0, st>>>((const float*)W, K, cout, cin, (float*)Wt);
     SSC_HIP(hipGetLastError());
+    KernelTimer timer(st);
     return dispatch_gg<float>(grad_out, cout, Wt, cin, nbrT, rb->n_in, K, grad_feats, st);
   }
   if (use_bf16_kernel(dt, rb->n_out, cout, cin, K)) {
     // kappa^T packed for the bf16 kernel: Bp[s][o/8][i][o%8] = W[s][o][i]
     SSC_TRY(pack_b_bf16(W, K, cout, cin, true, Wt, st));
+    KernelTimer timer(st);
     return gather_bf16(grad_out, rb->n_out, cout, Wt, cin, nbrT, nullptr, rb->n_in, K, grad_feats, st);
   }
   transpose_kernel<uint16_t><<<cdiv(nw, 256), 256, 0, st>>>((const uint16_t*)W, K, cout, cin, (uint16_t*)Wt);
   SSC_HIP(hipGetLastError());
+  KernelTimer timer(st);
   return dispatch_gg<uint16_t>(grad_out, cout, Wt, cin, nbrT, rb->n_in, K, grad_feats, st);
 }
 

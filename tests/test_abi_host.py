@@ -77,3 +77,11 @@ def test_invalid_descriptors(abi):
         B.basis_info(bad)
     with pytest.raises(abi.SSConvError):
         B.debug_set(9, 1)
+
+
+def test_kernel_timing_without_timed_call(abi):
+    from paper_2111_07383_amd import binding as B
+    B.debug_set(4, 0)
+    with pytest.raises(abi.SSConvError) as e:       # nothing timed on this thread: no device call made
+        B.debug_kernel_ms()
+    assert e.value.code == abi.E_INVALID

@@ -133,3 +133,25 @@ def test_row_order_independence():
         outs.append(P.forward(torch.from_numpy(np.ascontiguousarray(ff)).to(DEV), rb, W).cpu().numpy())
         rb.close()
     assert rel_err(outs[1], outs[0][perm]) < 1e-6
+
+
+@pytest.mark.parametrize("dt", [torch.float32, torch.bfloat16])
+def test_kernel_timing_hook(dt):
+    c = torch.from_numpy(_coords(5, 3000, 24)).to(DEV)
+    rb = P.Rulebook(c, 24, 3)
+    W = (torch.randn((27, 48, 32), device=DEV) * 0.1).to(dt)
+    x = torch.randn((rb.n_in, 32), device=DEV).to(dt)
+    P.debug_set(4, 1)
+    try:
+        y0 = P.forward(x, rb, W)
+        y1 = P.forward(x, rb, W)
+        n, ms = P.debug_kernel_ms()
+        assert n == 2 and ms > 0.0
+        torch.testing.assert_close(y0, y1, rtol=0, atol=0)
+        P.debug_set(4, 1)                                # switching on again clears the log
+        assert _code(P.debug_kernel_ms) == E_INVALID
+    finally:
+        P.debug_set(4, 0)
+    P.forward(x, rb, W)                                  # timing off: nothing recorded
+    assert _code(P.debug_kernel_ms) == E_INVALID
+    rb.close()
