@@ -3,8 +3,8 @@
 //
 //   out[x] = sum_s kappa(s) in[nbr[s][x]]   for the output rows x of a tile
 //
-// A workgroup of four wavefronts owns BM = 4*WMB*16 output rows and BN = WNB*16
-// output channels.  Its reduction dimension is the concatenation, over the
+// A workgroup of NW wavefronts (8 for fp32, 4 for bf16) owns BM = NW*WMB*16 output
+// rows and BN = WNB*16 output channels.  Its reduction dimension is the concatenation, over the
 // offsets present in its rows, of the Cin input channels of each offset, cut
 // into 32-wide chunks; a chunk may straddle two offsets, so no channel padding
 // is paid per offset.
@@ -15,10 +15,12 @@
 //     16-byte global->LDS DMA loads (global_load_lds_dwordx4) straight into
 //     MFMA fragment order: lane l of a load lands at byte 16*l of a 1 KB
 //     block, which is exactly the 16 bytes that lane l later feeds the MFMA;
-//   * S stages are in flight; a stage is waited for with s_waitcnt on the
-//     wavefront's own DMA count (every wavefront issues the same number per
-//     stage: absent rows read a zero line, surplus kappa slots load into a
-//     junk block) and published with one barrier per chunk;
+//   * three stages: iteration c waits for the wavefront's own DMAs of chunk
+//     c+1 (every wavefront issues the same number per stage: absent rows read
+//     a zero line, surplus kappa slots load into a junk block), publishes them
+//     with one barrier, and runs the MFMAs of chunk c from registers with the
+//     fragment reads of chunk c+1 and the DMAs of chunk c+2 spread between the
+//     column blocks;
 //   * rows without a neighbour at an offset contribute zeros (measured on the
 //     benchmark surfaces, skipping at 16-row granularity would save ~1% of the
 //     MFMA work but costs branches around every MFMA).
@@ -35,7 +37,6 @@ namespace {
 typedef float f4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
-constexpr int kNT = 256;
 constexpr int kBK = 32;
 constexpr int kMaxK = 128;
 constexpr int kLdsLimit = 160 * 1024;
@@ -61,26 +62,27 @@ __device__ __forceinline__ void mma_frag(f4& acc, const uint4 (&a)[1], const uin
   acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, bv, acc, 0, 0, 0);
 }
 
-template <typename T, int WMB, int WNB, int S>
+template <typename T, int WMB, int WNB, int S, int NW>
 struct Shape {
-  static constexpr int BM = 4 * WMB * 16;
+  static constexpr int NT = 64 * NW;                     // NW wavefronts
+  static constexpr int BM = NW * WMB * 16;
   static constexpr int BN = WNB * 16;
   static constexpr int VE = 16 / (int)sizeof(T);         // elements per 16-byte vector
   static constexpr int RV = 8 / VE;                      // 16-byte vectors per lane per chunk
-  static constexpr int BJ = (WNB + 3) / 4;               // kappa blocks loaded per wavefront per chunk
-  static constexpr int ABYTES = 4 * WMB * RV * 1024;     // gathered rows of one stage
+  static constexpr int BJ = (WNB + NW - 1) / NW;         // kappa blocks loaded per wavefront per chunk
+  static constexpr int ABYTES = NW * WMB * RV * 1024;    // gathered rows of one stage
   static constexpr int BBYTES = WNB * RV * 1024;         // kappa chunk of one stage
   static constexpr int STAGE = ABYTES + BBYTES;
   static constexpr int L = (WMB + BJ) * RV;              // DMA loads per wavefront per stage
 };
 
-template <typename T, int WMB, int WNB, int S>
-__global__ __launch_bounds__(kNT) void gather_mfma_kernel(const T* __restrict__ src, int ca,
+template <typename T, int WMB, int WNB, int S, int NW>
+__global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restrict__ src, int ca,
                                                           const T* __restrict__ Bt, int cb,
                                                           const int32_t* __restrict__ nbr,
                                                           const int32_t* __restrict__ order, int64_t n_pos, int K,
                                                           T* __restrict__ out) {
-  using SH = Shape<T, WMB, WNB, S>;
+  using SH = Shape<T, WMB, WNB, S, NW>;
   constexpr int BM = SH::BM, RV = SH::RV, VE = SH::VE, BJ = SH::BJ, L = SH::L;
   // dynamic LDS only (base at LDS address 0): stages | junk | bmask | act | count | index table
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -96,7 +98,7 @@ __global__ __launch_bounds__(kNT) void gather_mfma_kernel(const T* __restrict__ 
   const int n0 = blockIdx.y * SH::BN;
 
   // 1. neighbour indices of the tile (all offsets) and the 16-row blocks each offset touches
-  for (int s = w; s < K; s += 4) {
+  for (int s = w; s < K; s += NW) {
     uint32_t m = 0;
 #pragma unroll
     for (int j = 0; j < BM / 64; ++j) {
@@ -149,27 +151,31 @@ __global__ __launch_bounds__(kNT) void gather_mfma_kernel(const T* __restrict__ 
       ap[mb] = alive[mb] ? src + (int64_t)idx_ * ca + r_ch : zero;                                  \
     }                                                                                               \
     _Pragma("unroll") for (int j = 0; j < BJ; ++j) {                                                \
-      const int nb_ = w + 4 * j;                                                                    \
+      const int nb_ = w + NW * j;                                                                   \
       const int n_ = n0 + 16 * nb_ + r16;                                                           \
       bok[j] = nb_ < WNB && live_ && n_ < cb;                                                       \
       bp[j] = bok[j] ? Bt + ((int64_t)s_ * cb + n_) * ca + r_ch : zero;                             \
     }                                                                                               \
   } while (0)
 
-#define SSC_ISSUE(c_)                                                                               \
+  // DMA q of this wavefront for the chunk going into stage st_: q < WMB*RV -> row block q / RV,
+  // vector q % RV; else kappa slot (q - WMB*RV) / RV (a slot past WNB loads into the junk block)
+#define SSC_DMA(q_, st_)                                                                            \
   do {                                                                                              \
-    const int st_ = (c_) % S;                                                                       \
-    const uint32_t abase_ = stage0 + st_ * SH::STAGE;                                               \
-    _Pragma("unroll") for (int mb = 0; mb < WMB; ++mb) {                                            \
-      _Pragma("unroll") for (int q = 0; q < RV; ++q)                                                \
-        dma16(ap[mb] + (alive[mb] ? q * VE : 0), abase_ + ((w * WMB + mb) * RV + q) * 1024);        \
+    const uint32_t abase_ = stage0 + (st_) * SH::STAGE;                                             \
+    if ((q_) < WMB * RV) {                                                                          \
+      const int mb_ = (q_) / RV, v_ = (q_) % RV;                                                    \
+      dma16(ap[mb_] + (alive[mb_] ? v_ * VE : 0), abase_ + ((w * WMB + mb_) * RV + v_) * 1024);     \
+    } else {                                                                                        \
+      const int j_ = ((q_) - WMB * RV) / RV, v_ = ((q_) - WMB * RV) % RV;                           \
+      const int nb_ = w + NW * j_;                                                                  \
+      dma16(bp[j_] + (bok[j_] ? v_ * VE : 0),                                                       \
+            nb_ < WNB ? abase_ + SH::ABYTES + (nb_ * RV + v_) * 1024 : junk_a);                     \
     }                                                                                               \
-    const uint32_t bbase_ = abase_ + SH::ABYTES;                                                    \
-    _Pragma("unroll") for (int j = 0; j < BJ; ++j) {                                                \
-      const int nb_ = w + 4 * j;                                                                    \
-      _Pragma("unroll") for (int q = 0; q < RV; ++q)                                                \
-        dma16(bp[j] + (bok[j] ? q * VE : 0), nb_ < WNB ? bbase_ + (nb_ * RV + q) * 1024 : junk_a);  \
-    }                                                                                               \
+  } while (0)
+
+#define SSC_ADVANCE()                                                                               \
+  do {                                                                                              \
     r_ch += kBK;                                                                                    \
     if (r_ch >= ca) {                                                                               \
       while (r_ch >= ca) r_ch -= ca, ++r_slot;                                                      \
@@ -180,6 +186,25 @@ __global__ __launch_bounds__(kNT) void gather_mfma_kernel(const T* __restrict__ 
     }                                                                                               \
   } while (0)
 
+#define SSC_ISSUE(c_)                                                                               \
+  do {                                                                                              \
+    _Pragma("unroll") for (int q = 0; q < L; ++q) SSC_DMA(q, (c_) % S);                             \
+    SSC_ADVANCE();                                                                                  \
+  } while (0)
+
+  // fragment u of the chunk in stage base sb_: u < WMB*RV -> row block u / RV, vector u % RV;
+  // else kappa block (u - WMB*RV) / RV
+  constexpr int NR = (WMB + WNB) * RV;
+#define SSC_FRAG(AF, BF, u_, sb_)                                                                   \
+  do {                                                                                              \
+    if ((u_) < WMB * RV)                                                                            \
+      AF[(u_) / RV][(u_) % RV] =                                                                    \
+          *reinterpret_cast<const uint4*>((sb_) + ((w * WMB + (u_) / RV) * RV + (u_) % RV) * 1024 + 16 * lane); \
+    else                                                                                            \
+      BF[((u_) - WMB * RV) / RV][((u_) - WMB * RV) % RV] =                                          \
+          *reinterpret_cast<const uint4*>((sb_) + SH::ABYTES + ((u_) - WMB * RV) * 1024 + 16 * lane); \
+  } while (0)
+
   SSC_REFRESH();
 
   f4 acc[WMB][WNB];
@@ -188,35 +213,54 @@ __global__ __launch_bounds__(kNT) void gather_mfma_kernel(const T* __restrict__ 
 #pragma unroll
     for (int nb = 0; nb < WNB; ++nb) acc[mb][nb] = f4{0.f, 0.f, 0.f, 0.f};
 
+  // Software pipeline over the chunks (S stages): iteration c waits for this wavefront's DMAs of
+  // chunk c+1, publishes them with one barrier, then runs the MFMAs of chunk c (fragments already
+  // in registers) one column block at a time, with the fragment reads of chunk c+1 and the DMAs
+  // of chunk c+S-1 spread between the blocks.  The stage refilled in iteration c held chunk c-1,
+  // whose fragments were consumed by the MFMAs of iteration c-1, before this barrier.
+  static_assert(S == 3, "the pipelined chunk loop is written for three stages");
   for (int c = 0; c < S - 1 && c < nchunk; ++c) SSC_ISSUE(c);
-  for (int c = 0; c < nchunk; ++c) {
-    // own DMAs of stage c done: later stages may stay in flight (all of them in steady state)
-    if (c + S - 2 < nchunk)
-      wait_vm<L * (S - 2)>();
-    else
-      wait_vm<0>();
+  uint4 fa0[WMB][RV], fb0[WNB][RV], fa1[WMB][RV], fb1[WNB][RV];
+  if (nchunk > 0) {
+    if (nchunk > 1) wait_vm<L>(); else wait_vm<0>();
     __syncthreads();
-    if (c + S - 1 < nchunk) SSC_ISSUE(c + S - 1);
-    const char* sb = stages + (c % S) * SH::STAGE;
-    // every fragment of the chunk is read before the first MFMA, so one LDS round trip
-    // covers the whole chunk; the MFMAs then run back to back on in-place accumulators
-    uint4 af[WMB][RV], bf[WNB][RV];
 #pragma unroll
-    for (int mb = 0; mb < WMB; ++mb)
-#pragma unroll
-      for (int q = 0; q < RV; ++q)
-        af[mb][q] = *reinterpret_cast<const uint4*>(sb + ((w * WMB + mb) * RV + q) * 1024 + 16 * lane);
-#pragma unroll
-    for (int nb = 0; nb < WNB; ++nb)
-#pragma unroll
-      for (int q = 0; q < RV; ++q)
-        bf[nb][q] = *reinterpret_cast<const uint4*>(sb + SH::ABYTES + (nb * RV + q) * 1024 + 16 * lane);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int nb = 0; nb < WNB; ++nb)
-#pragma unroll
-      for (int mb = 0; mb < WMB; ++mb) mma_frag(acc[mb][nb], af[mb], bf[nb]);
+    for (int u = 0; u < NR; ++u) SSC_FRAG(fa0, fb0, u, stages);
   }
+#define SSC_BODY(k_, AC, BC, AN, BN)                                                                \
+  {                                                                                                 \
+    const int cc_ = c + (k_);                                                                       \
+    if (cc_ >= nchunk) break;                                                                       \
+    wait_vm<0>();                                                                                   \
+    __syncthreads();                                                                                \
+    const bool rd_ = cc_ + 1 < nchunk;                                                              \
+    const bool iss_ = cc_ + S - 1 < nchunk;                                                         \
+    const int ks_ = (cc_ + S - 1) % S;                                                              \
+    const char* sbr_ = stages + ((cc_ + 1) % S) * SH::STAGE;                                        \
+    __builtin_amdgcn_sched_barrier(0);                                                              \
+    _Pragma("unroll") for (int nb = 0; nb < WNB; ++nb) {                                            \
+      _Pragma("unroll") for (int mb = 0; mb < WMB; ++mb) mma_frag(acc[mb][nb], AC[mb], BC[nb]);     \
+      __builtin_amdgcn_sched_barrier(0);                                                            \
+      if (rd_) {                                                                                    \
+        _Pragma("unroll") for (int u = (nb * NR + WNB - 1) / WNB; u < ((nb + 1) * NR + WNB - 1) / WNB; ++u) \
+          SSC_FRAG(AN, BN, u, sbr_);                                                                \
+      }                                                                                             \
+      if (iss_) {                                                                                   \
+        _Pragma("unroll") for (int q = (nb * L + WNB - 1) / WNB; q < ((nb + 1) * L + WNB - 1) / WNB; ++q) \
+          SSC_DMA(q, ks_);                                                                          \
+      }                                                                                             \
+      __builtin_amdgcn_sched_barrier(0);                                                            \
+    }                                                                                               \
+    if (iss_) SSC_ADVANCE();                                                                        \
+  }
+  for (int c = 0;; c += 2) {
+    SSC_BODY(0, fa0, fb0, fa1, fb1)
+    SSC_BODY(1, fa1, fb1, fa0, fb0)
+  }
+#undef SSC_BODY
+#undef SSC_FRAG
+#undef SSC_ADVANCE
+#undef SSC_DMA
 #undef SSC_ISSUE
 #undef SSC_REFRESH
 
@@ -237,21 +281,21 @@ __global__ __launch_bounds__(kNT) void gather_mfma_kernel(const T* __restrict__ 
   }
 }
 
-template <typename T, int WMB, int WNB, int S>
+template <typename T, int WMB, int WNB, int S, int NW>
 size_t smem_bytes(int K) {
-  using SH = Shape<T, WMB, WNB, S>;
+  using SH = Shape<T, WMB, WNB, S, NW>;
   return (size_t)S * SH::STAGE + 1024 + kMaxK * 5 + 16 + (size_t)K * SH::BM * 4;
 }
 
-template <typename T, int WMB, int WNB, int S>
+template <typename T, int WMB, int WNB, int S, int NW>
 int launch(const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, const int32_t* order, int64_t n_pos,
            int K, void* out, hipStream_t st) {
-  using SH = Shape<T, WMB, WNB, S>;
-  const size_t smem = smem_bytes<T, WMB, WNB, S>(K);
-  auto kern = gather_mfma_kernel<T, WMB, WNB, S>;
+  using SH = Shape<T, WMB, WNB, S, NW>;
+  const size_t smem = smem_bytes<T, WMB, WNB, S, NW>(K);
+  auto kern = gather_mfma_kernel<T, WMB, WNB, S, NW>;
   SSC_HIP(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem));
   dim3 grid(cdiv(n_pos, SH::BM), cdiv(cb, SH::BN));
-  kern<<<grid, kNT, smem, st>>>((const T*)src, ca, (const T*)Bt, cb, nbr, order, n_pos, K, (T*)out);
+  kern<<<grid, SH::NT, smem, st>>>((const T*)src, ca, (const T*)Bt, cb, nbr, order, n_pos, K, (T*)out);
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;
 }
@@ -259,13 +303,14 @@ int launch(const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, 
 
 // Tile configurations, best first; the first whose LDS footprint fits is used.
 struct Cfg {
-  int wmb, wnb, stages;
+  int wmb, wnb, stages, nw;  // row blocks per wavefront, column blocks, LDS stages, wavefronts
 };
 
 template <typename T>
 size_t cfg_smem(const Cfg& c, int K) {
   const int VE = 16 / (int)sizeof(T), RV = 8 / VE;
-  return (size_t)c.stages * (4 * c.wmb + c.wnb) * RV * 1024 + 1024 + kMaxK * 5 + 16 + (size_t)K * 4 * c.wmb * 16 * 4;
+  return (size_t)c.stages * (c.nw * c.wmb + c.wnb) * RV * 1024 + 1024 + kMaxK * 5 + 16 +
+         (size_t)K * c.nw * c.wmb * 16 * 4;
 }
 
 int column_blocks(ssconv_dtype dt, int cb) {
@@ -277,8 +322,10 @@ int column_blocks(ssconv_dtype dt, int cb) {
 
 bool pick_cfg(ssconv_dtype dt, int cb, int K, Cfg* out) {
   const int wnb = column_blocks(dt, cb);
-  const Cfg f32[] = {{2, wnb, 3}, {1, wnb, 2}, {1, wnb, 3}};
-  const Cfg b16[] = {{2, wnb, 3}, {1, wnb, 3}};
+  // fp32: eight wavefronts of 16 rows (two per SIMD, so one issues MFMAs while the other waits on
+  // its DMAs, LDS reads or the barrier), else four of 32 or 16 rows
+  const Cfg f32[] = {{1, wnb, 3, 8}, {2, wnb, 3, 4}, {1, wnb, 3, 4}};
+  const Cfg b16[] = {{2, wnb, 3, 4}, {1, wnb, 3, 4}};
   const Cfg* list = dt == SSCONV_F32 ? f32 : b16;
   const int n = dt == SSCONV_F32 ? 3 : 2;
   for (int i = 0; i < n; ++i) {
@@ -291,19 +338,19 @@ bool pick_cfg(ssconv_dtype dt, int cb, int K, Cfg* out) {
   return false;
 }
 
-template <typename T, int WMB, int S>
+template <typename T, int WMB, int S, int NW>
 int launch_wnb(int wnb, const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, const int32_t* order,
                int64_t n_pos, int K, void* out, hipStream_t st) {
   switch (wnb) {
-    case 1: return launch<T, WMB, 1, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 2: return launch<T, WMB, 2, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 3: return launch<T, WMB, 3, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 4: return launch<T, WMB, 4, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 5: return launch<T, WMB, 5, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 6: return launch<T, WMB, 6, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 7: return launch<T, WMB, 7, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 8: return launch<T, WMB, 8, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    default: return launch<T, WMB, 13, S>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 1: return launch<T, WMB, 1, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 2: return launch<T, WMB, 2, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 3: return launch<T, WMB, 3, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 4: return launch<T, WMB, 4, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 5: return launch<T, WMB, 5, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 6: return launch<T, WMB, 6, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 7: return launch<T, WMB, 7, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 8: return launch<T, WMB, 8, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    default: return launch<T, WMB, 13, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
   }
 }
 
@@ -320,16 +367,16 @@ int gather_mfma(const void* src, ssconv_dtype dt, int ca, const void* Bt, int cb
   Cfg c;
   if (!pick_cfg(dt, cb, K, &c)) return fail(SSCONV_E_INVALID, "no gather tile fits the LDS for K=%d", K);
   const int64_t variant = debug_gather_variant();
-  if (variant == 1) c.wmb = 1, c.stages = 2;   // tuning override: one row block per wavefront, double buffer
-  if (variant == 2) c.wmb = 1, c.stages = 3;   // tuning override: one row block per wavefront, three stages
+  // tuning overrides (same results): 1 = four wavefronts of 32 rows, 2 = four of 16 rows
+  if (variant == 1 && cfg_smem<float>({2, c.wnb, 3, 4}, K) <= (size_t)kLdsLimit) c = {2, c.wnb, 3, 4};
+  if (variant == 2) c = {1, c.wnb, 3, 4};
   if (dt == SSCONV_F32) {
-    if (c.wmb == 2) return launch_wnb<float, 2, 3>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    if (c.stages == 2) return launch_wnb<float, 1, 2>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    return launch_wnb<float, 1, 3>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    if (c.nw == 8) return launch_wnb<float, 1, 3, 8>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    if (c.wmb == 2) return launch_wnb<float, 2, 3, 4>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    return launch_wnb<float, 1, 3, 4>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
   }
-  if (c.wmb == 2) return launch_wnb<uint16_t, 2, 3>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-  if (c.stages == 2) return launch_wnb<uint16_t, 1, 2>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-  return launch_wnb<uint16_t, 1, 3>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+  if (c.wmb == 2) return launch_wnb<uint16_t, 2, 3, 4>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+  return launch_wnb<uint16_t, 1, 3, 4>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
 }
 
 }  // namespace ssconv

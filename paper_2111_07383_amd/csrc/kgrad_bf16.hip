@@ -9,19 +9,25 @@
 // fixed order afterwards (deterministic, no atomics).
 //
 // v_mfma_f32_16x16x32_bf16 takes 8 consecutive PAIRS of one channel per lane, the transpose of
-// the row layout.  Rows of 32 pairs are DMA'd into LDS row-major (buffer_load ... lds on 32-bit
-// row offsets: the tail of a unit reads past the end of the buffer, which writes zeros) and the
-// operands are read with ds_read_b64_tr_b16: within a 16-lane group, output lane i / slot j
-// receives element i%4 of the 8 bytes addressed by source lane 4j + i/4, so source lane L
-// pointing at row (base + L/4), channel (c0 + 4*(L%4)) delivers pairs base..base+3 of channel
-// c0 + i; two such reads form one operand.  Rows are padded by one 16-byte granule so that the
-// four rows of a read fall in different banks.
+// the row layout.  A chunk of 32 pairs is staged in LDS per operand as 16-byte granule columns
+// of 32 rows each; one 1 KB DMA (buffer_load ... lds on 32-bit row offsets: the tail of a unit
+// reads past the end of the buffer, which writes zeros) fills granule column j with lanes 0-31
+// and column j + H with lanes 32-63 (H = half the columns), so a lane fetches the same pair row
+// in every DMA of a chunk: one pair-table read per chunk, and the DMAs of a chunk differ only in
+// an immediate offset.  DMA blocks are padded to 1088 bytes so that the two columns read
+// together (2i, 2i + 1) sit 16 banks apart.  The operands are read with ds_read_b64_tr_b16:
+// within a 16-lane group, output lane i / slot j receives element i%4 of the 8 bytes addressed
+// by source lane 4j + i/4, so source lane L pointing at row (base + L/4), channel
+// (c0 + 4*(L%4)) delivers pairs base..base+3 of channel c0 + i; two such reads form one operand.
 //
 // Pipeline (four LDS stages): iteration c waits for its own DMAs of chunk c+1, publishes them
-// with one barrier, then runs the MFMAs of chunk c with the transpose reads of chunk c+1, the
-// pair-table reads and the DMAs of chunk c+3 spread between them.  The unit's pair indices are
-// staged in LDS in blocks of 1024, double-buffered and DMA'd one block ahead.
+// with one barrier, then runs the MFMAs of chunk c with the transpose reads of chunk c+1 and the
+// DMAs of chunk c+3 spread between them.  Wavefronts 0-1 fetch grad_out rows, 2-3 feats rows.
+// The unit's pair indices are staged in LDS in blocks of 1024, double-buffered and DMA'd one
+// block ahead.
 #include <algorithm>
+#include <utility>
+#include <vector>
 
 #include "kgrad_mfma.hpp"
 #include "lds_dma.hpp"
@@ -41,27 +47,51 @@ constexpr int kPBLK = 1024;                // pair indices per staged block
 template <int W>
 struct KB {
   static constexpr int TW = 32 * W;                 // tile width in channels (each side)
-  static constexpr int GR = TW / 8;                 // 16-byte granules of one row segment
-  static constexpr int RS = GR + 1;                 // granules per LDS row (one pad granule)
-  static constexpr int NDMA = (32 * RS + 63) / 64;  // DMA instructions per operand per stage
-  static constexpr int OPB = NDMA * 1024;           // bytes per operand per stage
+  static constexpr int H = 2 * W;                   // DMA blocks per operand (two granule columns each)
+  static constexpr int BLK = 1024 + 64;             // bytes per DMA block (padded)
+  static constexpr int OPB = H * BLK;               // bytes per operand per stage
   static constexpr int STAGE = 2 * OPB;
-  static constexpr int PW = (2 * NDMA + 3) / 4;     // row DMAs per wavefront per stage
-  static constexpr int SMEM = kS * STAGE + 1024 + 2 * kPBLK * 8;
+  static constexpr int PW = W;                      // DMAs per wavefront per chunk
+  static_assert(W <= 7, "DMA immediate offsets are instantiated for up to 7 blocks per wavefront");
+  static constexpr int SMEM = kS * STAGE + 2 * kPBLK * 8;
 };
 
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"
+// 16 bytes per lane at byte offset off + IMM of the buffer rsrc into LDS at lds + IMM + 16 * lane
+// (the immediate offset applies to both addresses).
+template <int IMM>
 __device__ __forceinline__ void dma16_buf(__amdgpu_buffer_rsrc_t rsrc, uint32_t off, uint32_t lds) {
+  static_assert(IMM >= 0 && IMM < 4096, "MUBUF immediate offset");
   const uint32_t l = __builtin_amdgcn_readfirstlane(lds);
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" ::"s"(l), "v"(off), "s"(rsrc)
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen offset:%3 lds" ::"s"(l), "v"(off),
+               "s"(rsrc), "n"(IMM)
                : "memory", "m0");
 }
 #pragma clang diagnostic pop
 
-__device__ __forceinline__ s4 tr_read(const char* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) s4*)(uintptr_t)lds_addr(p));
+// dma16_buf with immediate offset 16 q; q is a constant once the callers' loops are unrolled
+__device__ __forceinline__ void dma16_buf_q(int q, __amdgpu_buffer_rsrc_t rsrc, uint32_t off, uint32_t lds) {
+  switch (q) {
+    case 0: dma16_buf<0>(rsrc, off, lds); break;
+    case 1: dma16_buf<16>(rsrc, off, lds); break;
+    case 2: dma16_buf<32>(rsrc, off, lds); break;
+    case 3: dma16_buf<48>(rsrc, off, lds); break;
+    case 4: dma16_buf<64>(rsrc, off, lds); break;
+    case 5: dma16_buf<80>(rsrc, off, lds); break;
+    default: dma16_buf<96>(rsrc, off, lds); break;
+  }
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs: launch index i runs on XCD i % 8, which
+// takes slot positions (i % 8) * ceil(n / 8) + i / 8, a contiguous range per XCD.
+__device__ __forceinline__ int xcd_slot(int i, int n) {
+  const int x = i & 7, j = i >> 3, q = n >> 3, r = n & 7;
+  return (x < r ? x * (q + 1) : r * (q + 1) + (x - r) * q) + j;
+}
+
+__device__ __forceinline__ s4 tr_read(uint32_t lds) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(uintptr_t)lds);
 }
 
 template <int W>
@@ -73,15 +103,15 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
   using C = KB<W>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   char* stages = smem;
-  char* junk = smem + kS * C::STAGE;
-  int2* pblk = reinterpret_cast<int2*>(junk + 1024);  // [2][kPBLK]
+  char* pblk = smem + kS * C::STAGE;  // [2][kPBLK] int2
   const int tid = threadIdx.x, lane = tid & 63, g = lane >> 4, r16 = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = w >> 1, wn = w & 1;
 
-  // work unit -> (offset s, slice of R_s), tile (mt, nt)
+  // launch slot -> work unit (XCD-contiguous over the row-sorted order) -> (offset s, slice of
+  // R_s), tile (mt, nt)
   const int tile = blockIdx.x % (mtiles * ntiles);
-  const int u = blockIdx.x / (mtiles * ntiles);
+  const int u = units.order[xcd_slot(blockIdx.x / (mtiles * ntiles), units.nunits)];
   int s = 0;
   while (s + 1 < units.K && units.uoff[s + 1] <= u) ++s;
   const int j = u - units.uoff[s], ns = units.uoff[s + 1] - units.uoff[s];
@@ -99,24 +129,19 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
   // the unit's pair list as a byte buffer (past its end: zeros, i.e. row 0 -- masked below)
   const __amdgpu_buffer_rsrc_t p_rsrc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<int2*>(pairs + beg), (short)0, npairs * 8, kBufferWord3);
-  const uint32_t stage0 = lds_addr(stages), junk_a = lds_addr(junk), pblk_a = lds_addr(pblk);
+  const uint32_t stage0 = lds_addr(stages), pblk_a = lds_addr(pblk);
 
-  // Row-DMA duty of this wavefront (q < PW): DMA d = w + 4q of the stage covers operand
-  // d / NDMA (0: grad_out, 1: feats) slots (d % NDMA) * 64 + lane = row * RS + granule.
-  int rowq[C::PW];
-  uint32_t goff[C::PW], pent[C::PW];
-  bool liveq[C::PW];
-#pragma unroll
-  for (int q = 0; q < C::PW; ++q) {
-    const int d = w + 4 * q;
-    const bool isF = d >= C::NDMA;
-    const int slot = (isF ? d - C::NDMA : d) * 64 + lane;
-    const int row = slot / C::RS, gran = slot % C::RS;
-    rowq[q] = row < 32 ? row : 0;
-    liveq[q] = d < 2 * C::NDMA && row < 32 && gran < C::GR;
-    pent[q] = (uint32_t)rowq[q] * 8u + (isF ? 4u : 0u);  // byte offset of this lane's index in a chunk's 32 pairs
-    goff[q] = (uint32_t)((isF ? n0 : m0) + 8 * gran) * 2u;
-  }
+  // DMA duty: wavefronts 0-1 fetch grad_out (operand 0), 2-3 feats (operand 1); wavefront w
+  // issues blocks jb .. jb + W - 1 of its operand, jb = W * (w % 2).  Lane l fetches pair row
+  // l % 32, granule column (block + H * (l / 32)).
+  const bool isF = w >= 2;
+  const int jb = W * (w & 1);
+  const int prow = lane & 31;
+  const __amdgpu_buffer_rsrc_t x_rsrc = isF ? f_rsrc : g_rsrc;
+  const uint32_t x_rowb = (uint32_t)(isF ? cin : cout) * 2u;
+  const uint32_t x_stat = (uint32_t)(isF ? n0 : m0) * 2u + 16u * (uint32_t)(jb + C::H * (lane >> 5));
+  const uint32_t m0_base = stage0 + (isF ? C::OPB : 0) + jb * C::BLK;  // + stage * STAGE + q * BLK
+  const uint32_t p_ent = (uint32_t)prow * 8u + (isF ? 4u : 0u);        // this lane's index in a chunk's pairs
 
   // pair block b (slice pairs [b*kPBLK, (b+1)*kPBLK)) into buffer b % 2: 8 KB per block, two
   // 1 KB DMAs per wavefront
@@ -124,42 +149,37 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
   do {                                                                                              \
     _Pragma("unroll") for (int i_ = 0; i_ < 2; ++i_) {                                              \
       const int blk_ = w + 4 * i_;                                                                  \
-      dma16_buf(p_rsrc, (uint32_t)((b_) * kPBLK * 8 + blk_ * 1024 + 16 * lane),                     \
-                pblk_a + ((b_) & 1) * kPBLK * 8 + blk_ * 1024);                                     \
+      dma16_buf<0>(p_rsrc, (uint32_t)((b_) * kPBLK * 8 + blk_ * 1024 + 16 * lane),                  \
+                   pblk_a + ((b_) & 1) * kPBLK * 8 + blk_ * 1024);                                  \
     }                                                                                               \
   } while (0)
 
-  // row index (into grad_out or feats, -1: none) of row DMA q of chunk c_, from the pair table.
-  // Pair k = c_*32 + row of the slice sits in buffer (c_ / 32) % 2 at entry (c_ % 32)*32 + row
-  // (32 chunks per block): a wave-uniform base plus this lane's constant pent[q].
-#define SSK_PAIR(dst_, q_, c_)                                                                      \
+  // byte offset of this lane's row in chunk c_ (kAbsent past the unit's end).  Pair k = c_*32 +
+  // row of the slice sits in buffer (c_ / 32) % 2 at entry (c_ % 32)*32 + row (32 chunks per block).
+#define SSK_ROW(dst_, c_)                                                                           \
   do {                                                                                              \
-    const uint32_t pb_ = pblk_a + ((uint32_t)(c_) >> 5 & 1u) * (kPBLK * 8) + ((uint32_t)(c_) & 31u) * 256u; \
-    const int v_ = *reinterpret_cast<const int*>(smem + (pb_ - lds_addr(smem)) + pent[q_]);         \
-    dst_ = (liveq[q_] && rowq[q_] < npairs - (c_) * 32) ? v_ : -1;                                  \
+    const uint32_t pb_ = ((uint32_t)(c_) >> 5 & 1u) * (kPBLK * 8) + ((uint32_t)(c_) & 31u) * 256u;  \
+    const int v_ = *reinterpret_cast<const int*>(pblk + pb_ + p_ent);                               \
+    dst_ = (prow < npairs - (c_) * 32) ? (uint32_t)v_ * x_rowb + x_stat : kAbsent;                  \
   } while (0)
 
-  // row DMA q into stage k_ of the row pr_ (from SSK_PAIR)
-#define SSK_DMA(q_, pr_, k_)                                                                        \
-  do {                                                                                              \
-    const int d_ = w + 4 * (q_);                                                                    \
-    const bool isF_ = d_ >= C::NDMA;                                                                \
-    const int dd_ = isF_ ? d_ - C::NDMA : d_;                                                       \
-    const uint32_t o_ = (pr_) >= 0 ? (uint32_t)(pr_) * (uint32_t)((isF_ ? cin : cout) * 2) + goff[q_] : kAbsent; \
-    dma16_buf(isF_ ? f_rsrc : g_rsrc, o_,                                                           \
-              d_ < 2 * C::NDMA ? stage0 + (k_) * C::STAGE + (isF_ ? C::OPB : 0) + dd_ * 1024 : junk_a); \
-  } while (0)
+  // DMA q of this wavefront (block jb + q) into stage k_, from row offset ro_.  The MUBUF
+  // immediate offset 16 q is added to the LDS address as well, so M0 is set 16 q bytes lower.
+#define SSK_DMA(q_, ro_, k_) dma16_buf_q(q_, x_rsrc, ro_, m0_base + (k_) * C::STAGE + (q_) * (C::BLK - 16))
 
-  // operands of the chunk in stage k_ via transpose reads: row base 8g + 4h + L/4, column 4(L%4)
-  const int rsel = 8 * g + (r16 >> 2), csel = 4 * (r16 & 3);
+  // operands of the chunk in stage k_ via transpose reads: rows 8g + 4h + L/4, channel
+  // (wm * W + i) * 16 + 4 (L % 4) -> granule column 2 (wm * W + i) + (L % 4) / 2, i.e. block
+  // 2i + (L % 4) / 2 and half wm (grad_out; feats: wn), byte 8 ((L % 4) % 2)
+  const uint32_t rd_lane =
+      (uint32_t)((((r16 & 3) >> 1) * C::BLK) + (8 * g + (r16 >> 2)) * 16 + ((r16 & 1) * 8));
+  const uint32_t rd_a = stage0 + wm * 512 + rd_lane, rd_b = stage0 + C::OPB + wn * 512 + rd_lane;
 #define SSK_READ(da_, db_, i_, k_)                                                                  \
   do {                                                                                              \
-    const char* sb_ = stages + (k_) * C::STAGE;                                                     \
-    const int ca_ = (wm * W + (i_)) * 16 + csel, cb_ = (wn * W + (i_)) * 16 + csel;                 \
-    const s4 a0_ = tr_read(sb_ + (rsel * C::RS) * 16 + ca_ * 2);                                    \
-    const s4 a1_ = tr_read(sb_ + ((rsel + 4) * C::RS) * 16 + ca_ * 2);                              \
-    const s4 b0_ = tr_read(sb_ + C::OPB + (rsel * C::RS) * 16 + cb_ * 2);                           \
-    const s4 b1_ = tr_read(sb_ + C::OPB + ((rsel + 4) * C::RS) * 16 + cb_ * 2);                     \
+    const uint32_t o_ = (k_) * C::STAGE + 2 * (i_) * C::BLK;                                        \
+    const s4 a0_ = tr_read(rd_a + o_);                                                              \
+    const s4 a1_ = tr_read(rd_a + o_ + 64);                                                         \
+    const s4 b0_ = tr_read(rd_b + o_);                                                              \
+    const s4 b1_ = tr_read(rd_b + o_ + 64);                                                         \
     da_[i_] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0_, a1_, 0, 1, 2, 3, 4, 5, 6, 7)); \
     db_[i_] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(b0_, b1_, 0, 1, 2, 3, 4, 5, 6, 7)); \
   } while (0)
@@ -189,14 +209,14 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
 #pragma unroll
   for (int c = 0; c < kS - 1; ++c)
     if (c < nchunk) {
+      uint32_t ro;
+      SSK_ROW(ro, c);
 #pragma unroll
-      for (int q = 0; q < L; ++q) {
-        int pr;
-        SSK_PAIR(pr, q, c);
-        SSK_DMA(q, pr, c);
-      }
+      for (int q = 0; q < L; ++q) SSK_DMA(q, ro, c);
     }
 
+  // The barrier of iteration c needs no LDS fence: the transpose reads of a chunk are consumed
+  // by its MFMAs before the next barrier, and its stage is refilled only two barriers later.
 #define SSK_BODY(k_, AC, BC, AN, BN)                                                                \
   if (c + (k_) < nchunk) {                                                                          \
     const int cc_ = c + (k_);                                                                       \
@@ -204,7 +224,7 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
       wait_vm<(kS - 3) * L>();                                                                      \
     else                                                                                            \
       wait_vm<0>();                                                                                 \
-    __syncthreads();                                                                                \
+    asm volatile("s_barrier" ::: "memory");                                                         \
     const bool rd_ = cc_ + 1 < nchunk;                                                              \
     const int ci_ = cc_ + kS - 1; /* chunk whose rows are issued now */                             \
     const bool iss_ = ci_ < nchunk;                                                                 \
@@ -213,16 +233,15 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
     if (iss_ && (ci_ % (kPBLK / 32)) == 0 && ci_ / (kPBLK / 32) + 1 < nblk)                         \
       SSK_PAIRS(ci_ / (kPBLK / 32) + 1);                                                            \
     constexpr int ks_ = ((k_) + kS - 1) % kS, kr_ = ((k_) + 1) % kS;                                \
-    int prq_[L];                                                                                    \
-    _Pragma("unroll") for (int q = 0; q < L; ++q) SSK_PAIR(prq_[q], q, ci_);                        \
+    uint32_t ro_ = kAbsent;                                                                         \
+    if (iss_) SSK_ROW(ro_, ci_);                                                                    \
     __builtin_amdgcn_sched_barrier(0);                                                              \
     _Pragma("unroll") for (int i = 0; i < W; ++i) {                                                 \
       _Pragma("unroll") for (int jj = 0; jj < W; ++jj)                                              \
         acc[i][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(AC[i], BC[jj], acc[i][jj], 0, 0, 0);   \
       __builtin_amdgcn_sched_barrier(0);                                                            \
       if (rd_) SSK_READ(AN, BN, i, kr_);                                                            \
-      _Pragma("unroll") for (int q = (i * L) / W; q < ((i + 1) * L) / W; ++q)                       \
-        if (iss_) SSK_DMA(q, prq_[q], ks_);                                                         \
+      if (iss_) SSK_DMA(i, ro_, ks_);                                                               \
       __builtin_amdgcn_sched_barrier(0);                                                            \
     }                                                                                               \
   }
@@ -235,6 +254,7 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
     for (int i = 0; i < W; ++i) SSK_READ(a0, b0, i, 0);
   }
   static_assert(kS == 4, "the unrolled chunk loop is written for four stages");
+  static_assert(L == W, "one DMA per row block of the MFMA loop");
   for (int c = 0; c < nchunk; c += kS) {
     SSK_BODY(0, a0, b0, a1, b1)
     SSK_BODY(1, a1, b1, a0, b0)
@@ -244,7 +264,7 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
 #undef SSK_BODY
 #undef SSK_READ
 #undef SSK_DMA
-#undef SSK_PAIR
+#undef SSK_ROW
 #undef SSK_PAIRS
 
   float* dst = part + (int64_t)u * cout * cin;
@@ -280,7 +300,7 @@ KgradUnits kgrad_units(const ssconv_rulebook* rb, int want) {
   const int K = rb->K;
   int64_t total = 0;
   for (int s = 0; s < K; ++s) total += rb->pair_off[s + 1] - rb->pair_off[s];
-  want = std::max(want, K);
+  want = std::min(std::max(want, K), kKgradMaxUnits);
   int n[kKgradMaxK];
   double rem[kKgradMaxK];
   int sum = 0;
@@ -299,9 +319,24 @@ KgradUnits kgrad_units(const ssconv_rulebook* rb, int want) {
     rem[best] -= 1.0;
     ++sum;
   }
+  while (sum > kKgradMaxUnits) {  // the one-unit minimum can overshoot: trim the largest offsets
+    int big = 0;
+    for (int s = 1; s < K; ++s)
+      if (n[s] > n[big]) big = s;
+    --n[big];
+    --sum;
+  }
   u.uoff[0] = 0;
   for (int s = 0; s < K; ++s) u.uoff[s + 1] = u.uoff[s] + n[s];
   u.nunits = u.uoff[K];
+  // launch order: by the centre of each unit's slice along R_s (pairs are sorted by output row),
+  // ties by offset -- a stable order, so the launch is deterministic
+  std::vector<std::pair<double, int>> key(u.nunits);
+  for (int s = 0; s < K; ++s)
+    for (int j = 0; j < n[s]; ++j) key[u.uoff[s] + j] = {(j + 0.5) / n[s], u.uoff[s] + j};
+  std::stable_sort(key.begin(), key.end(),
+                   [](const std::pair<double, int>& a, const std::pair<double, int>& b) { return a.first < b.first; });
+  for (int i = 0; i < u.nunits; ++i) u.order[i] = (uint16_t)key[i].second;
   return u;
 }
 

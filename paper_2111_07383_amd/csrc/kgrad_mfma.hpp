@@ -20,14 +20,20 @@ KgradPlan kgrad_plan(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int co
 
 // Work units of the bf16 kernel gradient: offset s owns units uoff[s] .. uoff[s+1]-1, which cut
 // its pair list R_s into near-equal slices (passed to the kernels by value).
+// Units are launched in `order`: sorted by the position of their slice along the output rows
+// and handed out XCD-contiguously, so the units of all offsets over one stretch of rows run on
+// one XCD together and share its L2 for the gathered rows.
 constexpr int kKgradMaxK = 125;  // ksize <= 5
+constexpr int kKgradMaxUnits = 512;
 struct KgradUnits {
   int K = 0, nunits = 0;
   int uoff[kKgradMaxK + 1] = {};
+  uint16_t order[kKgradMaxUnits] = {};
 };
 
-// Units for the rule book: about `want` in total (at least one per offset), distributed over the
-// offsets in proportion to their pair counts (largest remainders).
+// Units for the rule book: about `want` in total (at least one per offset, at most
+// kKgradMaxUnits), distributed over the offsets in proportion to their pair counts (largest
+// remainders), with their launch order.
 KgradUnits kgrad_units(const ssconv_rulebook* rb, int want);
 
 // bf16 tile width (in 32-channel steps of the 2x2 wavefront grid) for cin x cout.
