@@ -196,7 +196,8 @@ int ssconv_gate_backward(const ssconv_fields* fields /*host*/, const void* x, co
  * (0 restores automatic sizing); option 2 = make the N-th following device
  * allocation fail (0 disables); option 3 = kernel-selection override for
  * tuning sweeps and cross-checks (0 = automatic choice; 1, 2 = tile variants
- * of the generic gather-GEMM kernel; 5 = bf16 convolutions use the generic
+ * of the generic gather-GEMM kernel; 3 = the generic kernel keeps 32-bit
+ * neighbour indices in LDS; 5 = bf16 convolutions use the generic
  * gather-GEMM kernel instead of the bf16 pipeline kernel; 6 = the bf16 kernel
  * gradient uses per-offset splits instead of balanced work units; results
  * agree within the dtype's tolerance for every value); option 4 = kernel

@@ -284,10 +284,11 @@ int pick_wnb(int cb) {
 }
 
 template <typename T>
-int dispatch_gg(const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, int64_t n_rows, int K, void* out,
-                hipStream_t st) {
+int dispatch_gg(const void* src, int64_t n_src, int ca, const void* Bt, int cb, const int32_t* nbr, int64_t n_rows, int K,
+                void* out, hipStream_t st) {
   const ssconv_dtype dt = sizeof(T) == 4 ? SSCONV_F32 : SSCONV_BF16;
-  if (gather_mfma_supported(dt, ca, cb, K)) return gather_mfma(src, dt, ca, Bt, cb, nbr, nullptr, n_rows, K, out, st);
+  if (gather_mfma_supported(dt, ca, cb, K))
+    return gather_mfma(src, n_src, dt, ca, Bt, cb, nbr, nullptr, n_rows, K, out, st);
   switch (pick_wnb(cb)) {
     case 1: launch_gg<T, 1>(src, ca, Bt, cb, nbr, n_rows, K, out, st); break;
     case 2: launch_gg<T, 2>(src, ca, Bt, cb, nbr, n_rows, K, out, st); break;
@@ -351,7 +352,7 @@ int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_ruleb
   if (rb->n_out == 0) return SSCONV_OK;
   if (dt == SSCONV_F32) {
     KernelTimer timer(st);
-    return dispatch_gg<float>(feats, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st);
+    return dispatch_gg<float>(feats, rb->n_in, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st);
   }
   if (use_bf16_kernel(dt, rb->n_in, cin, cout, rb->K)) {
     // kappa packed for the bf16 kernel in a stream-ordered scratch buffer
@@ -366,7 +367,7 @@ int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_ruleb
     return rc;
   }
   KernelTimer timer(st);
-  return dispatch_gg<uint16_t>(feats, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st);
+  return dispatch_gg<uint16_t>(feats, rb->n_in, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st);
 }
 
 int dw_nsplit(const ssconv_rulebook* rb) {
@@ -428,7 +429,7 @@ int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout
     transpose_kernel<float><<<cdiv(nw, 256), 256, 0, st>>>((const float*)W, K, cout, cin, (float*)Wt);
     SSC_HIP(hipGetLastError());
     KernelTimer timer(st);
-    return dispatch_gg<float>(grad_out, cout, Wt, cin, nbrT, rb->n_in, K, grad_feats, st);
+    return dispatch_gg<float>(grad_out, rb->n_out, cout, Wt, cin, nbrT, rb->n_in, K, grad_feats, st);
   }
   if (use_bf16_kernel(dt, rb->n_out, cout, cin, K)) {
     // kappa^T packed for the bf16 kernel: Bp[s][o/8][i][o%8] = W[s][o][i]
@@ -439,7 +440,7 @@ int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout
   transpose_kernel<uint16_t><<<cdiv(nw, 256), 256, 0, st>>>((const uint16_t*)W, K, cout, cin, (uint16_t*)Wt);
   SSC_HIP(hipGetLastError());
   KernelTimer timer(st);
-  return dispatch_gg<uint16_t>(grad_out, cout, Wt, cin, nbrT, rb->n_in, K, grad_feats, st);
+  return dispatch_gg<uint16_t>(grad_out, rb->n_out, cout, Wt, cin, nbrT, rb->n_in, K, grad_feats, st);
 }
 
 int conv_backward_dw(const void* feats, const void* grad_out, ssconv_dtype dt, int cin, int cout,

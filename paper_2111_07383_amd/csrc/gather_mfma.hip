@@ -76,7 +76,15 @@ struct Shape {
   static constexpr int L = (WMB + BJ) * RV;              // DMA loads per wavefront per stage
 };
 
-template <typename T, int WMB, int WNB, int S, int NW>
+// Neighbour-index table entries: 32-bit, or 16-bit (0xFFFF = none) when the source has fewer than
+// 65535 rows, which halves the table for large offset counts.
+template <typename IX>
+__device__ __forceinline__ int ix_get(IX v) {
+  if constexpr (sizeof(IX) == 2) return v == (IX)0xFFFF ? -1 : (int)v;
+  return (int)v;
+}
+
+template <typename T, int WMB, int WNB, int S, int NW, typename IX>
 __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restrict__ src, int ca,
                                                           const T* __restrict__ Bt, int cb,
                                                           const int32_t* __restrict__ nbr,
@@ -91,7 +99,7 @@ __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restric
   uint32_t* bmask = reinterpret_cast<uint32_t*>(junk + 1024);                  // [kMaxK]
   uint8_t* act = reinterpret_cast<uint8_t*>(bmask + kMaxK);                    // [kMaxK]
   int* n_act_p = reinterpret_cast<int*>(act + kMaxK);                          // [4]
-  int32_t* idx_tab = n_act_p + 4;                                              // [K][BM]
+  IX* idx_tab = reinterpret_cast<IX*>(n_act_p + 4);                            // [K][BM]
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, r16 = lane & 15;
   const int64_t p0 = (int64_t)blockIdx.x * BM;
@@ -104,7 +112,7 @@ __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restric
     for (int j = 0; j < BM / 64; ++j) {
       const int64_t p = p0 + 64 * j + lane;
       const int idx = p < n_pos ? nbr[(int64_t)s * n_pos + p] : -1;
-      idx_tab[s * BM + 64 * j + lane] = idx;
+      idx_tab[s * BM + 64 * j + lane] = (IX)idx;
       const uint64_t b = __ballot(idx >= 0);
 #pragma unroll
       for (int q = 0; q < 4; ++q)
@@ -146,7 +154,7 @@ __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restric
     const bool live_ = r_slot < n_act;                                                              \
     const int s_ = live_ ? act[r_slot] : 0;                                                         \
     _Pragma("unroll") for (int mb = 0; mb < WMB; ++mb) {                                            \
-      const int idx_ = live_ ? idx_tab[s_ * BM + 16 * (w * WMB + mb) + r16] : -1;                   \
+      const int idx_ = live_ ? ix_get(idx_tab[s_ * BM + 16 * (w * WMB + mb) + r16]) : -1;           \
       alive[mb] = idx_ >= 0;                                                                        \
       ap[mb] = alive[mb] ? src + (int64_t)idx_ * ca + r_ch : zero;                                  \
     }                                                                                               \
@@ -213,16 +221,17 @@ __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restric
 #pragma unroll
     for (int nb = 0; nb < WNB; ++nb) acc[mb][nb] = f4{0.f, 0.f, 0.f, 0.f};
 
-  // Software pipeline over the chunks (S stages): iteration c waits for this wavefront's DMAs of
-  // chunk c+1, publishes them with one barrier, then runs the MFMAs of chunk c (fragments already
+  // Software pipeline over the chunks (S = 3 or 4 stages): iteration c waits for this wavefront's
+  // DMAs of chunk c+1 (chunk c+2's may stay in flight with four stages), publishes them with one
+  // barrier, then runs the MFMAs of chunk c (fragments already
   // in registers) one column block at a time, with the fragment reads of chunk c+1 and the DMAs
   // of chunk c+S-1 spread between the blocks.  The stage refilled in iteration c held chunk c-1,
   // whose fragments were consumed by the MFMAs of iteration c-1, before this barrier.
-  static_assert(S == 3, "the pipelined chunk loop is written for three stages");
+  static_assert(S == 3 || S == 4, "the pipelined chunk loop is written for three or four stages");
   for (int c = 0; c < S - 1 && c < nchunk; ++c) SSC_ISSUE(c);
   uint4 fa0[WMB][RV], fb0[WNB][RV], fa1[WMB][RV], fb1[WNB][RV];
   if (nchunk > 0) {
-    if (nchunk > 1) wait_vm<L>(); else wait_vm<0>();
+    if (nchunk >= S - 1) wait_vm<L * (S - 2)>(); else wait_vm<0>();
     __syncthreads();
 #pragma unroll
     for (int u = 0; u < NR; ++u) SSC_FRAG(fa0, fb0, u, stages);
@@ -231,7 +240,10 @@ __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restric
   {                                                                                                 \
     const int cc_ = c + (k_);                                                                       \
     if (cc_ >= nchunk) break;                                                                       \
-    wait_vm<0>();                                                                                   \
+    if (cc_ + S - 2 < nchunk)                                                                       \
+      wait_vm<L * (S - 3)>();                                                                       \
+    else                                                                                            \
+      wait_vm<0>();                                                                                 \
     __syncthreads();                                                                                \
     const bool rd_ = cc_ + 1 < nchunk;                                                              \
     const bool iss_ = cc_ + S - 1 < nchunk;                                                         \
@@ -281,18 +293,18 @@ __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restric
   }
 }
 
-template <typename T, int WMB, int WNB, int S, int NW>
+template <typename T, int WMB, int WNB, int S, int NW, typename IX>
 size_t smem_bytes(int K) {
   using SH = Shape<T, WMB, WNB, S, NW>;
-  return (size_t)S * SH::STAGE + 1024 + kMaxK * 5 + 16 + (size_t)K * SH::BM * 4;
+  return (size_t)S * SH::STAGE + 1024 + kMaxK * 5 + 16 + (size_t)K * SH::BM * sizeof(IX);
 }
 
-template <typename T, int WMB, int WNB, int S, int NW>
+template <typename T, int WMB, int WNB, int S, int NW, typename IX>
 int launch(const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, const int32_t* order, int64_t n_pos,
            int K, void* out, hipStream_t st) {
   using SH = Shape<T, WMB, WNB, S, NW>;
-  const size_t smem = smem_bytes<T, WMB, WNB, S, NW>(K);
-  auto kern = gather_mfma_kernel<T, WMB, WNB, S, NW>;
+  const size_t smem = smem_bytes<T, WMB, WNB, S, NW, IX>(K);
+  auto kern = gather_mfma_kernel<T, WMB, WNB, S, NW, IX>;
   SSC_HIP(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem));
   dim3 grid(cdiv(n_pos, SH::BM), cdiv(cb, SH::BN));
   kern<<<grid, SH::NT, smem, st>>>((const T*)src, ca, (const T*)Bt, cb, nbr, order, n_pos, K, (T*)out);
@@ -304,13 +316,14 @@ int launch(const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, 
 // Tile configurations, best first; the first whose LDS footprint fits is used.
 struct Cfg {
   int wmb, wnb, stages, nw;  // row blocks per wavefront, column blocks, LDS stages, wavefronts
+  bool idx16;                // 16-bit neighbour-index table
 };
 
 template <typename T>
 size_t cfg_smem(const Cfg& c, int K) {
   const int VE = 16 / (int)sizeof(T), RV = 8 / VE;
   return (size_t)c.stages * (c.nw * c.wmb + c.wnb) * RV * 1024 + 1024 + kMaxK * 5 + 16 +
-         (size_t)K * c.nw * c.wmb * 16 * 4;
+         (size_t)K * c.nw * c.wmb * 16 * (c.idx16 ? 2 : 4);
 }
 
 int column_blocks(ssconv_dtype dt, int cb) {
@@ -320,15 +333,18 @@ int column_blocks(ssconv_dtype dt, int cb) {
   return (blocks + tiles - 1) / tiles;  // fp32: at most 8 column blocks per tile
 }
 
-bool pick_cfg(ssconv_dtype dt, int cb, int K, Cfg* out) {
+bool pick_cfg(ssconv_dtype dt, int cb, int K, int64_t n_src, Cfg* out) {
   const int wnb = column_blocks(dt, cb);
   // fp32: eight wavefronts of 16 rows (two per SIMD, so one issues MFMAs while the other waits on
-  // its DMAs, LDS reads or the barrier), else four of 32 or 16 rows
-  const Cfg f32[] = {{1, wnb, 3, 8}, {2, wnb, 3, 4}, {1, wnb, 3, 4}};
-  const Cfg b16[] = {{2, wnb, 3, 4}, {1, wnb, 3, 4}};
+  // its DMAs, LDS reads or the barrier), four stages where the LDS allows, else four wavefronts
+  // of 32 or 16 rows; a 16-bit index table when the source has fewer than 65535 rows
+  const Cfg f32[] = {{1, wnb, 4, 8, true}, {1, wnb, 3, 8, true}, {1, wnb, 3, 8, false},
+                     {2, wnb, 3, 4, false}, {1, wnb, 3, 4, false}};
+  const Cfg b16[] = {{2, wnb, 3, 4, false}, {1, wnb, 3, 4, false}};
   const Cfg* list = dt == SSCONV_F32 ? f32 : b16;
-  const int n = dt == SSCONV_F32 ? 3 : 2;
+  const int n = dt == SSCONV_F32 ? 5 : 2;
   for (int i = 0; i < n; ++i) {
+    if (list[i].idx16 && n_src >= 0xFFFF) continue;
     const size_t need = dt == SSCONV_F32 ? cfg_smem<float>(list[i], K) : cfg_smem<uint16_t>(list[i], K);
     if (need <= (size_t)kLdsLimit) {
       *out = list[i];
@@ -338,45 +354,51 @@ bool pick_cfg(ssconv_dtype dt, int cb, int K, Cfg* out) {
   return false;
 }
 
-template <typename T, int WMB, int S, int NW>
+template <typename T, int WMB, int S, int NW, typename IX>
 int launch_wnb(int wnb, const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, const int32_t* order,
                int64_t n_pos, int K, void* out, hipStream_t st) {
   switch (wnb) {
-    case 1: return launch<T, WMB, 1, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 2: return launch<T, WMB, 2, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 3: return launch<T, WMB, 3, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 4: return launch<T, WMB, 4, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 5: return launch<T, WMB, 5, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 6: return launch<T, WMB, 6, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 7: return launch<T, WMB, 7, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 8: return launch<T, WMB, 8, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    default: return launch<T, WMB, 13, S, NW>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 1: return launch<T, WMB, 1, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 2: return launch<T, WMB, 2, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 3: return launch<T, WMB, 3, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 4: return launch<T, WMB, 4, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 5: return launch<T, WMB, 5, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 6: return launch<T, WMB, 6, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 7: return launch<T, WMB, 7, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 8: return launch<T, WMB, 8, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    default: return launch<T, WMB, 13, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
   }
 }
 
 }  // namespace
 
 bool gather_mfma_supported(ssconv_dtype dt, int ca, int cb, int K) {
-  Cfg c;
-  return ca % 8 == 0 && ca >= 8 && K <= kMaxK && pick_cfg(dt, cb, K, &c);
+  Cfg c;  // the 32-bit index table fits whenever any configuration does
+  return ca % 8 == 0 && ca >= 8 && K <= kMaxK && pick_cfg(dt, cb, K, INT64_MAX, &c);
 }
 
-int gather_mfma(const void* src, ssconv_dtype dt, int ca, const void* Bt, int cb, const int32_t* nbr,
+int gather_mfma(const void* src, int64_t n_src, ssconv_dtype dt, int ca, const void* Bt, int cb, const int32_t* nbr,
                 const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st) {
   if (n_pos == 0) return SSCONV_OK;
-  Cfg c;
-  if (!pick_cfg(dt, cb, K, &c)) return fail(SSCONV_E_INVALID, "no gather tile fits the LDS for K=%d", K);
+  // tuning overrides (same results): 1 = four wavefronts of 32 rows, 2 = four of 16 rows,
+  // 3 = no 16-bit index table
   const int64_t variant = debug_gather_variant();
-  // tuning overrides (same results): 1 = four wavefronts of 32 rows, 2 = four of 16 rows
-  if (variant == 1 && cfg_smem<float>({2, c.wnb, 3, 4}, K) <= (size_t)kLdsLimit) c = {2, c.wnb, 3, 4};
-  if (variant == 2) c = {1, c.wnb, 3, 4};
+  Cfg c;
+  if (!pick_cfg(dt, cb, K, variant == 3 ? INT64_MAX : n_src, &c))
+    return fail(SSCONV_E_INVALID, "no gather tile fits the LDS for K=%d", K);
+  if (variant == 1 && cfg_smem<float>({2, c.wnb, 3, 4, false}, K) <= (size_t)kLdsLimit) c = {2, c.wnb, 3, 4, false};
+  if (variant == 2) c = {1, c.wnb, 3, 4, false};
+#define SSC_GO(T, WMB, S, NW, IX) return launch_wnb<T, WMB, S, NW, IX>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st)
   if (dt == SSCONV_F32) {
-    if (c.nw == 8) return launch_wnb<float, 1, 3, 8>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    if (c.wmb == 2) return launch_wnb<float, 2, 3, 4>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    return launch_wnb<float, 1, 3, 4>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    if (c.nw == 8 && c.idx16 && c.stages == 4) SSC_GO(float, 1, 4, 8, uint16_t);
+    if (c.nw == 8 && c.idx16) SSC_GO(float, 1, 3, 8, uint16_t);
+    if (c.nw == 8) SSC_GO(float, 1, 3, 8, int32_t);
+    if (c.wmb == 2) SSC_GO(float, 2, 3, 4, int32_t);
+    SSC_GO(float, 1, 3, 4, int32_t);
   }
-  if (c.wmb == 2) return launch_wnb<uint16_t, 2, 3, 4>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-  return launch_wnb<uint16_t, 1, 3, 4>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+  if (c.wmb == 2) SSC_GO(uint16_t, 2, 3, 4, int32_t);
+  SSC_GO(uint16_t, 1, 3, 4, int32_t);
+#undef SSC_GO
 }
 
 }  // namespace ssconv

@@ -137,3 +137,22 @@ def test_forward_backward_deterministic():
     assert torch.equal(rb2.pairs(), rb.pairs())
     rb.close()
     rb2.close()
+
+
+@pytest.mark.parametrize("i,variant", [(2, 1), (2, 2), (2, 3), (3, 3), (4, 5), (4, 6)])
+def test_kernel_selection_overrides(i, variant):
+    """Every alternative kernel configuration (forced from the host) stays within tolerance."""
+    print(f"config {i} kernel variant {variant}", flush=True)
+    L, dt, desc, basis, rb, W, feats = _layer_io(i)
+    want, g, d_in, dw = single_layer_reference(i)
+    P.debug_set(3, variant)
+    try:
+        out = P.forward(feats, rb, W).float().cpu().numpy()
+        gf, gc = P.backward(feats, _tensor(g, dt), rb, W, desc, basis)
+    finally:
+        P.debug_set(3, 0)
+    tol = TOL[CONFIGS[i].dtype]
+    errs = rel_err(out, want), rel_err(gf.float().cpu().numpy(), d_in), rel_err(gc.cpu().numpy(), dw)
+    print(f"config {i} variant {variant} errors {errs}", flush=True)
+    assert max(errs) < tol
+    rb.close()
