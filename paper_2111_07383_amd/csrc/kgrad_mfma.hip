@@ -299,11 +299,11 @@ KgradPlan kgrad_plan(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int co
   }
   int64_t mx = 1;
   for (int s = 0; s < rb->K; ++s) mx = std::max(mx, rb->pair_off[s + 1] - rb->pair_off[s]);
-  // fp32: about 4096 wavefronts; bf16: about 512 workgroups.  At least 256 pairs per slice,
-  // at most 64 slices.
+  // fp32: at most 4096 wavefronts, i.e. two full rounds of the 2048 wavefront slots (256 CUs x
+  // two four-wavefront workgroups): rounding up would start a third, nearly empty round.  bf16:
+  // about 512 workgroups.  At least 256 pairs per slice, at most 64 slices.
   const int64_t tiles = (int64_t)rb->K * p.mtiles * p.ntiles;
-  const int64_t want = dt == SSCONV_F32 ? 4096 : 512;
-  int64_t ns = (want + tiles - 1) / tiles;
+  int64_t ns = dt == SSCONV_F32 ? 4096 / tiles : (512 + tiles - 1) / tiles;
   ns = std::min<int64_t>(ns, std::max<int64_t>(1, mx / 256));
   p.nsplit = (int)std::max<int64_t>(1, std::min<int64_t>(ns, 64));
   return p;
