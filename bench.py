@@ -196,8 +196,10 @@ class SingleLayer:
         self.grad = torch.from_numpy(make_grad(spec, self.n_out, self.L.cout)).to(dev).to(self.dt)
         rb = P.Rulebook(self.coords, spec.grid, self.L.ksize, self.L.stride, self.L.submanifold)
         ws = P.backward_workspace_size(rb, self.dt, self.L.cin, self.L.cout)
+        self.hash_cap = int(rb.hash_slots(0).shape[0])
         rb.close()
         self.ws = torch.empty((ws,), dtype=torch.uint8, device=dev)
+        self.events = None      # per-step [rulebook, synth, forward, backward] boundaries when set
 
     def forward_only(self):
         P, torch = self.P, self.torch
@@ -209,12 +211,60 @@ class SingleLayer:
         P.forward(self.feats, self._rb, self._W, out=self._out)
 
     def step(self):
-        P, L = self.P, self.L
+        P, L, torch = self.P, self.L, self.torch
+        ev = None
+        if self.events is not None:
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+            self.events.append(ev)
+            ev[0].record()
         rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, L.stride, L.submanifold)
+        if ev:
+            ev[1].record()
         W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt)
+        if ev:
+            ev[2].record()
         out = P.forward(self.feats, rb, W)
+        if ev:
+            ev[3].record()
         P.backward(self.feats, self.grad, rb, W, self.desc, self.basis, n_coeff=self.n_coeff, workspace=self.ws)
+        if ev:
+            ev[4].record()
         rb.close()
+        return out
+
+    def phase_report(self):
+        """Per-phase medians of the timed steps against each phase's roofline time, as defined for
+        the layer: rule book and synthesis bound by HBM bytes, each GEMM phase by the larger of
+        useful FLOPs / MFMA peak and algorithmic bytes / HBM peak."""
+        if not self.events:
+            return None
+        L, K = self.L, self.L.ksize ** 3
+        t = np.array([[a.elapsed_time(b) for a, b in zip(ev, ev[1:])] for ev in self.events])  # ms
+        med = np.median(t, 0)
+        b = 2 if self.spec.dtype == "bf16" else 4
+        n_in, n_out, P_ = int(self.coords.shape[0]), int(self.n_out), int(self.n_pairs)
+        peak = PEAK[self.spec.dtype] * 1e12
+        hbm = HBM_PEAK_GBS * 1e9
+        flops = 2.0 * P_ * L.cin * L.cout
+        w_bytes = K * L.cin * L.cout * b
+        rb_bytes = 16 * n_in + 8 * self.hash_cap + 8 * n_in + 12 * n_out * K + 8 * P_
+        synth_bytes = w_bytes + 4 * int(self.basis.numel()) + 4 * int(self.n_coeff)
+        gemm_bytes = n_in * L.cin * b + n_out * L.cout * b + w_bytes + 4 * P_
+        dw_bytes = n_in * L.cin * b + n_out * L.cout * b + 8 * P_ + K * L.cin * L.cout * 4
+        roof = [rb_bytes / hbm, synth_bytes / hbm, max(flops / peak, gemm_bytes / hbm),
+                max(flops / peak, gemm_bytes / hbm) + max(flops / peak, dw_bytes / hbm)]
+        names = ["rulebook", "synth", "forward", "backward"]
+        out = {n: {"ms": float(m), "roofline_ms": float(r) * 1e3, "frac": float(r * 1e3 / m)}
+               for n, m, r in zip(names, med, roof)}
+        layer_ms = float(med[:3].sum())
+        layer_roof = float(sum(roof[:3])) * 1e3
+        out["layer"] = {"what": "rulebook+synth+forward", "ms": layer_ms, "roofline_ms": layer_roof,
+                        "frac": layer_roof / layer_ms, "M_sites_per_s": n_out / layer_ms / 1e3}
+        out["forward"]["M_sites_per_s"] = n_out / float(med[2]) / 1e3
+        out["backward"]["M_sites_per_s"] = n_out / float(med[3]) / 1e3
+        step = t.sum(1)
+        out["step_ms"] = {"p10": float(np.percentile(step, 10)), "median": float(np.median(step)),
+                          "p90": float(np.percentile(step, 90))}
         return out
 
     def sites(self):
@@ -410,6 +460,8 @@ def main():
     log(f"warmup done ({args.warmup} steps); timing {args.steps} steps")
     import paper_2111_07383_amd as P
     P.debug_set(4, 1)                 # HIP events around each gather-GEMM launch, on its stream
+    if args.only == "step" and isinstance(b, SingleLayer):
+        b.events = []                 # phase boundaries of every timed step (torch's stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
@@ -441,6 +493,11 @@ def main():
                        "launches_timed": n_timed, "algorithmic_flops_per_launch": flops_launch,
                        "kernel_ms_per_step": kern_ms / args.steps}
     log(f"gather-GEMM: {n_timed} launches, {avg_ms:.4f} ms avg, {achieved:.1f} TFLOP/s")
+    if isinstance(b, SingleLayer) and b.events:
+        out["phases"] = b.phase_report()
+        ph = out["phases"]
+        log("phases (median ms / roofline fraction): " +
+            ", ".join(f"{k} {ph[k]['ms']:.3f}/{ph[k]['frac']:.2f}" for k in ("rulebook", "synth", "forward", "backward", "layer")))
     if not args.no_cpu_baseline and args.config != 5:
         log("timing the CPU oracle on a bounded sample")
         out["cpu_baseline"] = cpu_baseline(args.config, args.cpu_budget)

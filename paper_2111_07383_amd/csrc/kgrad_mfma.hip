@@ -5,13 +5,17 @@
 // a GEMM per offset whose reduction runs over the compact pair list R_s.
 //
 // fp32 (v_mfma_f32_16x16x4f32): the A operand of lane l is A[m = l%16][k = l/16]
-// and the B operand B[k = l/16][n = l%16], so the 16 lanes of a lane group read 16
-// consecutive channels (64 bytes) of ONE gathered row -- both operands come straight
-// from global memory in MFMA layout, with no LDS and no transposition.  Each
+// and the B operand B[k = l/16][n = l%16], so a step of the reduction takes 4 pairs
+// and each lane group reads 16 consecutive channels of ONE gathered row.  Each
 // wavefront owns a (16*WMB out channels) x (16*WNB in channels) tile of one offset
-// and a contiguous slice of its pairs; pair indices are fetched two steps ahead
-// and rows one step ahead of the MFMAs.  Every slice writes its own partial tile;
-// the partials are summed in a fixed order afterwards (deterministic, no atomics).
+// and a contiguous slice of its pairs, and stages the rows of its steps in a
+// private LDS ring (four steps deep, no barriers): one 1 KB DMA (buffer_load ...
+// lds) fetches 16 granules of 4 channels of all 4 pairs of a step, pair-minor, so a
+// lane fetches the same pair row in every DMA of a step and reads its operands
+// without bank conflicts; the slice's pair indices are staged 128 at a time.
+// Every slice writes its own partial tile; the partials are summed in a fixed order
+// afterwards (deterministic, no atomics).  Sources of 2 GB or more use a variant
+// that loads the rows straight into registers one step ahead.
 //
 // bf16 (v_mfma_f32_16x16x32_bf16): each lane's operand holds 8 consecutive PAIRS of
 // one channel, i.e. the transpose of the row layout.  Gathered rows are DMA'd
@@ -269,6 +273,183 @@ int tile_blocks(int c) {
 
 int round_wb(int b) { return b <= 1 ? 1 : b <= 2 ? 2 : b <= 4 ? 4 : b <= 7 ? 7 : 8; }
 
+// ---------------------------------------------------------------------------
+// fp32 with a per-wavefront LDS ring
+// ---------------------------------------------------------------------------
+constexpr uint32_t kAbsentRow = 0x80000000u;  // byte offset past any buffer: the DMA writes zeros
+constexpr int kBufWord3 = 0x00020000;         // buffer descriptor word 3 for gfx9-family raw loads
+constexpr int kFD = 4;                        // LDS stages (steps of 4 pairs) per wavefront
+
+template <int WMB, int WNB>
+struct KF {
+  static constexpr int LG = (WMB + 3) / 4;        // grad_out DMAs per step (16 granules each)
+  static constexpr int LF = (WNB + 3) / 4;        // feats DMAs per step
+  static constexpr int L = LG + LF;
+  static constexpr int STEP = L * 1024;           // LDS bytes per step
+  static constexpr int WAVE = 2 * 1024 + kFD * STEP;  // pair ring (2 x 128 pairs) + stages
+  static constexpr int SMEM = 4 * WAVE;
+};
+
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// 16 bytes per lane from byte offset off + IMM of the buffer rsrc into LDS at lds + 16 * lane.  The
+// MUBUF immediate offset is added to the LDS address as well, so M0 is set IMM bytes lower.
+template <int IMM>
+__device__ __forceinline__ void dma_buf_imm(__amdgpu_buffer_rsrc_t rsrc, uint32_t off, uint32_t lds) {
+  static_assert(IMM >= 0 && IMM < 4096, "MUBUF immediate offset");
+  const uint32_t l = __builtin_amdgcn_readfirstlane(lds - IMM);
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen offset:%3 lds" ::"s"(l), "v"(off),
+               "s"(rsrc), "n"(IMM)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// DMA block j (0 or 1) of a step: channels 64 j .. 64 j + 63 of the tile
+__device__ __forceinline__ void dma_blk(int j, __amdgpu_buffer_rsrc_t rsrc, uint32_t off, uint32_t lds) {
+  if (j == 0)
+    dma_buf_imm<0>(rsrc, off, lds);
+  else
+    dma_buf_imm<256>(rsrc, off, lds);
+}
+
+template <int WMB, int WNB>
+__global__ __launch_bounds__(256) void kgrad_f32_lds_kernel(const float* __restrict__ G, int64_t g_rows, int cout,
+                                                            const float* __restrict__ F, int64_t f_rows, int cin,
+                                                            const int2* __restrict__ pairs,
+                                                            const int64_t* __restrict__ pair_off, int K, int mtiles,
+                                                            int ntiles, int nsplit, float* __restrict__ part) {
+  using C = KF<WMB, WNB>;
+  static_assert(C::LG <= 2 && C::LF <= 2, "at most two DMA blocks per operand");
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int lane = threadIdx.x & 63, g = lane >> 4, r16 = lane & 15;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int64_t task = (int64_t)blockIdx.x * 4 + w;
+  const int64_t ntask = (int64_t)K * nsplit * mtiles * ntiles;
+  if (task >= ntask) return;  // whole wavefront; the kernel has no barriers
+  const int nt = (int)(task % ntiles);
+  const int mt = (int)((task / ntiles) % mtiles);
+  const int split = (int)((task / ((int64_t)ntiles * mtiles)) % nsplit);
+  const int s = (int)(task / ((int64_t)ntiles * mtiles * nsplit));
+  const int m0 = mt * 16 * WMB, n0 = nt * 16 * WNB;
+  const int64_t off = pair_off[s], cnt = pair_off[s + 1] - off;
+  const int64_t beg = off + cnt * split / nsplit, end = off + cnt * (split + 1) / nsplit;
+  const int npairs = (int)(end - beg);
+  const int nstep = (npairs + 3) / 4;
+
+  char* const wl = smem + w * C::WAVE;  // [2][128] int2 pair ring, then kFD stages
+  const uint32_t pr_a = lds_addr(wl), st_a = pr_a + 2048;
+  const __amdgpu_buffer_rsrc_t g_rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(G), (short)0, (int)(g_rows * cout * 4), kBufWord3);
+  const __amdgpu_buffer_rsrc_t f_rsrc =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(F), (short)0, (int)(f_rows * cin * 4), kBufWord3);
+  const __amdgpu_buffer_rsrc_t p_rsrc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int2*>(pairs + beg), (short)0, npairs * 8, kBufWord3);
+
+  // DMA lane l: pair l % 4 of the step, granule (4 channels) l / 4 of the DMA block
+  const int pl = lane & 3, gl = lane >> 2;
+  const uint32_t g_stat = (uint32_t)(m0 + 4 * gl) * 4u, f_stat = (uint32_t)(n0 + 4 * gl) * 4u;
+  const uint32_t g_rowb = (uint32_t)cout * 4u, f_rowb = (uint32_t)cin * 4u;
+  // operand reads: lane (r16, g) takes channel 16 mb + r16 of pair g -> granule 4 mb + r16 / 4
+  const uint32_t rd_lane = (uint32_t)((r16 >> 2) * 64 + g * 16 + (r16 & 3) * 4);
+  const int nblk = (npairs + 127) / 128;
+
+#define KF_PAIRS(b_) dma_buf_imm<0>(p_rsrc, (uint32_t)(b_) * 1024u + 16u * lane, pr_a + ((b_) & 1) * 1024)
+
+  // step t_: refill the pair ring when entering a new block of 32 steps, look up this lane's pair,
+  // then the step's DMAs into stage t_ % kFD
+#define KF_ISSUE(t_)                                                                                \
+  do {                                                                                              \
+    if (((t_) & 31) == 0 && (t_) > 0 && ((t_) >> 5) + 1 < nblk) KF_PAIRS(((t_) >> 5) + 1);          \
+    const int pi_ = 4 * (t_) + pl;                                                                  \
+    const int2 pv_ = *reinterpret_cast<const int2*>(wl + ((pi_ >> 7) & 1) * 1024 + (pi_ & 127) * 8);\
+    const bool ok_ = pi_ < npairs;                                                                  \
+    const uint32_t gb_ = ok_ ? (uint32_t)pv_.x * g_rowb + g_stat : kAbsentRow;                      \
+    const uint32_t fb_ = ok_ ? (uint32_t)pv_.y * f_rowb + f_stat : kAbsentRow;                      \
+    const uint32_t sb_ = st_a + ((t_) % kFD) * C::STEP;                                             \
+    _Pragma("unroll") for (int j = 0; j < C::LG; ++j) dma_blk(j, g_rsrc, gb_, sb_ + j * 1024);      \
+    _Pragma("unroll") for (int j = 0; j < C::LF; ++j) dma_blk(j, f_rsrc, fb_, sb_ + (C::LG + j) * 1024); \
+  } while (0)
+
+  bool mok[WMB], nok[WNB];
+#pragma unroll
+  for (int mb = 0; mb < WMB; ++mb) mok[mb] = m0 + 16 * mb + r16 < cout;
+#pragma unroll
+  for (int nb = 0; nb < WNB; ++nb) nok[nb] = n0 + 16 * nb + r16 < cin;
+
+  f4 acc[WMB][WNB];
+#pragma unroll
+  for (int mb = 0; mb < WMB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < WNB; ++nb) acc[mb][nb] = f4{0.f, 0.f, 0.f, 0.f};
+
+  if (nblk > 0) KF_PAIRS(0);
+  if (nblk > 1) KF_PAIRS(1);
+  wait_vm<0>();
+  for (int t = 0; t < kFD - 1 && t < nstep; ++t) KF_ISSUE(t);
+  for (int t = 0; t < nstep; ++t) {
+    // this wavefront's DMAs of step t have landed (later steps may stay in flight)
+    if (t + kFD - 2 < nstep)
+      wait_vm<C::L * (kFD - 2)>();
+    else
+      wait_vm<0>();
+    const char* sb = wl + 2048 + (t % kFD) * C::STEP;
+    float a[WMB], b[WNB];
+#pragma unroll
+    for (int mb = 0; mb < WMB; ++mb) {
+      const float v = *reinterpret_cast<const float*>(sb + (mb >> 2) * 1024 + (mb & 3) * 256 + rd_lane);
+      a[mb] = mok[mb] ? v : 0.f;
+    }
+#pragma unroll
+    for (int nb = 0; nb < WNB; ++nb) {
+      const float v = *reinterpret_cast<const float*>(sb + (C::LG + (nb >> 2)) * 1024 + (nb & 3) * 256 + rd_lane);
+      b[nb] = nok[nb] ? v : 0.f;
+    }
+    // the stage refilled now held step t-1, whose operands were consumed by its MFMAs
+    if (t + kFD - 1 < nstep) KF_ISSUE(t + kFD - 1);
+#pragma unroll
+    for (int mb = 0; mb < WMB; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < WNB; ++nb)
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a[mb], b[nb], acc[mb][nb], 0, 0, 0);
+  }
+#undef KF_ISSUE
+#undef KF_PAIRS
+
+  float* dst = part + ((int64_t)split * K + s) * cout * cin;
+#pragma unroll
+  for (int mb = 0; mb < WMB; ++mb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + 16 * mb + 4 * g + i;
+      if (m >= cout) continue;
+#pragma unroll
+      for (int nb = 0; nb < WNB; ++nb)
+        if (nok[nb]) dst[(int64_t)m * cin + n0 + 16 * nb + r16] = acc[mb][nb][i];
+    }
+}
+
+template <int WMB, int WNB>
+void launch_f32_lds(dim3 grid, const float* G, int64_t g_rows, int cout, const float* F, int64_t f_rows, int cin,
+                    const int2* pairs, const int64_t* pair_off, int K, int mt, int nt, int nsplit, float* part,
+                    hipStream_t st) {
+  auto kern = kgrad_f32_lds_kernel<WMB, WNB>;
+  (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, KF<WMB, WNB>::SMEM);
+  kern<<<grid, 256, KF<WMB, WNB>::SMEM, st>>>(G, g_rows, cout, F, f_rows, cin, pairs, pair_off, K, mt, nt, nsplit, part);
+}
+
+template <int WMB>
+void launch_f32_lds_n(int wnb, dim3 grid, const float* G, int64_t g_rows, int cout, const float* F, int64_t f_rows,
+                      int cin, const int2* pairs, const int64_t* pair_off, int K, int mt, int nt, int nsplit,
+                      float* part, hipStream_t st) {
+  switch (wnb) {
+    case 1: launch_f32_lds<WMB, 1>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, K, mt, nt, nsplit, part, st); break;
+    case 2: launch_f32_lds<WMB, 2>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, K, mt, nt, nsplit, part, st); break;
+    case 4: launch_f32_lds<WMB, 4>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, K, mt, nt, nsplit, part, st); break;
+    case 7: launch_f32_lds<WMB, 7>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, K, mt, nt, nsplit, part, st); break;
+    default: launch_f32_lds<WMB, 8>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, K, mt, nt, nsplit, part, st); break;
+  }
+}
+
 template <int WMB>
 void launch_f32_n(int wnb, dim3 grid, const float* G, int cout, const float* F, int cin, const int2* pairs,
                   const int64_t* pair_off, int K, int mt, int nt, int nsplit, float* part, hipStream_t st) {
@@ -335,6 +516,19 @@ int kgrad_partials(const void* grad_out, const void* feats, ssconv_dtype dt, int
   dim3 grid(cdiv(ntask, 4));
   const float* G = (const float*)grad_out;
   const float* F = (const float*)feats;
+  // LDS-ring kernel when every row offset fits 31 bits (buffer DMA ranges)
+  const int64_t g_rows = rb->n_out, f_rows = rb->n_in;
+  if (g_rows * cout * 4 < ((int64_t)1 << 31) && f_rows * cin * 4 < ((int64_t)1 << 31) && debug_gather_variant() != 7) {
+    switch (p.wmb) {
+      case 1: launch_f32_lds_n<1>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
+      case 2: launch_f32_lds_n<2>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
+      case 4: launch_f32_lds_n<4>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
+      case 7: launch_f32_lds_n<7>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
+      default: launch_f32_lds_n<8>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
+    }
+    SSC_HIP(hipGetLastError());
+    return SSCONV_OK;
+  }
   switch (p.wmb) {
     case 1: launch_f32_n<1>(p.wnb, grid, G, cout, F, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
     case 2: launch_f32_n<2>(p.wnb, grid, G, cout, F, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
