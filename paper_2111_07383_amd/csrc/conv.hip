@@ -385,8 +385,16 @@ static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 constexpr int kKgradUnits = 512;
 
 static bool use_kgrad_units(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout) {
-  return dt == SSCONV_BF16 && debug_gather_variant() != 6 && kgrad_supported(dt, cin, cout) && rb->K <= kKgradMaxK &&
+  if (dt == SSCONV_F32) return kgrad_f32_units_ok(rb, cin, cout);
+  return debug_gather_variant() != 6 && kgrad_supported(dt, cin, cout) && rb->K <= kKgradMaxK &&
          (int64_t)rb->n_in * cin * 2 < ((int64_t)1 << 31) && (int64_t)rb->n_out * cout * 2 < ((int64_t)1 << 31);
+}
+
+// Work units of the kernel gradient: bf16 ~512 (one workgroup each, launched in row order), fp32
+// enough wavefront tasks for two rounds of the wavefront slots.
+static KgradUnits plan_units(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout) {
+  if (dt == SSCONV_F32) return kgrad_units(rb, kgrad_f32_units_want(rb, cin, cout), false);
+  return kgrad_units(rb, kKgradUnits, true);
 }
 
 BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout) {
@@ -394,7 +402,7 @@ BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int co
   const size_t K = rb->K, sz = dtype_bytes(dt);
   size_t nparts;  // fp32 partial tiles of cout x cin
   if (use_kgrad_units(rb, dt, cin, cout)) {
-    nparts = (size_t)kgrad_units(rb, kKgradUnits).nunits;
+    nparts = (size_t)plan_units(rb, dt, cin, cout).nunits;
   } else {
     L.nsplit = kgrad_supported(dt, cin, cout) ? kgrad_plan(rb, dt, cin, cout).nsplit : dw_nsplit(rb);
     nparts = (size_t)L.nsplit * K;
@@ -451,8 +459,11 @@ int conv_backward_dw(const void* feats, const void* grad_out, ssconv_dtype dt, i
   const int K = rb->K;
   const int64_t n = (int64_t)K * cin * cout;
   if (use_kgrad_units(rb, dt, cin, cout)) {
-    const KgradUnits units = kgrad_units(rb, kKgradUnits);
-    SSC_TRY(kgrad_bf16(grad_out, rb->n_out, feats, rb->n_in, cin, cout, rb, units, part, st));
+    const KgradUnits units = plan_units(rb, dt, cin, cout);
+    if (dt == SSCONV_F32)
+      SSC_TRY(kgrad_f32(grad_out, feats, cin, cout, rb, units, part, st));
+    else
+      SSC_TRY(kgrad_bf16(grad_out, rb->n_out, feats, rb->n_in, cin, cout, rb, units, part, st));
     return reduce_units(part, units, (int64_t)cin * cout, dW, st);
   }
   if (kgrad_supported(dt, cin, cout))

@@ -294,13 +294,14 @@ __global__ void reduce_units_kernel(const float* __restrict__ part, KgradUnits u
 
 }  // namespace
 
-KgradUnits kgrad_units(const ssconv_rulebook* rb, int want) {
+KgradUnits kgrad_units(const ssconv_rulebook* rb, int want, bool ordered) {
   KgradUnits u;
   u.K = rb->K;
   const int K = rb->K;
+  const int cap = ordered ? kKgradMaxUnits : kKgradMaxUnitsF32;
   int64_t total = 0;
   for (int s = 0; s < K; ++s) total += rb->pair_off[s + 1] - rb->pair_off[s];
-  want = std::min(std::max(want, K), kKgradMaxUnits);
+  want = std::min(std::max(want, K), cap);
   int n[kKgradMaxK];
   double rem[kKgradMaxK];
   int sum = 0;
@@ -310,16 +311,13 @@ KgradUnits kgrad_units(const ssconv_rulebook* rb, int want) {
     rem[s] = quota - n[s];
     sum += n[s];
   }
-  while (sum < want) {  // largest remainders first
-    int best = 0;
-    for (int s = 1; s < K; ++s)
-      if (rem[s] > rem[best]) best = s;
-    if (rem[best] <= 0.0) break;
-    ++n[best];
-    rem[best] -= 1.0;
-    ++sum;
-  }
-  while (sum > kKgradMaxUnits) {  // the one-unit minimum can overshoot: trim the largest offsets
+  // largest remainders first (the floors leave fewer than K units to hand out, one per offset at
+  // most); ties by offset, so the split is deterministic
+  int by_rem[kKgradMaxK];
+  for (int s = 0; s < K; ++s) by_rem[s] = s;
+  std::stable_sort(by_rem, by_rem + K, [&](int a, int b) { return rem[a] > rem[b]; });
+  for (int i = 0; i < K && sum < want && rem[by_rem[i]] > 0.0; ++i) ++n[by_rem[i]], ++sum;
+  while (sum > cap) {  // the one-unit minimum can overshoot: trim the largest offsets
     int big = 0;
     for (int s = 1; s < K; ++s)
       if (n[s] > n[big]) big = s;
@@ -329,6 +327,7 @@ KgradUnits kgrad_units(const ssconv_rulebook* rb, int want) {
   u.uoff[0] = 0;
   for (int s = 0; s < K; ++s) u.uoff[s + 1] = u.uoff[s] + n[s];
   u.nunits = u.uoff[K];
+  if (!ordered) return u;
   // launch order: by the centre of each unit's slice along R_s (pairs are sorted by output row),
   // ties by offset -- a stable order, so the launch is deterministic
   std::vector<std::pair<double, int>> key(u.nunits);

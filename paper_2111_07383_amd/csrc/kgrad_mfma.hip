@@ -316,23 +316,25 @@ template <int WMB, int WNB>
 __global__ __launch_bounds__(256) void kgrad_f32_lds_kernel(const float* __restrict__ G, int64_t g_rows, int cout,
                                                             const float* __restrict__ F, int64_t f_rows, int cin,
                                                             const int2* __restrict__ pairs,
-                                                            const int64_t* __restrict__ pair_off, int K, int mtiles,
-                                                            int ntiles, int nsplit, float* __restrict__ part) {
+                                                            const int64_t* __restrict__ pair_off, KgradUnits units,
+                                                            int mtiles, int ntiles, float* __restrict__ part) {
   using C = KF<WMB, WNB>;
   static_assert(C::LG <= 2 && C::LF <= 2, "at most two DMA blocks per operand");
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int lane = threadIdx.x & 63, g = lane >> 4, r16 = lane & 15;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int64_t task = (int64_t)blockIdx.x * 4 + w;
-  const int64_t ntask = (int64_t)K * nsplit * mtiles * ntiles;
-  if (task >= ntask) return;  // whole wavefront; the kernel has no barriers
-  const int nt = (int)(task % ntiles);
-  const int mt = (int)((task / ntiles) % mtiles);
-  const int split = (int)((task / ((int64_t)ntiles * mtiles)) % nsplit);
-  const int s = (int)(task / ((int64_t)ntiles * mtiles * nsplit));
+  // task = (work unit u: a slice of one offset's pairs, output tile)
+  const int task = blockIdx.x * 4 + w;
+  if (task >= units.nunits * mtiles * ntiles) return;  // whole wavefront; the kernel has no barriers
+  const int nt = task % ntiles;
+  const int mt = (task / ntiles) % mtiles;
+  const int u = task / (ntiles * mtiles);
+  int s = 0;
+  while (s + 1 < units.K && units.uoff[s + 1] <= u) ++s;
+  const int j = u - units.uoff[s], ns = units.uoff[s + 1] - units.uoff[s];
   const int m0 = mt * 16 * WMB, n0 = nt * 16 * WNB;
   const int64_t off = pair_off[s], cnt = pair_off[s + 1] - off;
-  const int64_t beg = off + cnt * split / nsplit, end = off + cnt * (split + 1) / nsplit;
+  const int64_t beg = off + cnt * j / ns, end = off + cnt * (j + 1) / ns;
   const int npairs = (int)(end - beg);
   const int nstep = (npairs + 3) / 4;
 
@@ -415,7 +417,7 @@ __global__ __launch_bounds__(256) void kgrad_f32_lds_kernel(const float* __restr
 #undef KF_ISSUE
 #undef KF_PAIRS
 
-  float* dst = part + ((int64_t)split * K + s) * cout * cin;
+  float* dst = part + (int64_t)u * cout * cin;
 #pragma unroll
   for (int mb = 0; mb < WMB; ++mb)
 #pragma unroll
@@ -430,23 +432,23 @@ __global__ __launch_bounds__(256) void kgrad_f32_lds_kernel(const float* __restr
 
 template <int WMB, int WNB>
 void launch_f32_lds(dim3 grid, const float* G, int64_t g_rows, int cout, const float* F, int64_t f_rows, int cin,
-                    const int2* pairs, const int64_t* pair_off, int K, int mt, int nt, int nsplit, float* part,
+                    const int2* pairs, const int64_t* pair_off, const KgradUnits& units, int mt, int nt, float* part,
                     hipStream_t st) {
   auto kern = kgrad_f32_lds_kernel<WMB, WNB>;
   (void)hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, KF<WMB, WNB>::SMEM);
-  kern<<<grid, 256, KF<WMB, WNB>::SMEM, st>>>(G, g_rows, cout, F, f_rows, cin, pairs, pair_off, K, mt, nt, nsplit, part);
+  kern<<<grid, 256, KF<WMB, WNB>::SMEM, st>>>(G, g_rows, cout, F, f_rows, cin, pairs, pair_off, units, mt, nt, part);
 }
 
 template <int WMB>
 void launch_f32_lds_n(int wnb, dim3 grid, const float* G, int64_t g_rows, int cout, const float* F, int64_t f_rows,
-                      int cin, const int2* pairs, const int64_t* pair_off, int K, int mt, int nt, int nsplit,
+                      int cin, const int2* pairs, const int64_t* pair_off, const KgradUnits& units, int mt, int nt,
                       float* part, hipStream_t st) {
   switch (wnb) {
-    case 1: launch_f32_lds<WMB, 1>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, K, mt, nt, nsplit, part, st); break;
-    case 2: launch_f32_lds<WMB, 2>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, K, mt, nt, nsplit, part, st); break;
-    case 4: launch_f32_lds<WMB, 4>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, K, mt, nt, nsplit, part, st); break;
-    case 7: launch_f32_lds<WMB, 7>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, K, mt, nt, nsplit, part, st); break;
-    default: launch_f32_lds<WMB, 8>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, K, mt, nt, nsplit, part, st); break;
+    case 1: launch_f32_lds<WMB, 1>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, units, mt, nt, part, st); break;
+    case 2: launch_f32_lds<WMB, 2>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, units, mt, nt, part, st); break;
+    case 4: launch_f32_lds<WMB, 4>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, units, mt, nt, part, st); break;
+    case 7: launch_f32_lds<WMB, 7>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, units, mt, nt, part, st); break;
+    default: launch_f32_lds<WMB, 8>(grid, G, g_rows, cout, F, f_rows, cin, pairs, pair_off, units, mt, nt, part, st); break;
   }
 }
 
@@ -516,25 +518,44 @@ int kgrad_partials(const void* grad_out, const void* feats, ssconv_dtype dt, int
   dim3 grid(cdiv(ntask, 4));
   const float* G = (const float*)grad_out;
   const float* F = (const float*)feats;
-  // LDS-ring kernel when every row offset fits 31 bits (buffer DMA ranges)
-  const int64_t g_rows = rb->n_out, f_rows = rb->n_in;
-  if (g_rows * cout * 4 < ((int64_t)1 << 31) && f_rows * cin * 4 < ((int64_t)1 << 31) && debug_gather_variant() != 7) {
-    switch (p.wmb) {
-      case 1: launch_f32_lds_n<1>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
-      case 2: launch_f32_lds_n<2>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
-      case 4: launch_f32_lds_n<4>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
-      case 7: launch_f32_lds_n<7>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
-      default: launch_f32_lds_n<8>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
-    }
-    SSC_HIP(hipGetLastError());
-    return SSCONV_OK;
-  }
   switch (p.wmb) {
     case 1: launch_f32_n<1>(p.wnb, grid, G, cout, F, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
     case 2: launch_f32_n<2>(p.wnb, grid, G, cout, F, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
     case 4: launch_f32_n<4>(p.wnb, grid, G, cout, F, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
     case 7: launch_f32_n<7>(p.wnb, grid, G, cout, F, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
     default: launch_f32_n<8>(p.wnb, grid, G, cout, F, cin, pairs, rb->pair_off_dev, rb->K, p.mtiles, p.ntiles, p.nsplit, part, st); break;
+  }
+  SSC_HIP(hipGetLastError());
+  return SSCONV_OK;
+}
+
+bool kgrad_f32_units_ok(const ssconv_rulebook* rb, int cin, int cout) {
+  return rb->K <= kKgradMaxK && (int64_t)rb->n_out * cout * 4 < ((int64_t)1 << 31) &&
+         (int64_t)rb->n_in * cin * 4 < ((int64_t)1 << 31) && debug_gather_variant() != 7;
+}
+
+int kgrad_f32_units_want(const ssconv_rulebook* rb, int cin, int cout) {
+  const KgradPlan p = kgrad_plan(rb, SSCONV_F32, cin, cout);
+  // two full rounds of the 2048 wavefront slots (256 CUs x two four-wavefront workgroups)
+  return std::max(1, kKgradMaxUnitsF32 / (p.mtiles * p.ntiles));
+}
+
+int kgrad_f32(const void* grad_out, const void* feats, int cin, int cout, const ssconv_rulebook* rb,
+              const KgradUnits& units, float* part, hipStream_t st) {
+  if (units.nunits == 0) return SSCONV_OK;
+  const KgradPlan p = kgrad_plan(rb, SSCONV_F32, cin, cout);
+  const int64_t ntask = (int64_t)units.nunits * p.mtiles * p.ntiles;
+  dim3 grid(cdiv(ntask, 4));
+  const int2* pairs = reinterpret_cast<const int2*>(rb->pairs);
+  const float* G = (const float*)grad_out;
+  const float* F = (const float*)feats;
+  const int64_t g_rows = rb->n_out, f_rows = rb->n_in;
+  switch (p.wmb) {
+    case 1: launch_f32_lds_n<1>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, units, p.mtiles, p.ntiles, part, st); break;
+    case 2: launch_f32_lds_n<2>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, units, p.mtiles, p.ntiles, part, st); break;
+    case 4: launch_f32_lds_n<4>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, units, p.mtiles, p.ntiles, part, st); break;
+    case 7: launch_f32_lds_n<7>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, units, p.mtiles, p.ntiles, part, st); break;
+    default: launch_f32_lds_n<8>(p.wnb, grid, G, g_rows, cout, F, f_rows, cin, pairs, rb->pair_off_dev, units, p.mtiles, p.ntiles, part, st); break;
   }
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;

@@ -24,7 +24,8 @@ KgradPlan kgrad_plan(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int co
 // and handed out XCD-contiguously, so the units of all offsets over one stretch of rows run on
 // one XCD together and share its L2 for the gathered rows.
 constexpr int kKgradMaxK = 125;  // ksize <= 5
-constexpr int kKgradMaxUnits = 512;
+constexpr int kKgradMaxUnits = 512;      // bf16 (launch order recorded)
+constexpr int kKgradMaxUnitsF32 = 4096;  // fp32 (one wavefront per unit and tile)
 struct KgradUnits {
   int K = 0, nunits = 0;
   int uoff[kKgradMaxK + 1] = {};
@@ -32,9 +33,16 @@ struct KgradUnits {
 };
 
 // Units for the rule book: about `want` in total (at least one per offset, at most
-// kKgradMaxUnits), distributed over the offsets in proportion to their pair counts (largest
-// remainders), with their launch order.
-KgradUnits kgrad_units(const ssconv_rulebook* rb, int want);
+// kKgradMaxUnits when `ordered`, else kKgradMaxUnitsF32), distributed over the offsets in
+// proportion to their pair counts (largest remainders); `ordered` also records the launch order.
+KgradUnits kgrad_units(const ssconv_rulebook* rb, int want, bool ordered);
+
+// fp32 kernel gradient over work units (per-wavefront LDS ring): usable when every row offset
+// fits 31 bits; the unit count that fills two rounds of wavefront slots.
+bool kgrad_f32_units_ok(const ssconv_rulebook* rb, int cin, int cout);
+int kgrad_f32_units_want(const ssconv_rulebook* rb, int cin, int cout);
+int kgrad_f32(const void* grad_out, const void* feats, int cin, int cout, const ssconv_rulebook* rb,
+              const KgradUnits& units, float* part, hipStream_t st);
 
 // bf16 tile width (in 32-channel steps of the 2x2 wavefront grid) for cin x cout.
 int kgrad_bf16_tile(int cin, int cout);
