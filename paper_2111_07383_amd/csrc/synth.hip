@@ -3,7 +3,7 @@
 // W[s][o][i] = sum_q w[off(field(o), field(i)) + q] * B^{k l}_q[s][a][b], one thread per
 // element of W so the dominant cost -- writing W -- is a coalesced stream.
 // The adjoint dw[off + q] = sum_{s,a,b} dW[s][o][i] B_q[s][a][b] uses one
-// workgroup per (out field, in field) pair with a fixed reduction tree.
+// workgroup per (out field, in field) pair with a fixed reduction order.
 #include "synth.hpp"
 
 namespace ssconv {
@@ -79,11 +79,15 @@ __global__ __launch_bounds__(256) void synth_kernel(SynthArgs a, const float* __
   W[idx] = DT<T>::from_f(acc);
 }
 
-constexpr int kMaxNq = 2 * SSCONV_MAX_SHELLS * (2 * SSCONV_MAX_L + 1);
+// One workgroup per (in field, out field) pair; its coefficients are done 8 at a time in
+// registers: thread partial sums over the block's elements in a fixed order, a fixed butterfly
+// within each wavefront, then the four wavefront sums added in order (independent of scheduling).
+constexpr int kQB = 8;
 
 __global__ __launch_bounds__(256) void synth_adjoint_kernel(SynthArgs a, const float* __restrict__ basis,
                                                             const float* __restrict__ dW, float* __restrict__ dcoef) {
-  // block = (in field j, out field i)
+  __shared__ float red[4][kQB];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int fi_all = blockIdx.x, fo_all = blockIdx.y;
   int eo = 0, ei = 0;
   while (eo + 1 < a.out.n && fo_all >= a.out.f0[eo + 1]) ++eo;
@@ -91,28 +95,35 @@ __global__ __launch_bounds__(256) void synth_adjoint_kernel(SynthArgs a, const f
   const int fo = fo_all - a.out.f0[eo], fi = fi_all - a.in.f0[ei];
   const int k = a.out.l[eo], l = a.in.l[ei], dk = 2 * k + 1, dl = 2 * l + 1;
   const int nq = a.nq[k][l];
-  if (nq == 0) return;
+  if (nq == 0) return;  // uniform per workgroup
   const int ro = a.out.ch0[eo] + fo * dk, cc = a.in.ch0[ei] + fi * dl;
   const int64_t off = coeff_off(a, eo, fo, k, ei, fi);
   const int n = a.K * dk * dl;
   const int64_t qstride = (int64_t)a.K * dk * dl;
   const float* bp = basis + a.base[k][l];
-  float acc[kMaxNq];
-  for (int q = 0; q < nq; ++q) acc[q] = 0.f;
-  for (int e = threadIdx.x; e < n; e += 256) {
-    const int s = e / (dk * dl), r = e % (dk * dl), aa = r / dl, bb = r % dl;
-    const float g = dW[((int64_t)s * a.cout + ro + aa) * a.cin + cc + bb];
-    for (int q = 0; q < nq; ++q) acc[q] = fmaf(g, bp[q * qstride + e], acc[q]);
-  }
-  __shared__ float red[256];
-  for (int q = 0; q < nq; ++q) {
-    red[threadIdx.x] = acc[q];
-    __syncthreads();
-    for (int w = 128; w > 0; w >>= 1) {
-      if ((int)threadIdx.x < w) red[threadIdx.x] += red[threadIdx.x + w];
-      __syncthreads();
+  for (int q0 = 0; q0 < nq; q0 += kQB) {
+    float acc[kQB];
+#pragma unroll
+    for (int j = 0; j < kQB; ++j) acc[j] = 0.f;
+    for (int e = threadIdx.x; e < n; e += 256) {
+      const int s = e / (dk * dl), r = e % (dk * dl), aa = r / dl, bb = r % dl;
+      const float g = dW[((int64_t)s * a.cout + ro + aa) * a.cin + cc + bb];
+#pragma unroll
+      for (int j = 0; j < kQB; ++j)
+        if (q0 + j < nq) acc[j] = fmaf(g, bp[(q0 + j) * qstride + e], acc[j]);
     }
-    if (threadIdx.x == 0) dcoef[off + q] = red[0];
+#pragma unroll
+    for (int j = 0; j < kQB; ++j) {
+      float v = acc[j];
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+      if (lane == 0) red[w][j] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < kQB && q0 + (int)threadIdx.x < nq) {
+      const int j = threadIdx.x;
+      dcoef[off + q0 + j] = ((red[0][j] + red[1][j]) + red[2][j]) + red[3][j];
+    }
     __syncthreads();
   }
 }
