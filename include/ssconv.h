@@ -6,11 +6,11 @@
  * active voxel sites and a feature matrix whose rows follow it -- with a
  * rotation-steerable kernel kappa to give (H_{n+1}, F_{n+1}) (Sec. 3.2).
  * The library implements the three steps of Sec. 3.2:
- *   1. rule book construction (Sec. 3.2.2 site state, Sec. 3.2.3 Alg. 1
- *      lines 1-7) over a GPU coordinate hash table;
+ *   1. rule book construction (Sec. 3.2.2 site state, the rule-book part of
+ *      Alg. 1 in Sec. 3.2.3) over a GPU coordinate hash table;
  *   2. kernel synthesis as a linear combination of steerable basis kernels
  *      (Sec. 3.2.1, Eq. 7-9);
- *   3. the feature update of Alg. 1 (lines 8-12) as an output-stationary
+ *   3. the feature update of Alg. 1 as an output-stationary
  *      gather -> matrix-core GEMM -> single write per output row;
  * plus the exact adjoint (feature and coefficient gradients) and the gated
  * nonlinearity of Sec. 3.3 (Eq. 12).
@@ -115,7 +115,7 @@ int ssconv_basis_info(const ssconv_basis_desc* desc /*host*/, int64_t* basis_flo
                       int64_t* n_coeff /*host*/);
 int ssconv_basis_build(const ssconv_basis_desc* desc /*host*/, float* basis /*host*/);
 
-/* ---- rule book (Sec. 3.2.2, Eq. 10; Sec. 3.2.3, Alg. 1 lines 1-7) --------
+/* ---- rule book (Sec. 3.2.2, Eq. 10; Sec. 3.2.3, rule book of Alg. 1) -----
  * coords: [n, 4] int32 (b, x, y, z), n >= 0, no duplicates.
  * grid (host): input grid extent per axis.  ksize: odd, 1..5.
  * stride: 1 or 2.  submanifold = 1 keeps H_{n+1} = H_n (stride must be 1, rows
@@ -156,7 +156,7 @@ void ssconv_rulebook_destroy(ssconv_rulebook_t rb);
 int ssconv_synth_kernel(const ssconv_basis_desc* desc /*host*/, const float* basis,
                         const float* coeffs, ssconv_dtype w_dtype, void* W, hipStream_t stream);
 
-/* ---- forward (Sec. 3.2.3, Alg. 1 lines 8-12) -------------------------------
+/* ---- forward (Sec. 3.2.3, feature update of Alg. 1) -----------------------
  * out[x] = sum_s sum_{(x,y) in R_s} kappa(s) feats[y], every output row written
  * exactly once (rows with no pair become 0).  feats [n_in, cin], W
  * [ksize^3, cout, cin], out [n_out, cout], all in `dtype` (bf16 inputs are

@@ -1,4 +1,4 @@
-// Sparse steerable convolution on matrix cores (Sec. 3.2.3, Alg. 1 lines 8-12) and its adjoint.
+// Sparse steerable convolution on matrix cores (Sec. 3.2.3, the feature update of Alg. 1) and its adjoint.
 //
 // gather_gemm: output-stationary implicit GEMM.  A workgroup owns BM = 64 output
 // rows x BN = 16*WNB output channels and accumulates, in MFMA accumulators,

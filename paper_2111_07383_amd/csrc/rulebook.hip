@@ -1,4 +1,4 @@
-// Rule book construction on the GPU (Sec. 3.2.2, Eq. 10; Sec. 3.2.3, Alg. 1 lines 1-7).
+// Rule book construction on the GPU (Sec. 3.2.2, Eq. 10; Sec. 3.2.3, the rule-book part of Alg. 1).
 //
 // Instead of Alg. 1's all-pairs loop, every input site is inserted into an
 // open-addressing hash table in HBM (64-bit slots key<<32 | row, lock-free
