@@ -99,7 +99,8 @@ struct ssconv_rulebook {
   int32_t* out_coords = nullptr;  // [n_out, 4]
   int32_t* nbr = nullptr;         // [K, n_out]
   int32_t* pairs = nullptr;       // [n_pairs, 2] grouped by offset
-  int64_t* pair_off_dev = nullptr;  // [K + 1]
+  int64_t* pair_off_dev = nullptr;  // [K + 1], followed by the build flags
+  void* mem[3] = {nullptr, nullptr, nullptr};  // the allocations every buffer above lives in
   // host copies
   int64_t* pair_off = nullptr;  // [K + 1] (host)
 };

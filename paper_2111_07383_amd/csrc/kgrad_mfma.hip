@@ -82,7 +82,6 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
   const int64_t npairs = end - beg;
   const int nchunk = (int)((npairs + 31) / 32);
   const uint32_t stage0 = (uint32_t)(uintptr_t)stages, junk_a = (uint32_t)(uintptr_t)junk;
-  const uint32_t pblk_a = (uint32_t)(uintptr_t)pblk;
 
   // pair indices: block b covers slice pairs [b*PBLK, (b+1)*PBLK); registers hold the next block
   constexpr int PPT = C::PBLK / 256;

@@ -66,8 +66,14 @@ __global__ void validate_kernel(const int32_t* __restrict__ c, int64_t n, int g0
   }
 }
 
-__global__ void fill_u64(uint64_t* __restrict__ p, int64_t n, uint64_t v) {
-  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// Empty hash slots; the first thread also clears the build flags when asked (flags[0] = 0,
+// flags[1] = max batch index seen = -1).
+__global__ void fill_slots(uint64_t* __restrict__ p, int64_t n, uint64_t v, int* __restrict__ flags) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (flags && i == 0) {
+    flags[0] = 0;
+    flags[1] = -1;
+  }
   if (i < n) p[i] = v;
 }
 
@@ -221,16 +227,20 @@ thread_local Staging g_stage;
 
 void rulebook_free(ssconv_rulebook* rb) {
   if (!rb) return;
-  hipStream_t s = rb->stream;
-  if (rb->hash_out && rb->hash_out != rb->hash_in) dev_free(rb->hash_out, s);
-  dev_free(rb->hash_in, s);
-  dev_free(rb->out_coords, s);
-  dev_free(rb->nbr, s);
-  dev_free(rb->pairs, s);
-  dev_free(rb->pair_off_dev, s);
+  for (void* m : rb->mem) dev_free(m, rb->stream);  // every device buffer lives in these blocks
   delete[] rb->pair_off;
   delete rb;
 }
+
+// Carves 256-byte aligned pieces out of one allocation.
+struct Carve {
+  size_t at = 0;
+  size_t take(size_t bytes) {
+    const size_t o = at;
+    at += (bytes + 255) & ~(size_t)255;
+    return o;
+  }
+};
 
 // Temporary device buffers released on every exit path.
 struct Scratch {
@@ -255,17 +265,22 @@ static int max_batch(const int* g) {
   return (int)std::min<int64_t>(m, 0x7fffffff);
 }
 
-static int build_hash(const int32_t* coords, int64_t n, const int* g, hipStream_t st, uint64_t** slots,
-                      int64_t* cap, int* flags) {
+static int hash_capacity(int64_t n, int64_t* cap) {
   int64_t c = debug_hash_capacity();
   if (c <= 0) c = next_pow2(2 * n);
   if (c & (c - 1)) return fail(SSCONV_E_INVALID, "forced hash capacity must be a power of two");
   *cap = c;
-  SSC_TRY(dev_alloc((void**)slots, (size_t)c * 8, st));
-  fill_u64<<<cdiv(c, 256), 256, 0, st>>>(*slots, c, kEmpty);
+  return SSCONV_OK;
+}
+
+// Fills the table (capacity cap, already allocated) and inserts the n sites; init_flags also
+// clears the build flags in the fill kernel.
+static int build_hash(const int32_t* coords, int64_t n, const int* g, hipStream_t st, uint64_t* slots, int64_t cap,
+                      int* flags, bool init_flags) {
+  fill_slots<<<cdiv(cap, 256), 256, 0, st>>>(slots, cap, kEmpty, init_flags ? flags : nullptr);
   if (n > 0)
-    hash_insert_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, g[0], g[1], g[2], max_batch(g), *slots,
-                                                     (uint64_t)(c - 1), flags);
+    hash_insert_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, g[0], g[1], g[2], max_batch(g), slots,
+                                                     (uint64_t)(cap - 1), flags);
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;
 }
@@ -286,14 +301,39 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
   rb->pair_off = new int64_t[K + 1]();
   int64_t* host = nullptr;
   SSC_TRY(g_stage.get(&host));
-
-  Scratch tmp(st);
+  // Device memory comes in few allocations (each costs host time on every build): the handle's
+  // buffers in at most three blocks, the temporaries in one or two.  pair_off_dev is followed by
+  // the build flags, so both come back in one copy.
+  SSC_TRY(hash_capacity(n, &rb->cap_in));
+  const size_t pairs_bound = (size_t)K * (size_t)n * 8;  // submanifold: every output has <= K pairs
+  const bool pairs_in_block = submanifold && pairs_bound <= ((size_t)1 << 30);
   int* dflags = nullptr;  // [0] flags, [1] max b
-  SSC_TRY(tmp.alloc((void**)&dflags, 64));
-  SSC_HIP(hipMemsetAsync(dflags, 0, 4, st));
-  SSC_HIP(hipMemsetAsync(dflags + 1, 0xff, 4, st));  // max b = -1
+  {
+    Carve c;
+    const size_t o_hash = c.take((size_t)rb->cap_in * 8), o_off = c.take((size_t)(K + 2) * 8);
+    size_t o_oc = 0, o_nbr = 0, o_pairs = 0;
+    if (submanifold) {
+      o_oc = c.take((size_t)n * 16);
+      o_nbr = c.take((size_t)K * n * 4);
+      if (pairs_in_block) o_pairs = c.take(pairs_bound);
+    }
+    char* b0 = nullptr;
+    SSC_TRY(dev_alloc((void**)&b0, c.at, st));
+    rb->mem[0] = b0;
+    rb->hash_in = (uint64_t*)(b0 + o_hash);
+    rb->pair_off_dev = (int64_t*)(b0 + o_off);
+    dflags = (int*)(rb->pair_off_dev + K + 1);
+    if (submanifold) {
+      rb->out_coords = (int32_t*)(b0 + o_oc);
+      rb->nbr = (int32_t*)(b0 + o_nbr);
+      if (pairs_in_block) rb->pairs = (int32_t*)(b0 + o_pairs);
+    }
+  }
+
   if (!submanifold) {
     // the output bitmap spans the batch: its extent is needed on the host before the next launch
+    SSC_HIP(hipMemsetAsync(dflags, 0, 4, st));
+    SSC_HIP(hipMemsetAsync(dflags + 1, 0xff, 4, st));  // max b = -1
     if (n > 0) validate_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, grid[0], grid[1], grid[2], dflags, dflags + 1);
     SSC_HIP(hipGetLastError());
     SSC_HIP(hipMemcpyAsync(host, dflags, 8, hipMemcpyDeviceToHost, st));
@@ -304,12 +344,12 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     rb->nbatch = maxb + 1;
   }
 
-  SSC_TRY(build_hash(coords, n, rb->grid, st, &rb->hash_in, &rb->cap_in, dflags));
+  SSC_TRY(build_hash(coords, n, rb->grid, st, rb->hash_in, rb->cap_in, dflags, submanifold != 0));
 
   // ---- output site set ----
+  Scratch tmp(st);
   if (submanifold) {
     rb->n_out = n;
-    SSC_TRY(dev_alloc((void**)&rb->out_coords, (size_t)n * 16, st));
     if (n) SSC_HIP(hipMemcpyAsync(rb->out_coords, coords, (size_t)n * 16, hipMemcpyDeviceToDevice, st));
     rb->hash_out = rb->hash_in;
     rb->cap_out = rb->cap_in;
@@ -317,14 +357,16 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     const int* go = rb->grid_out;
     const int64_t nbits = rb->nbatch * (int64_t)go[0] * go[1] * go[2];
     const int64_t nw = (nbits + 31) / 32;
-    uint32_t* bits = nullptr;
-    int32_t* wcnt = nullptr;
-    int64_t *woff = nullptr, *stmp = nullptr, *dtotal = nullptr;
-    SSC_TRY(tmp.alloc((void**)&bits, (size_t)nw * 4));
-    SSC_TRY(tmp.alloc((void**)&wcnt, (size_t)nw * 4));
-    SSC_TRY(tmp.alloc((void**)&woff, (size_t)nw * 8));
-    SSC_TRY(tmp.alloc((void**)&stmp, (size_t)scan_tmp_elems(nw) * 8 + 8));
-    dtotal = stmp + scan_tmp_elems(nw);
+    Carve c;
+    const size_t o_bits = c.take((size_t)nw * 4), o_wcnt = c.take((size_t)nw * 4), o_woff = c.take((size_t)nw * 8),
+                 o_stmp = c.take((size_t)scan_tmp_elems(nw) * 8 + 8);
+    char* t0 = nullptr;
+    SSC_TRY(tmp.alloc((void**)&t0, c.at));
+    uint32_t* bits = (uint32_t*)(t0 + o_bits);
+    int32_t* wcnt = (int32_t*)(t0 + o_wcnt);
+    int64_t* woff = (int64_t*)(t0 + o_woff);
+    int64_t* stmp = (int64_t*)(t0 + o_stmp);
+    int64_t* dtotal = stmp + scan_tmp_elems(nw);
     if (nw) SSC_HIP(hipMemsetAsync(bits, 0, (size_t)nw * 4, st));
     if (n > 0) {
       dim3 gm(cdiv(n, 256), K);
@@ -339,24 +381,38 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     SSC_HIP(hipMemcpyAsync(host, dtotal, 8, hipMemcpyDeviceToHost, st));
     SSC_HIP(hipStreamSynchronize(st));
     rb->n_out = host[0];
-    SSC_TRY(dev_alloc((void**)&rb->out_coords, (size_t)rb->n_out * 16, st));
+    // second block: output coordinates, output hash, neighbour map, pairs (upper bound <= 1 GB)
+    SSC_TRY(hash_capacity(rb->n_out, &rb->cap_out));
+    const size_t bound = (size_t)K * (size_t)rb->n_out * 8;
+    Carve c1;
+    const size_t o_oc = c1.take((size_t)rb->n_out * 16), o_hash = c1.take((size_t)rb->cap_out * 8),
+                 o_nbr = c1.take((size_t)K * rb->n_out * 4);
+    const size_t o_pairs = bound <= ((size_t)1 << 30) ? c1.take(bound) : 0;
+    char* b1 = nullptr;
+    SSC_TRY(dev_alloc((void**)&b1, c1.at, st));
+    rb->mem[1] = b1;
+    rb->out_coords = (int32_t*)(b1 + o_oc);
+    rb->hash_out = (uint64_t*)(b1 + o_hash);
+    rb->nbr = (int32_t*)(b1 + o_nbr);
+    if (bound <= ((size_t)1 << 30)) rb->pairs = (int32_t*)(b1 + o_pairs);
     if (nw) emit_outputs<<<cdiv(nw, 256), 256, 0, st>>>(bits, nw, woff, go[0], go[1], go[2], rb->out_coords);
     SSC_HIP(hipGetLastError());
-    SSC_TRY(build_hash(rb->out_coords, rb->n_out, go, st, &rb->hash_out, &rb->cap_out, dflags));
+    SSC_TRY(build_hash(rb->out_coords, rb->n_out, go, st, rb->hash_out, rb->cap_out, dflags, false));
   }
 
   // ---- neighbour map and per-offset pair lists ----
   const int64_t n_out = rb->n_out;
-  SSC_TRY(dev_alloc((void**)&rb->nbr, (size_t)K * n_out * 4, st));
-  SSC_TRY(dev_alloc((void**)&rb->pair_off_dev, (size_t)(K + 1) * 8, st));
   if (n_out > 0) {
     const int nblk = (int)cdiv(n_out, 256);
     const int64_t ncnt = (int64_t)K * nblk;
-    int32_t* counts = nullptr;
-    int64_t *offs = nullptr, *stmp = nullptr;
-    SSC_TRY(tmp.alloc((void**)&counts, (size_t)ncnt * 4));
-    SSC_TRY(tmp.alloc((void**)&offs, (size_t)ncnt * 8));
-    SSC_TRY(tmp.alloc((void**)&stmp, (size_t)scan_tmp_elems(ncnt) * 8 + 8));
+    Carve c;
+    const size_t o_cnt = c.take((size_t)ncnt * 4), o_offs = c.take((size_t)ncnt * 8),
+                 o_stmp = c.take((size_t)scan_tmp_elems(ncnt) * 8 + 8);
+    char* t1 = nullptr;
+    SSC_TRY(tmp.alloc((void**)&t1, c.at));
+    int32_t* counts = (int32_t*)(t1 + o_cnt);
+    int64_t* offs = (int64_t*)(t1 + o_offs);
+    int64_t* stmp = (int64_t*)(t1 + o_stmp);
     int64_t* dtotal = stmp + scan_tmp_elems(ncnt);
     dim3 gp(nblk, K);
     probe_kernel<true><<<gp, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0], grid[1], grid[2],
@@ -367,36 +423,31 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     // the pair lists are written at their upper bound (every output has at most K neighbours), so
     // the write pass follows without a round trip to the host and the counts come back once,
     // below; past 1 GB the exact size is read back first
-    const size_t bound = (size_t)K * n_out * 8;
-    if (bound <= ((size_t)1 << 30)) {
-      SSC_TRY(dev_alloc((void**)&rb->pairs, bound, st));
-    } else {
+    if (!rb->pairs) {
       SSC_HIP(hipMemcpyAsync(host, dtotal, 8, hipMemcpyDeviceToHost, st));
       SSC_HIP(hipStreamSynchronize(st));
-      SSC_TRY(dev_alloc((void**)&rb->pairs, (size_t)host[0] * 8, st));
+      SSC_TRY(dev_alloc((void**)&rb->mem[2], (size_t)host[0] * 8, st));
+      rb->pairs = (int32_t*)rb->mem[2];
     }
     probe_kernel<false><<<gp, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0], grid[1], grid[2],
                                            rb->hash_in, (uint64_t)(rb->cap_in - 1), rb->nbr, nullptr, offs, rb->pairs);
     SSC_HIP(hipGetLastError());
-    SSC_HIP(hipMemcpyAsync(host, rb->pair_off_dev, (size_t)(K + 1) * 8, hipMemcpyDeviceToHost, st));
-    SSC_HIP(hipMemcpyAsync(host + K + 1, dflags, 4, hipMemcpyDeviceToHost, st));
-    SSC_HIP(hipStreamSynchronize(st));
-    for (int s = 0; s <= K; ++s) rb->pair_off[s] = host[s];
-    rb->n_pairs = host[K];
-    const int fl = (int)(host[K + 1] & 0xffffffff);
-    if (fl & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid, has b < 0, or (max b + 1) * grid volume exceeds the 32-bit key space");
-    if (fl & kFlagDup) return fail(SSCONV_E_DUPLICATE, "duplicate input site");
-    if (fl & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
   } else {
     SSC_HIP(hipMemsetAsync(rb->pair_off_dev, 0, (size_t)(K + 1) * 8, st));
-    SSC_HIP(hipMemcpyAsync(host, dflags, 4, hipMemcpyDeviceToHost, st));
-    SSC_HIP(hipStreamSynchronize(st));
-    const int fl = (int)(host[0] & 0xffffffff);
-    if (fl & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid, has b < 0, or (max b + 1) * grid volume exceeds the 32-bit key space");
-    if (fl & kFlagDup) return fail(SSCONV_E_DUPLICATE, "duplicate input site");
-    if (fl & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
-    SSC_TRY(dev_alloc((void**)&rb->pairs, 8, st));
+    if (!rb->pairs) {
+      SSC_TRY(dev_alloc((void**)&rb->mem[2], 8, st));
+      rb->pairs = (int32_t*)rb->mem[2];
+    }
   }
+  // pair offsets and flags in one copy: the single synchronisation of a submanifold build
+  SSC_HIP(hipMemcpyAsync(host, rb->pair_off_dev, (size_t)(K + 2) * 8, hipMemcpyDeviceToHost, st));
+  SSC_HIP(hipStreamSynchronize(st));
+  for (int s = 0; s <= K; ++s) rb->pair_off[s] = host[s];
+  rb->n_pairs = host[K];
+  const int fl = (int)(host[K + 1] & 0xffffffff);
+  if (fl & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid, has b < 0, or (max b + 1) * grid volume exceeds the 32-bit key space");
+  if (fl & kFlagDup) return fail(SSCONV_E_DUPLICATE, "duplicate input site");
+  if (fl & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
   return SSCONV_OK;
 }
 
