@@ -243,14 +243,14 @@ __global__ void reduce_splits(const float* __restrict__ part, int nsplit, int64_
 }
 
 template <typename T>
-__global__ void transpose_kernel(const T* __restrict__ W, int K, int rows, int cols, T* __restrict__ Wt) {
-  // W [K][rows][cols] -> Wt [K][cols][rows]
+__global__ void transpose_kernel(const T* __restrict__ W, int K, int rows, int cols, int mirror, T* __restrict__ Wt) {
+  // W [K][rows][cols] -> Wt [K][cols][rows], offsets reversed (Wt[s] = W[K-1-s]^T) when mirror
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t per = (int64_t)rows * cols;
   if (i >= per * K) return;
   const int64_t s = i / per, r = i % per;
   const int c = (int)(r / rows), rr = (int)(r % rows);
-  Wt[i] = W[s * per + (int64_t)rr * cols + c];
+  Wt[i] = W[(mirror ? K - 1 - s : s) * per + (int64_t)rr * cols + c];
 }
 
 __global__ void fill_i32(int32_t* __restrict__ p, int64_t n, int32_t v) {
@@ -358,7 +358,7 @@ int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_ruleb
     // kappa packed for the bf16 kernel in a stream-ordered scratch buffer
     void* Bp = nullptr;
     SSC_TRY(dev_alloc(&Bp, (size_t)rb->K * cin * cout * 2, st));
-    int rc = pack_b_bf16(W, rb->K, cin, cout, false, Bp, st);
+    int rc = pack_b_bf16(W, rb->K, cin, cout, false, false, Bp, st);
     if (rc == SSCONV_OK) {
       KernelTimer timer(st);
       rc = gather_bf16(feats, rb->n_in, cin, Bp, cout, rb->nbr, nullptr, rb->n_out, rb->K, out, st);
@@ -408,8 +408,8 @@ BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int co
     nparts = (size_t)L.nsplit * K;
   }
   size_t o = 0;
-  L.nbrT = o;
-  o += align256(K * (size_t)rb->n_in * 4);
+  L.nbrT = o;  // inverse neighbour map: only generated output sets need one
+  if (!rb->submanifold) o += align256(K * (size_t)rb->n_in * 4);
   L.Wt = o;
   o += align256(K * (size_t)cin * cout * sz);
   L.part = o;
@@ -420,32 +420,41 @@ BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int co
   return L;
 }
 
+// The feature gradient is the gather GEMM over the transposed neighbour map with kappa^T.  For a
+// submanifold layer the transposed map is the map itself with the offsets reversed (y = x - d(s)
+// holds exactly when x = y - d(K-1-s), d(K-1-s) = -d(s), on the same site set), so it runs on the
+// forward map with kappa^T stored in reversed offset order and no inverse map is built.
 int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout, const ssconv_rulebook* rb,
                         const void* W, void* grad_feats, char* ws, const BwdLayout& L, hipStream_t st) {
   if (rb->n_in == 0) return SSCONV_OK;
-  int32_t* nbrT = (int32_t*)(ws + L.nbrT);
+  const bool mirror = rb->submanifold != 0;
+  const int32_t* nbrT = rb->nbr;
   void* Wt = ws + L.Wt;
   const int K = rb->K;
-  const int64_t nT = (int64_t)K * rb->n_in;
-  fill_i32<<<cdiv(nT, 256), 256, 0, st>>>(nbrT, nT, -1);
-  if (rb->n_out > 0) {
-    dim3 gi(cdiv(rb->n_out, 256), K);
-    invert_nbr<<<gi, 256, 0, st>>>(rb->nbr, rb->n_out, K, rb->n_in, nbrT);
+  if (!mirror) {
+    int32_t* inv = (int32_t*)(ws + L.nbrT);
+    const int64_t nT = (int64_t)K * rb->n_in;
+    fill_i32<<<cdiv(nT, 256), 256, 0, st>>>(inv, nT, -1);
+    if (rb->n_out > 0) {
+      dim3 gi(cdiv(rb->n_out, 256), K);
+      invert_nbr<<<gi, 256, 0, st>>>(rb->nbr, rb->n_out, K, rb->n_in, inv);
+    }
+    nbrT = inv;
   }
   const int64_t nw = (int64_t)K * cin * cout;
   if (dt == SSCONV_F32) {
-    transpose_kernel<float><<<cdiv(nw, 256), 256, 0, st>>>((const float*)W, K, cout, cin, (float*)Wt);
+    transpose_kernel<float><<<cdiv(nw, 256), 256, 0, st>>>((const float*)W, K, cout, cin, mirror, (float*)Wt);
     SSC_HIP(hipGetLastError());
     KernelTimer timer(st);
     return dispatch_gg<float>(grad_out, rb->n_out, cout, Wt, cin, nbrT, rb->n_in, K, grad_feats, st);
   }
   if (use_bf16_kernel(dt, rb->n_out, cout, cin, K)) {
-    // kappa^T packed for the bf16 kernel: Bp[s][o/8][i][o%8] = W[s][o][i]
-    SSC_TRY(pack_b_bf16(W, K, cout, cin, true, Wt, st));
+    // kappa^T packed for the bf16 kernel: Bp[s][o/8][i][o%8] = W[s'][o][i], s' = s or K-1-s
+    SSC_TRY(pack_b_bf16(W, K, cout, cin, true, mirror, Wt, st));
     KernelTimer timer(st);
     return gather_bf16(grad_out, rb->n_out, cout, Wt, cin, nbrT, nullptr, rb->n_in, K, grad_feats, st);
   }
-  transpose_kernel<uint16_t><<<cdiv(nw, 256), 256, 0, st>>>((const uint16_t*)W, K, cout, cin, (uint16_t*)Wt);
+  transpose_kernel<uint16_t><<<cdiv(nw, 256), 256, 0, st>>>((const uint16_t*)W, K, cout, cin, mirror, (uint16_t*)Wt);
   SSC_HIP(hipGetLastError());
   KernelTimer timer(st);
   return dispatch_gg<uint16_t>(grad_out, rb->n_out, cout, Wt, cin, nbrT, rb->n_in, K, grad_feats, st);

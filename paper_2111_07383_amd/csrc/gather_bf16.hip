@@ -386,9 +386,9 @@ __global__ __launch_bounds__(kNT) void gather_bf16_kernel(const uint16_t* __rest
   }
 }
 
-// Bp[s][k/8][n][k%8] from kappa given as Bt[s][n][k] (transposed = 0) or as W[s][k][n]
-// (transposed = 1); one thread per 16-byte output vector.
-__global__ void pack_b_kernel(const uint16_t* __restrict__ W, int K, int ca, int cb, int transposed,
+// Bp[s][k/8][n][k%8] from kappa given as Bt[s'][n][k] (transposed = 0) or as W[s'][k][n]
+// (transposed = 1), s' = s or K-1-s (mirror); one thread per 16-byte output vector.
+__global__ void pack_b_kernel(const uint16_t* __restrict__ W, int K, int ca, int cb, int transposed, int mirror,
                               uint16_t* __restrict__ Bp) {
   const int64_t v = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int cg8 = ca / 8;
@@ -396,7 +396,7 @@ __global__ void pack_b_kernel(const uint16_t* __restrict__ W, int K, int ca, int
   if (v >= total) return;
   const int n = (int)(v % cb);
   const int kg = (int)((v / cb) % cg8);
-  const int64_t s = v / ((int64_t)cb * cg8);
+  const int64_t s = mirror ? K - 1 - v / ((int64_t)cb * cg8) : v / ((int64_t)cb * cg8);
   uint4 o;
   if (!transposed) {
     o = *reinterpret_cast<const uint4*>(W + (s * cb + n) * ca + 8 * kg);
@@ -448,10 +448,11 @@ bool gather_bf16_supported(int64_t n_src, int ca, int cb, int K) {
          bf16_smem_for(bf16_nb(cb), K) <= (size_t)kLdsLimit;
 }
 
-int pack_b_bf16(const void* W, int K, int ca, int cb, bool transposed, void* Bp, hipStream_t st) {
+int pack_b_bf16(const void* W, int K, int ca, int cb, bool transposed, bool mirror, void* Bp, hipStream_t st) {
   const int64_t total = (int64_t)K * (ca / 8) * cb;
   if (total == 0) return SSCONV_OK;
-  pack_b_kernel<<<cdiv(total, 256), 256, 0, st>>>((const uint16_t*)W, K, ca, cb, transposed ? 1 : 0, (uint16_t*)Bp);
+  pack_b_kernel<<<cdiv(total, 256), 256, 0, st>>>((const uint16_t*)W, K, ca, cb, transposed ? 1 : 0, mirror ? 1 : 0,
+                                                   (uint16_t*)Bp);
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;
 }

@@ -16,9 +16,9 @@ int gather_mfma(const void* src, int64_t n_src, ssconv_dtype dt, int ca, const v
 // bf16 kernel with 256-row tiles and packed kappa (gather_bf16.hip).
 bool gather_bf16_supported(int64_t n_src, int ca, int cb, int K);
 
-// Bp[s][k/8][n][k%8] (bf16) from Bt[s][n][k] (transposed = false) or from W[s][k][n]
-// (transposed = true), for k < ca, n < cb; ca a multiple of 8.
-int pack_b_bf16(const void* W, int K, int ca, int cb, bool transposed, void* Bp, hipStream_t st);
+// Bp[s][k/8][n][k%8] (bf16) from Bt[s'][n][k] (transposed = false) or from W[s'][k][n]
+// (transposed = true), s' = s, or K-1-s when mirrored; for k < ca, n < cb; ca a multiple of 8.
+int pack_b_bf16(const void* W, int K, int ca, int cb, bool transposed, bool mirror, void* Bp, hipStream_t st);
 
 // out[order ? order[p] : p][:] = sum_s Bt[s] (cb x ca) . src[nbr[s][p]] with Bt given packed as above;
 // src holds n_src rows.
