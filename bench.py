@@ -164,6 +164,9 @@ def parse():
                     help="write profiles/kernels_<workload>.txt from the rocprofv3 --kernel-trace --stats run in this "
                          "directory (runs on the CPU)")
     ap.add_argument("--stats-log", default="", help="stdout of that profiled run (holds the benchmark's JSON line)")
+    ap.add_argument("--counter-summary", default="",
+                    help="write profiles/counters_<workload>.txt from the rocprofv3 --pmc runs (fetch/, write/, mfma/) "
+                         "in this directory (runs on the CPU)")
     ap.add_argument("--copy-pmc", default="",
                     help="directory of the copy-calibration counter runs (default: the --traffic-summary one)")
     return ap.parse_args()
@@ -417,8 +420,79 @@ def write_stats_summary(args):
     log(f"wrote {os.path.relpath(path, ROOT)}")
 
 
+def write_counter_summary(args):
+    """Per-kernel HBM bandwidth and MFMA utilisation of one workload's step from rocprofv3 --pmc
+    runs: fetch/ and write/ (FETCH_SIZE, WRITE_SIZE) and mfma/ (GRBM_GUI_ACTIVE,
+    SQ_VALU_MFMA_BUSY_CYCLES) under args.counter_summary, copy calibration under args.copy_pmc;
+    writes profiles/counters_<workload>.txt."""
+    import collections
+    import re
+    from workloads import CONFIGS
+    spec = CONFIGS[args.config]
+    d, dc = args.counter_summary, args.copy_pmc or args.counter_summary
+    mb = args.copy_mb or 256
+
+    def name(r):
+        n = r["Kernel_Name"].replace("(anonymous namespace)::", "").replace("void ", "").replace("ssconv::", "")
+        return re.sub(r"\(.*", "", n)[:44]
+
+    def per_kernel(rows, counter):
+        vals, dur = collections.defaultdict(dict), collections.defaultdict(dict)
+        for r in rows:
+            if r["Counter_Name"] != counter:
+                continue
+            k = name(r)
+            vals[k][r["Dispatch_Id"]] = vals[k].get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+            dur[k][r["Dispatch_Id"]] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        return ({k: float(np.mean(list(v.values()))) for k, v in vals.items()},
+                {k: float(np.mean(list(v.values()))) for k, v in dur.items()},
+                {k: len(v) for k, v in vals.items()})
+
+    fetch, fdur, calls = per_kernel(_counter_rows(os.path.join(d, "fetch")), "FETCH_SIZE")
+    write, _, _ = per_kernel(_counter_rows(os.path.join(d, "write")), "WRITE_SIZE")
+    busy, mdur, _ = per_kernel(_counter_rows(os.path.join(d, "mfma")), "SQ_VALU_MFMA_BUSY_CYCLES")
+    gui, _, _ = per_kernel(_counter_rows(os.path.join(d, "mfma")), "GRBM_GUI_ACTIVE")
+    cf = _per_dispatch(_counter_rows(os.path.join(dc, "copy_fetch")), COPY_KERNEL, "FETCH_SIZE")
+    cw = _per_dispatch(_counter_rows(os.path.join(dc, "copy_write")), COPY_KERNEL, "WRITE_SIZE")
+    ff, fw = mb * 1024.0 / float(np.mean(cf)), mb * 1024.0 / float(np.mean(cw))
+    run = f"python3 bench.py --config {spec.index} --steps 3 --warmup 1 --no-cpu-baseline"
+    lines = [f"# rocprofv3 counters per kernel: {spec.name} ({spec.dtype}), one step = rule book + synthesis + "
+             "forward + backward",
+             "commands (from the repository root, TMPDIR=/tmp, each under timeout -s KILL 120):",
+             f"  rocprofv3 --pmc FETCH_SIZE --output-format csv -d {d}/fetch -o p -- {run}",
+             f"  rocprofv3 --pmc WRITE_SIZE --output-format csv -d {d}/write -o p -- {run}",
+             f"  rocprofv3 --pmc GRBM_GUI_ACTIVE SQ_VALU_MFMA_BUSY_CYCLES --output-format csv -d {d}/mfma -o p -- {run}",
+             f"  (copy calibration as in profiles/traffic_*.txt: fetch factor {ff:.4f}, write factor {fw:.4f})",
+             f"  python3 bench.py --config {spec.index} --copy-mb {mb} --counter-summary {d}"
+             + (f" --copy-pmc {dc}" if dc != d else ""),
+             "HBM bytes = FETCH_SIZE and WRITE_SIZE scaled by the copy calibration; GB/s over the dispatch's own",
+             "duration in the counter run; MFMA busy = SQ_VALU_MFMA_BUSY_CYCLES / (1024 SIMDs x GRBM_GUI_ACTIVE / 8",
+             "XCDs), i.e. the share of all SIMD cycles with the matrix core busy; clock = GRBM_GUI_ACTIVE / 8 / duration",
+             "(shown for launches of 100 us or more; shorter ones are dominated by launch overhead).",
+             "",
+             f"{'kernel':44s} {'calls':>5s} {'us':>8s} {'MB read':>9s} {'MB write':>9s} {'GB/s':>8s} {'%HBM':>6s} "
+             f"{'MFMA%':>6s} {'GHz':>5s}"]
+    order = sorted(fetch, key=lambda k: -fdur.get(k, 0.0) * calls.get(k, 0))
+    for k in order[:16]:
+        rd, wr = fetch[k] * ff * 1024, write.get(k, 0.0) * fw * 1024
+        us = fdur[k] / 1e3
+        gbs = (rd + wr) / max(fdur[k], 1.0)
+        mf = busy.get(k, 0.0) / (1024.0 * gui[k] / 8.0) if gui.get(k) else 0.0
+        ghz = gui[k] / 8.0 / mdur[k] if gui.get(k) and mdur.get(k) else 0.0
+        clk = f"{ghz:5.2f}" if us >= 100 else "    -"   # GUI_ACTIVE includes launch overhead
+        lines.append(f"{k:44s} {calls[k]:5d} {us:8.1f} {rd / 1e6:9.1f} {wr / 1e6:9.1f} {gbs:8.0f} "
+                     f"{100 * gbs / HBM_PEAK_GBS:6.1f} {100 * mf:6.1f} {clk}")
+    path = os.path.join(ROOT, "profiles", f"counters_{spec.name}.txt")
+    with open(path, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+    log(f"wrote {os.path.relpath(path, ROOT)}")
+
+
 def main():
     args = parse()
+    if args.counter_summary:
+        write_counter_summary(args)
+        return
     if args.stats_summary:
         write_stats_summary(args)
         return
