@@ -96,6 +96,16 @@ typedef struct ssconv_rulebook* ssconv_rulebook_t;
 const char* ssconv_last_error(void);
 const char* ssconv_version(void);
 
+/* Device memory the library allocates (rule book buffers, the packed bf16 kernel
+ * of ssconv_forward) comes from a per-process cache: a freed block is kept with
+ * an event recorded on the freeing stream and reused, on the same stream at
+ * once, on another stream after waiting for that event; up to 8 GB of free
+ * blocks are kept.  ssconv_empty_cache waits for and releases every free
+ * block (blocks in use are untouched); ssconv_cached_bytes returns the bytes
+ * held in free blocks.  Both are safe to call at any time. */
+int ssconv_empty_cache(void);
+int64_t ssconv_cached_bytes(void);
+
 /* ---- steerable basis (host) ---------------------------------------------
  * Sec. 3.2.1, Eq. 7-8.  Computed on the host in fp64 from Clebsch-Gordan
  * coefficients (Racah's formula) carried to the real harmonic basis.

@@ -12,8 +12,10 @@ from .binding import (  # noqa: F401
     basis_desc,
     basis_info,
     build_rulebook,
+    cached_bytes,
     debug_kernel_ms,
     debug_set,
+    empty_cache,
     forward,
     gate_backward,
     gate_forward,

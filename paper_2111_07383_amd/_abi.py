@@ -31,6 +31,8 @@ class BasisDesc(ctypes.Structure):
 SIGNATURES = {
     "ssconv_last_error": (c_char_p, []),
     "ssconv_version": (c_char_p, []),
+    "ssconv_empty_cache": (c_int, []),
+    "ssconv_cached_bytes": (c_int64, []),
     "ssconv_basis_info": (c_int, [POINTER(BasisDesc), POINTER(c_int64), POINTER(c_int64)]),
     "ssconv_basis_build": (c_int, [POINTER(BasisDesc), c_void_p]),
     "ssconv_build_rulebook": (c_int, [c_void_p, c_int64, POINTER(c_int), c_int, c_int, c_int, c_void_p,

@@ -249,6 +249,16 @@ def debug_set(option: int, value: int) -> None:
     check(lib().ssconv_debug_set(int(option), int(value)), "ssconv_debug_set")
 
 
+def empty_cache() -> None:
+    """Waits for and releases the library's cached free device blocks."""
+    check(lib().ssconv_empty_cache(), "ssconv_empty_cache")
+
+
+def cached_bytes() -> int:
+    """Bytes held in the library's cached free device blocks."""
+    return int(lib().ssconv_cached_bytes())
+
+
 def debug_kernel_ms() -> Tuple[int, float]:
     """(launches, total ms) of the gather-GEMM kernels timed on this thread since
     debug_set(4, 1); waits for the last of them."""

@@ -1,10 +1,11 @@
 // Error reporting, allocation and field tables shared by the SS-Conv entry points.
 #include "common.hpp"
 
+#include <atomic>
+#include <mutex>
+#include <unordered_map>
 #include <utility>
 #include <vector>
-
-#include <atomic>
 
 namespace ssconv {
 
@@ -42,6 +43,34 @@ int fail(int code, const char* fmt, ...) {
   return code;
 }
 
+// Device memory cache.  A block the library frees is kept with an event recorded on the freeing
+// stream and handed out again: reuse on the same stream needs nothing (stream order), reuse on
+// another stream first makes that stream wait for the event.  A stream-ordered allocation costs
+// tens of microseconds of host time after a synchronisation and can block the host while the
+// device is busy; a cache hit costs a lock and a short search.  Blocks come in 64 KB steps; a
+// request takes the smallest free block of at least its size and at most twice it (+ 1 MB).
+// Free blocks beyond kCacheLimit bytes are released, oldest first.
+namespace {
+struct Block {
+  void* p = nullptr;
+  size_t bytes = 0;
+  int dev = 0;
+  hipStream_t stream = nullptr;
+  hipEvent_t ev = nullptr;
+};
+constexpr size_t kCacheLimit = (size_t)8 << 30;
+std::mutex g_cache_mu;
+std::vector<Block> g_free_blocks;                // oldest first
+std::unordered_map<void*, Block> g_live_blocks;  // handed out
+size_t g_free_bytes = 0;
+
+void release_block(Block& b) {  // caller holds the lock; the block is stream-ordered after its event
+  (void)hipFreeAsync(b.p, b.stream);
+  if (b.ev) (void)hipEventDestroy(b.ev);
+  (void)hipGetLastError();
+}
+}  // namespace
+
 int dev_alloc(void** p, size_t bytes, hipStream_t stream) {
   *p = nullptr;
   if (bytes == 0) bytes = 256;
@@ -53,17 +82,92 @@ int dev_alloc(void** p, size_t bytes, hipStream_t stream) {
     }
     g_debug_fail_alloc.store(n - 1);
   }
-  hipError_t e = hipMallocAsync(p, bytes, stream);
-  if (e != hipSuccess || !*p) {
-    *p = nullptr;
-    (void)hipGetLastError();
-    return fail(SSCONV_E_NOMEM, "device allocation of %zu bytes failed: %s", bytes, hipGetErrorString(e));
+  const size_t want = (bytes + 65535) & ~(size_t)65535;
+  int dev = 0;
+  SSC_HIP(hipGetDevice(&dev));
+  {
+    std::lock_guard<std::mutex> lk(g_cache_mu);
+    size_t best = g_free_blocks.size();
+    for (size_t i = 0; i < g_free_blocks.size(); ++i) {
+      const Block& b = g_free_blocks[i];
+      if (b.dev == dev && b.bytes >= want && b.bytes <= 2 * want + ((size_t)1 << 20) &&
+          (best == g_free_blocks.size() || b.bytes < g_free_blocks[best].bytes))
+        best = i;
+    }
+    if (best < g_free_blocks.size()) {
+      Block b = g_free_blocks[best];
+      if (b.stream != stream) {
+        hipError_t e = hipStreamWaitEvent(stream, b.ev, 0);
+        if (e != hipSuccess) {
+          (void)hipGetLastError();
+          return fail(SSCONV_E_HIP, "hipStreamWaitEvent: %s", hipGetErrorString(e));
+        }
+      }
+      g_free_blocks.erase(g_free_blocks.begin() + (std::ptrdiff_t)best);
+      g_free_bytes -= b.bytes;
+      b.stream = stream;
+      g_live_blocks[b.p] = b;
+      *p = b.p;
+      return SSCONV_OK;
+    }
   }
+  hipError_t e = hipMallocAsync(p, want, stream);
+  if (e != hipSuccess || !*p) {
+    (void)hipGetLastError();
+    {  // give the cached blocks of this device back and try once more
+      std::lock_guard<std::mutex> lk(g_cache_mu);
+      for (size_t i = 0; i < g_free_blocks.size();) {
+        if (g_free_blocks[i].dev == dev) {
+          g_free_bytes -= g_free_blocks[i].bytes;
+          release_block(g_free_blocks[i]);
+          g_free_blocks.erase(g_free_blocks.begin() + (std::ptrdiff_t)i);
+        } else {
+          ++i;
+        }
+      }
+    }
+    *p = nullptr;
+    e = hipMallocAsync(p, want, stream);
+    if (e != hipSuccess || !*p) {
+      *p = nullptr;
+      (void)hipGetLastError();
+      return fail(SSCONV_E_NOMEM, "device allocation of %zu bytes failed: %s", bytes, hipGetErrorString(e));
+    }
+  }
+  std::lock_guard<std::mutex> lk(g_cache_mu);
+  Block b;
+  b.p = *p;
+  b.bytes = want;
+  b.dev = dev;
+  b.stream = stream;
+  g_live_blocks[b.p] = b;
   return SSCONV_OK;
 }
 
 void dev_free(void* p, hipStream_t stream) {
-  if (p) (void)hipFreeAsync(p, stream);
+  if (!p) return;
+  std::lock_guard<std::mutex> lk(g_cache_mu);
+  auto it = g_live_blocks.find(p);
+  if (it == g_live_blocks.end()) {
+    (void)hipFreeAsync(p, stream);
+    (void)hipGetLastError();
+    return;
+  }
+  Block b = it->second;
+  g_live_blocks.erase(it);
+  b.stream = stream;
+  if (!b.ev && hipEventCreateWithFlags(&b.ev, hipEventDisableTiming) != hipSuccess) b.ev = nullptr;
+  if (!b.ev || hipEventRecord(b.ev, stream) != hipSuccess) {
+    release_block(b);
+    return;
+  }
+  g_free_blocks.push_back(b);
+  g_free_bytes += b.bytes;
+  while (g_free_bytes > kCacheLimit && !g_free_blocks.empty()) {
+    g_free_bytes -= g_free_blocks.front().bytes;
+    release_block(g_free_blocks.front());
+    g_free_blocks.erase(g_free_blocks.begin());
+  }
 }
 
 int64_t debug_hash_capacity() { return g_debug_hash_cap.load(); }
@@ -132,6 +236,26 @@ extern "C" int ssconv_debug_set(int option, int64_t value) {
     return SSCONV_OK;
   }
   return ssconv::fail(SSCONV_E_INVALID, "unknown debug option %d", option);
+}
+
+extern "C" int ssconv_empty_cache(void) {
+  using namespace ssconv;
+  std::lock_guard<std::mutex> lk(g_cache_mu);
+  for (Block& b : g_free_blocks) {
+    if (b.ev) (void)hipEventSynchronize(b.ev);
+    (void)hipFree(b.p);
+    if (b.ev) (void)hipEventDestroy(b.ev);
+  }
+  (void)hipGetLastError();
+  g_free_blocks.clear();
+  g_free_bytes = 0;
+  return SSCONV_OK;
+}
+
+extern "C" int64_t ssconv_cached_bytes(void) {
+  using namespace ssconv;
+  std::lock_guard<std::mutex> lk(g_cache_mu);
+  return (int64_t)g_free_bytes;
 }
 
 extern "C" int ssconv_debug_kernel_ms(int64_t* count, float* total_ms) {

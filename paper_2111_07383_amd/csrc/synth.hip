@@ -59,24 +59,40 @@ __device__ __forceinline__ int64_t coeff_off(const SynthArgs& a, int eo, int fo,
   return off + (int64_t)fi * a.nq[k][a.in.l[ei]];
 }
 
+// Loads of the coefficients and basis values of one element are issued kQL at a time with no
+// dependence between them, so an element costs one memory round trip per kQL basis functions.
+constexpr int kQL = 8;
+
+// grid (ceil(cout * cin / 256), K): the workgroup row is one offset s, so the element index fits
+// in 32 bits and the (out, in) channel split is one 32-bit division.
 template <typename T>
 __global__ __launch_bounds__(256) void synth_kernel(SynthArgs a, const float* __restrict__ basis,
                                                     const float* __restrict__ coeffs, T* __restrict__ W) {
-  const int64_t total = (int64_t)a.K * a.cout * a.cin;
-  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (idx >= total) return;
-  const int ci = (int)(idx % a.cin);
-  const int co = (int)((idx / a.cin) % a.cout);
-  const int s = (int)(idx / ((int64_t)a.cin * a.cout));
+  const int plane = a.cout * a.cin;
+  const int idx = blockIdx.x * 256 + threadIdx.x;
+  if (idx >= plane) return;
+  const int s = blockIdx.y;
+  const int co = idx / a.cin, ci = idx - co * a.cin;
   const ChanInfo o = chan_info(a.out, co), i = chan_info(a.in, ci);
   const int k = o.l, l = i.l, dk = 2 * k + 1, dl = 2 * l + 1;
   const int nq = a.nq[k][l];
-  const int64_t off = coeff_off(a, o.entry, o.field, k, i.entry, i.field);
+  const float* cp = coeffs + coeff_off(a, o.entry, o.field, k, i.entry, i.field);
   const float* bp = basis + a.base[k][l] + ((int64_t)s * dk + o.comp) * dl + i.comp;
   const int64_t qstride = (int64_t)a.K * dk * dl;
   float acc = 0.f;
-  for (int q = 0; q < nq; ++q) acc = fmaf(coeffs[off + q], bp[q * qstride], acc);
-  W[idx] = DT<T>::from_f(acc);
+  for (int q0 = 0; q0 < nq; q0 += kQL) {
+    float cv[kQL], bv[kQL];
+#pragma unroll
+    for (int j = 0; j < kQL; ++j) {
+      const bool ok = q0 + j < nq;
+      cv[j] = ok ? cp[q0 + j] : 0.f;
+      bv[j] = ok ? bp[(q0 + j) * qstride] : 0.f;
+    }
+#pragma unroll
+    for (int j = 0; j < kQL; ++j)
+      if (q0 + j < nq) acc = fmaf(cv[j], bv[j], acc);
+  }
+  W[(int64_t)s * plane + idx] = DT<T>::from_f(acc);
 }
 
 // One workgroup per (in field, out field) pair; its coefficients are done 8 at a time in
@@ -132,12 +148,14 @@ __global__ __launch_bounds__(256) void synth_adjoint_kernel(SynthArgs a, const f
 
 int launch_synth(const SynthArgs& a, const float* basis, const float* coeffs, ssconv_dtype dt, void* W,
                  hipStream_t st) {
-  const int64_t total = (int64_t)a.K * a.cout * a.cin;
-  if (total == 0) return SSCONV_OK;
+  const int64_t plane = (int64_t)a.cout * a.cin;
+  if (plane == 0 || a.K == 0) return SSCONV_OK;
+  if (plane > 0x7fffffffll) return fail(SSCONV_E_INVALID, "Cout * Cin must be below 2^31");
+  const dim3 g((unsigned)cdiv(plane, 256), (unsigned)a.K);
   if (dt == SSCONV_F32)
-    synth_kernel<float><<<cdiv(total, 256), 256, 0, st>>>(a, basis, coeffs, (float*)W);
+    synth_kernel<float><<<g, 256, 0, st>>>(a, basis, coeffs, (float*)W);
   else
-    synth_kernel<uint16_t><<<cdiv(total, 256), 256, 0, st>>>(a, basis, coeffs, (uint16_t*)W);
+    synth_kernel<uint16_t><<<g, 256, 0, st>>>(a, basis, coeffs, (uint16_t*)W);
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;
 }

@@ -59,8 +59,9 @@ class Stack:
             s = L.layer
             if L.rb is not None:
                 L.rb.close()
-            L.rb = B.Rulebook(c, L.grid, s.ksize, s.stride, s.submanifold)
+            # synthesis first: it runs on the GPU while the host prepares the rule book
             L.W = B.synth_kernel(L.desc, L.basis, L.coeffs, self.dtype)
+            L.rb = B.Rulebook(c, L.grid, s.ksize, s.stride, s.submanifold)
             L.x = h
             L.y = B.forward(h, L.rb, L.W)
             h = B.gate_forward(regular_fields(s), L.y) if s.gated else L.y

@@ -155,3 +155,36 @@ def test_kernel_timing_hook(dt):
     P.forward(x, rb, W)                                  # timing off: nothing recorded
     assert _code(P.debug_kernel_ms) == E_INVALID
     rb.close()
+
+
+def test_device_memory_cache():
+    """Freed library blocks are cached and reused, also on another stream (after an event wait),
+    without changing any result; empty_cache releases them."""
+    P.empty_cache()
+    assert P.cached_bytes() == 0
+    c = torch.from_numpy(_coords(11, 4000, 24)).to(DEV)
+    ref = P.Rulebook(c, 24, 3)
+    W = (torch.randn((27, 48, 32), device=DEV) * 0.1).to(torch.bfloat16)
+    x = torch.randn((ref.n_in, 32), device=DEV).to(torch.bfloat16)
+    y_ref = P.forward(x, ref, W)
+    P.Rulebook(c, 24, 3).close()
+    assert P.cached_bytes() > 0
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(2):                               # blocks freed on the default stream, reused here
+            rb = P.Rulebook(c, 24, 3, stream=side)
+            y = P.forward(x, rb, W, stream=side)
+            nb, pairs = rb.neighbours(stream=side), rb.pairs(stream=side)
+            side.synchronize()
+            torch.testing.assert_close(nb, ref.neighbours(), rtol=0, atol=0)
+            torch.testing.assert_close(pairs, ref.pairs(), rtol=0, atol=0)
+            torch.testing.assert_close(y, y_ref, rtol=0, atol=0)
+            rb.close()
+    torch.cuda.synchronize()
+    P.empty_cache()
+    assert P.cached_bytes() == 0
+    rb = P.Rulebook(c, 24, 3)                            # allocations after emptying still work
+    torch.testing.assert_close(rb.neighbours(), ref.neighbours(), rtol=0, atol=0)
+    rb.close()
+    ref.close()
