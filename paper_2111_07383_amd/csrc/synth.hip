@@ -95,10 +95,11 @@ __global__ __launch_bounds__(256) void synth_kernel(SynthArgs a, const float* __
   W[(int64_t)s * plane + idx] = DT<T>::from_f(acc);
 }
 
-// One workgroup per (in field, out field) pair; its coefficients are done 8 at a time in
+// One workgroup per (in field, out field) pair; its coefficients are done 16 at a time in
 // registers: thread partial sums over the block's elements in a fixed order, a fixed butterfly
 // within each wavefront, then the four wavefront sums added in order (independent of scheduling).
-constexpr int kQB = 8;
+constexpr int kQB = 16;  // coefficients per pass (every (k, l) block of the workloads fits one pass)
+constexpr int kEU = 4;   // elements per thread per step, their loads issued together
 
 __global__ __launch_bounds__(256) void synth_adjoint_kernel(SynthArgs a, const float* __restrict__ basis,
                                                             const float* __restrict__ dW, float* __restrict__ dcoef) {
@@ -121,12 +122,21 @@ __global__ __launch_bounds__(256) void synth_adjoint_kernel(SynthArgs a, const f
     float acc[kQB];
 #pragma unroll
     for (int j = 0; j < kQB; ++j) acc[j] = 0.f;
-    for (int e = threadIdx.x; e < n; e += 256) {
-      const int s = e / (dk * dl), r = e % (dk * dl), aa = r / dl, bb = r % dl;
-      const float g = dW[((int64_t)s * a.cout + ro + aa) * a.cin + cc + bb];
+    for (int e0 = threadIdx.x; e0 < n; e0 += 256 * kEU) {
+      float g[kEU], bv[kEU][kQB];
 #pragma unroll
-      for (int j = 0; j < kQB; ++j)
-        if (q0 + j < nq) acc[j] = fmaf(g, bp[(q0 + j) * qstride + e], acc[j]);
+      for (int u = 0; u < kEU; ++u) {
+        const int e = e0 + u * 256;
+        const bool ok = e < n;
+        const int s = e / (dk * dl), r = e - s * (dk * dl), aa = r / dl, bb = r - aa * dl;
+        g[u] = ok ? dW[((int64_t)s * a.cout + ro + aa) * a.cin + cc + bb] : 0.f;
+#pragma unroll
+        for (int j = 0; j < kQB; ++j) bv[u][j] = (ok && q0 + j < nq) ? bp[(q0 + j) * qstride + e] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kEU; ++u)
+#pragma unroll
+        for (int j = 0; j < kQB; ++j) acc[j] = fmaf(g[u], bv[u][j], acc[j]);
     }
 #pragma unroll
     for (int j = 0; j < kQB; ++j) {
