@@ -210,7 +210,10 @@ int ssconv_gate_backward(const ssconv_fields* fields /*host*/, const void* x, co
  * neighbour indices in LDS; 5 = bf16 convolutions use the generic
  * gather-GEMM kernel instead of the bf16 pipeline kernel; 6 = the bf16 kernel
  * gradient uses per-offset splits instead of balanced work units; 7 = the
- * fp32 kernel gradient loads rows into registers instead of an LDS ring; results
+ * fp32 kernel gradient loads rows into registers instead of an LDS ring; 8 = the
+ * generic gather-GEMM kernel splits every tile's offsets three ways (fp32
+ * partials added in split order), which it otherwise does only when its tiles
+ * leave compute units idle; results
  * agree within the dtype's tolerance for every value); option 4 = kernel
  * timing: a nonzero value switches it on and clears this thread's log, 0
  * switches it off; while on, every gather-GEMM kernel launch (the one of

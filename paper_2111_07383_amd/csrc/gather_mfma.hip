@@ -89,7 +89,7 @@ __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restric
                                                           const T* __restrict__ Bt, int cb,
                                                           const int32_t* __restrict__ nbr,
                                                           const int32_t* __restrict__ order, int64_t n_pos, int K,
-                                                          T* __restrict__ out) {
+                                                          T* __restrict__ out, float* __restrict__ part) {
   using SH = Shape<T, WMB, WNB, S, NW>;
   constexpr int BM = SH::BM, RV = SH::RV, VE = SH::VE, BJ = SH::BJ, L = SH::L;
   // dynamic LDS only (base at LDS address 0): stages | junk | bmask | act | count | index table
@@ -134,7 +134,11 @@ __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restric
     if (lane == 0) n_act_p[0] = base;
   }
   __syncthreads();
-  const int n_act = n_act_p[0];
+  // split z of gridDim.z takes its share of the present offsets, in order, and writes an fp32
+  // partial (part != nullptr); the splits are added in order by split_reduce_kernel
+  const int nsplit = gridDim.z, z = blockIdx.z;  // at most 8 splits of at most 128 offsets
+  const int a0 = n_act_p[0] * z / nsplit;
+  const int n_act = n_act_p[0] * (z + 1) / nsplit - a0;
   const int total = n_act * ca;
   const int nchunk = (total + kBK - 1) / kBK;
 
@@ -152,7 +156,7 @@ __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restric
 #define SSC_REFRESH()                                                                               \
   do {                                                                                              \
     const bool live_ = r_slot < n_act;                                                              \
-    const int s_ = live_ ? act[r_slot] : 0;                                                         \
+    const int s_ = live_ ? act[a0 + r_slot] : 0;                                                    \
     _Pragma("unroll") for (int mb = 0; mb < WMB; ++mb) {                                            \
       const int idx_ = live_ ? ix_get(idx_tab[s_ * BM + 16 * (w * WMB + mb) + r16]) : -1;           \
       alive[mb] = idx_ >= 0;                                                                        \
@@ -276,6 +280,23 @@ __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restric
 #undef SSC_ISSUE
 #undef SSC_REFRESH
 
+  if (part) {
+#pragma unroll
+    for (int mb = 0; mb < WMB; ++mb) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t p = p0 + 16 * (w * WMB + mb) + 4 * g + i;
+        if (p >= n_pos) continue;
+        float* prow = part + ((int64_t)z * n_pos + p) * cb;
+#pragma unroll
+        for (int nb = 0; nb < WNB; ++nb) {
+          const int col = n0 + 16 * nb + r16;
+          if (col < cb) prow[col] = acc[mb][nb][i];
+        }
+      }
+    }
+    return;
+  }
 #pragma unroll
   for (int mb = 0; mb < WMB; ++mb) {
 #pragma unroll
@@ -293,10 +314,39 @@ __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restric
   }
 }
 
+// out[order ? order[p] : p][col] = sum over the splits, in split order, of part[z][p][col].
+template <typename T>
+__global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restrict__ part, int nsplit, int64_t n_pos,
+                                                           int cb, const int32_t* __restrict__ order,
+                                                           T* __restrict__ out) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t n = n_pos * cb;
+  if (e >= n) return;
+  float acc = part[e];
+  for (int z = 1; z < nsplit; ++z) acc += part[(int64_t)z * n + e];
+  const int64_t p = e / cb, col = e - p * cb;
+  out[(order ? order[p] : p) * cb + col] = DT<T>::from_f(acc);
+}
+
 template <typename T, int WMB, int WNB, int S, int NW, typename IX>
 size_t smem_bytes(int K) {
   using SH = Shape<T, WMB, WNB, S, NW>;
   return (size_t)S * SH::STAGE + 1024 + kMaxK * 5 + 16 + (size_t)K * SH::BM * sizeof(IX);
+}
+
+// Offset splits for a launch of `tiles` workgroups (one per compute unit at a time): the count in
+// 1..8 (at most K) with the fewest rounds of the 256 compute units per unit of work, each split
+// charged 3% for its own index loading and partial traffic; 1 when the tiles fill the chip.
+int pick_nsplit(int64_t tiles, int K) {
+  constexpr int64_t kCUs = 256;
+  int best = 1;
+  double best_cost = 1e30;
+  for (int ns = 1; ns <= 8 && ns <= K; ++ns) {
+    const double rounds = (double)((tiles * ns + kCUs - 1) / kCUs);
+    const double cost = rounds / ns + 0.03 * (ns - 1);
+    if (cost < best_cost - 1e-9) best_cost = cost, best = ns;
+  }
+  return best;
 }
 
 template <typename T, int WMB, int WNB, int S, int NW, typename IX>
@@ -306,9 +356,25 @@ int launch(const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, 
   const size_t smem = smem_bytes<T, WMB, WNB, S, NW, IX>(K);
   auto kern = gather_mfma_kernel<T, WMB, WNB, S, NW, IX>;
   SSC_HIP(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem));
-  dim3 grid(cdiv(n_pos, SH::BM), cdiv(cb, SH::BN));
-  kern<<<grid, SH::NT, smem, st>>>((const T*)src, ca, (const T*)Bt, cb, nbr, order, n_pos, K, (T*)out);
-  SSC_HIP(hipGetLastError());
+  const int64_t mt = cdiv(n_pos, SH::BM), nt = cdiv(cb, SH::BN);
+  const int nsplit = debug_gather_variant() == 8 ? std::min(K, 3) : pick_nsplit(mt * nt, K);
+  if (nsplit == 1) {
+    kern<<<dim3(mt, nt, 1), SH::NT, smem, st>>>((const T*)src, ca, (const T*)Bt, cb, nbr, order, n_pos, K, (T*)out,
+                                                 nullptr);
+    SSC_HIP(hipGetLastError());
+    return SSCONV_OK;
+  }
+  float* part = nullptr;
+  SSC_TRY(dev_alloc((void**)&part, (size_t)nsplit * n_pos * cb * 4, st));
+  kern<<<dim3(mt, nt, nsplit), SH::NT, smem, st>>>((const T*)src, ca, (const T*)Bt, cb, nbr, order, n_pos, K,
+                                                    (T*)out, part);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess) {
+    split_reduce_kernel<T><<<cdiv(n_pos * cb, 256), 256, 0, st>>>(part, nsplit, n_pos, cb, order, (T*)out);
+    e = hipGetLastError();
+  }
+  dev_free(part, st);
+  if (e != hipSuccess) return fail(SSCONV_E_HIP, "gather launch: %s", hipGetErrorString(e));
   return SSCONV_OK;
 }
 
@@ -381,7 +447,7 @@ int gather_mfma(const void* src, int64_t n_src, ssconv_dtype dt, int ca, const v
                 const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st) {
   if (n_pos == 0) return SSCONV_OK;
   // tuning overrides (same results): 1 = four wavefronts of 32 rows, 2 = four of 16 rows,
-  // 3 = no 16-bit index table
+  // 3 = no 16-bit index table, 8 = three offset splits (in launch)
   const int64_t variant = debug_gather_variant();
   Cfg c;
   if (!pick_cfg(dt, cb, K, variant == 3 ? INT64_MAX : n_src, &c))

@@ -139,7 +139,8 @@ def test_forward_backward_deterministic():
     rb2.close()
 
 
-@pytest.mark.parametrize("i,variant", [(2, 1), (2, 2), (2, 3), (3, 3), (2, 7), (3, 7), (4, 5), (4, 6)])
+@pytest.mark.parametrize("i,variant", [(2, 1), (2, 2), (2, 3), (3, 3), (2, 7), (3, 7), (4, 5), (4, 6), (2, 8),
+                                       (3, 8)])
 def test_kernel_selection_overrides(i, variant):
     """Every alternative kernel configuration (forced from the host) stays within tolerance."""
     print(f"config {i} kernel variant {variant}", flush=True)
