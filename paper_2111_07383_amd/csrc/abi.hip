@@ -63,7 +63,7 @@ extern "C" int ssconv_backward(const void* feats, const void* grad_out, ssconv_d
   }
   if (grad_coeffs) {
     float* dW = nullptr;
-    SSC_TRY(conv_backward_dw(feats, grad_out, dtype, cin, cout, rb, ws, L, &dW, stream));
+    SSC_TRY(conv_backward_dw(feats, grad_out, dtype, cin, cout, rb, sa.out, sa.in, ws, L, &dW, stream));
     SSC_TRY(launch_synth_adjoint(sa, basis, dW, grad_coeffs, stream));
   }
   return SSCONV_OK;

@@ -55,6 +55,21 @@ struct FieldTab {
 
 int make_fieldtab(const ssconv_fields* f, FieldTab* t);
 
+// Position of dW[s][o][i] in the field-pair-blocked layout of the kernel gradient: the
+// K*(2k+1)*(2l+1) values of each (out field, in field) pair are contiguous, in (s, a, b) order
+// (a, b = component in the out and in field), and the pair of out field rows [ro, ro+dk) and in
+// field columns [cc, cc+dl) starts at K*(ro*cin + dk*cc), so the layout is a permutation of
+// [K][cout][cin].  The coefficient gradient then reads each pair's block contiguously.
+__device__ __forceinline__ int64_t dw_block_pos(const FieldTab& fout, const FieldTab& fin, int K, int cin, int s,
+                                                int o, int i) {
+  int eo = 0, ei = 0;
+  while (eo + 1 < fout.n && o >= fout.ch0[eo + 1]) ++eo;
+  while (ei + 1 < fin.n && i >= fin.ch0[ei + 1]) ++ei;
+  const int dk = 2 * fout.l[eo] + 1, dl = 2 * fin.l[ei] + 1;
+  const int ro = fout.ch0[eo] + (o - fout.ch0[eo]) / dk * dk, cc = fin.ch0[ei] + (i - fin.ch0[ei]) / dl * dl;
+  return (int64_t)K * ((int64_t)ro * cin + (int64_t)dk * cc) + ((int64_t)s * dk + (o - ro)) * dl + (i - cc);
+}
+
 // ---------------------------------------------------------------------------
 // bf16 helpers (storage as uint16, round-to-nearest-even from fp32)
 // ---------------------------------------------------------------------------

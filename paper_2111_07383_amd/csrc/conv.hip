@@ -234,12 +234,16 @@ __global__ __launch_bounds__(kNT) void dw_gemm(const T* __restrict__ G, int cout
   }
 }
 
-__global__ void reduce_splits(const float* __restrict__ part, int nsplit, int64_t n, float* __restrict__ dst) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= n) return;
+// dW (field-pair-blocked, dw_block_pos) = sum of the splits' [K][cout][cin] partials, in split order.
+__global__ void reduce_splits(const float* __restrict__ part, int nsplit, int64_t n, FieldTab fout, FieldTab fin,
+                              int K, int cin, int cout, float* __restrict__ dst) {
+  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (e >= n) return;
   float acc = 0.f;
-  for (int j = 0; j < nsplit; ++j) acc += part[(int64_t)j * n + i];
-  dst[i] = acc;
+  for (int j = 0; j < nsplit; ++j) acc += part[(int64_t)j * n + e];
+  const int64_t plane = (int64_t)cin * cout;
+  const int s = (int)(e / plane), r = (int)(e - s * plane), o = r / cin, i = r - o * cin;
+  dst[dw_block_pos(fout, fin, K, cin, s, o, i)] = acc;
 }
 
 template <typename T>
@@ -391,7 +395,7 @@ static bool use_kgrad_units(const ssconv_rulebook* rb, ssconv_dtype dt, int cin,
 }
 
 // Work units of the kernel gradient: bf16 ~512 (one workgroup each, launched in row order), fp32
-// enough wavefront tasks for two rounds of the wavefront slots.
+// enough wavefront tasks for one round of the wavefront slots.
 static KgradUnits plan_units(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout) {
   if (dt == SSCONV_F32) return kgrad_units(rb, kgrad_f32_units_want(rb, cin, cout), false);
   return kgrad_units(rb, kKgradUnits, true);
@@ -461,7 +465,8 @@ int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout
 }
 
 int conv_backward_dw(const void* feats, const void* grad_out, ssconv_dtype dt, int cin, int cout,
-                     const ssconv_rulebook* rb, char* ws, const BwdLayout& L, float** dW_out, hipStream_t st) {
+                     const ssconv_rulebook* rb, const FieldTab& fout, const FieldTab& fin, char* ws,
+                     const BwdLayout& L, float** dW_out, hipStream_t st) {
   float* part = (float*)(ws + L.part);
   float* dW = (float*)(ws + L.dW);
   *dW_out = dW;
@@ -473,7 +478,7 @@ int conv_backward_dw(const void* feats, const void* grad_out, ssconv_dtype dt, i
       SSC_TRY(kgrad_f32(grad_out, feats, cin, cout, rb, units, part, st));
     else
       SSC_TRY(kgrad_bf16(grad_out, rb->n_out, feats, rb->n_in, cin, cout, rb, units, part, st));
-    return reduce_units(part, units, (int64_t)cin * cout, dW, st);
+    return reduce_units(part, units, cin, cout, fout, fin, dW, st);
   }
   if (kgrad_supported(dt, cin, cout))
     SSC_TRY(kgrad_partials(grad_out, feats, dt, cin, cout, rb, kgrad_plan(rb, dt, cin, cout), part, st));
@@ -481,7 +486,7 @@ int conv_backward_dw(const void* feats, const void* grad_out, ssconv_dtype dt, i
     SSC_TRY(dispatch_dw<float>(grad_out, cout, feats, cin, rb->pairs, rb->pair_off_dev, K, L.nsplit, part, st));
   else
     SSC_TRY(dispatch_dw<uint16_t>(grad_out, cout, feats, cin, rb->pairs, rb->pair_off_dev, K, L.nsplit, part, st));
-  reduce_splits<<<cdiv(n, 256), 256, 0, st>>>(part, L.nsplit, n, dW);
+  reduce_splits<<<cdiv(n, 256), 256, 0, st>>>(part, L.nsplit, n, fout, fin, K, cin, cout, dW);
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;
 }

@@ -15,7 +15,9 @@ int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_ruleb
 BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout);
 int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout, const ssconv_rulebook* rb,
                         const void* W, void* grad_feats, char* ws, const BwdLayout& L, hipStream_t st);
+// Kernel gradient dW in the field-pair-blocked layout (dw_block_pos) of the fields fout, fin.
 int conv_backward_dw(const void* feats, const void* grad_out, ssconv_dtype dt, int cin, int cout,
-                     const ssconv_rulebook* rb, char* ws, const BwdLayout& L, float** dW_out, hipStream_t st);
+                     const ssconv_rulebook* rb, const FieldTab& fout, const FieldTab& fin, char* ws,
+                     const BwdLayout& L, float** dW_out, hipStream_t st);
 
 }  // namespace ssconv

@@ -282,14 +282,18 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
     }
 }
 
-__global__ void reduce_units_kernel(const float* __restrict__ part, KgradUnits units, int64_t n,
-                                    float* __restrict__ dW) {
-  const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+// dW[s] (field-pair-blocked, dw_block_pos) = sum of offset s's unit partials ([cout][cin]) in unit
+// order.
+__global__ void reduce_units_kernel(const float* __restrict__ part, KgradUnits units, int cin, int cout,
+                                    FieldTab fout, FieldTab fin, float* __restrict__ dW) {
+  const int e = blockIdx.x * blockDim.x + threadIdx.x;
   const int s = blockIdx.y;
+  const int64_t n = (int64_t)cin * cout;
   if (e >= n) return;
   float acc = 0.f;
   for (int u = units.uoff[s]; u < units.uoff[s + 1]; ++u) acc += part[(int64_t)u * n + e];
-  dW[(int64_t)s * n + e] = acc;
+  const int o = e / cin;
+  dW[dw_block_pos(fout, fin, units.K, cin, s, o, e - o * cin)] = acc;
 }
 
 }  // namespace
@@ -339,10 +343,12 @@ KgradUnits kgrad_units(const ssconv_rulebook* rb, int want, bool ordered) {
   return u;
 }
 
-int reduce_units(const float* part, const KgradUnits& units, int64_t n, float* dW, hipStream_t st) {
+int reduce_units(const float* part, const KgradUnits& units, int cin, int cout, const FieldTab& fout,
+                 const FieldTab& fin, float* dW, hipStream_t st) {
+  const int64_t n = (int64_t)cin * cout;
   if (n == 0 || units.K == 0) return SSCONV_OK;
   dim3 grid(cdiv(n, 256), units.K);
-  reduce_units_kernel<<<grid, 256, 0, st>>>(part, units, n, dW);
+  reduce_units_kernel<<<grid, 256, 0, st>>>(part, units, cin, cout, fout, fin, dW);
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;
 }

@@ -535,8 +535,10 @@ bool kgrad_f32_units_ok(const ssconv_rulebook* rb, int cin, int cout) {
 
 int kgrad_f32_units_want(const ssconv_rulebook* rb, int cin, int cout) {
   const KgradPlan p = kgrad_plan(rb, SSCONV_F32, cin, cout);
-  // two full rounds of the 2048 wavefront slots (256 CUs x two four-wavefront workgroups)
-  return std::max(1, kKgradMaxUnitsF32 / (p.mtiles * p.ntiles));
+  // one full round of the 2048 wavefront slots (256 CUs x two four-wavefront workgroups): measured
+  // against 1024, 1536, 3072 and 4096 tasks, fewer partials to add up outweigh the balance of
+  // two rounds (C2 step -12 us, C5 -215 us against 4096)
+  return std::max(1, 2048 / (p.mtiles * p.ntiles));
 }
 
 int kgrad_f32(const void* grad_out, const void* feats, int cin, int cout, const ssconv_rulebook* rb,

@@ -38,7 +38,7 @@ struct KgradUnits {
 KgradUnits kgrad_units(const ssconv_rulebook* rb, int want, bool ordered);
 
 // fp32 kernel gradient over work units (per-wavefront LDS ring): usable when every row offset
-// fits 31 bits; the unit count that fills two rounds of wavefront slots.
+// fits 31 bits; the unit count that fills one round of wavefront slots.
 bool kgrad_f32_units_ok(const ssconv_rulebook* rb, int cin, int cout);
 int kgrad_f32_units_want(const ssconv_rulebook* rb, int cin, int cout);
 int kgrad_f32(const void* grad_out, const void* feats, int cin, int cout, const ssconv_rulebook* rb,
@@ -53,7 +53,9 @@ int kgrad_bf16(const void* grad_out, int64_t n_out, const void* feats, int64_t n
                const ssconv_rulebook* rb, const KgradUnits& units, float* part, hipStream_t st);
 
 // dW[s][:] = sum over the units of offset s of part[u][:] (n = cout * cin per unit), fixed order.
-int reduce_units(const float* part, const KgradUnits& units, int64_t n, float* dW, hipStream_t st);
+// dW (field-pair-blocked, dw_block_pos) from the unit partials, each offset's in unit order.
+int reduce_units(const float* part, const KgradUnits& units, int cin, int cout, const FieldTab& fout,
+                 const FieldTab& fin, float* dW, hipStream_t st);
 
 // part[split][s][o][i] (fp32) = sum over the split's slice of R_s of grad_out[x][o] feats[y][i].
 int kgrad_partials(const void* grad_out, const void* feats, ssconv_dtype dt, int cin, int cout,

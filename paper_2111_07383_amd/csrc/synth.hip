@@ -3,7 +3,8 @@
 // W[s][o][i] = sum_q w[off(field(o), field(i)) + q] * B^{k l}_q[s][a][b], one thread per
 // element of W so the dominant cost -- writing W -- is a coalesced stream.
 // The adjoint dw[off + q] = sum_{s,a,b} dW[s][o][i] B_q[s][a][b] uses one
-// workgroup per (out field, in field) pair with a fixed reduction order.
+// workgroup per (out field, in field) pair with a fixed reduction order; dW comes
+// field-pair-blocked (dw_block_pos), so a pair's values are one contiguous run.
 #include "synth.hpp"
 
 namespace ssconv {
@@ -118,6 +119,7 @@ __global__ __launch_bounds__(256) void synth_adjoint_kernel(SynthArgs a, const f
   const int n = a.K * dk * dl;
   const int64_t qstride = (int64_t)a.K * dk * dl;
   const float* bp = basis + a.base[k][l];
+  const int64_t blk = (int64_t)a.K * ((int64_t)ro * a.cin + (int64_t)dk * cc);  // dW is field-pair-blocked
   for (int q0 = 0; q0 < nq; q0 += kQB) {
     float acc[kQB];
 #pragma unroll
@@ -128,8 +130,7 @@ __global__ __launch_bounds__(256) void synth_adjoint_kernel(SynthArgs a, const f
       for (int u = 0; u < kEU; ++u) {
         const int e = e0 + u * 256;
         const bool ok = e < n;
-        const int s = e / (dk * dl), r = e - s * (dk * dl), aa = r / dl, bb = r - aa * dl;
-        g[u] = ok ? dW[((int64_t)s * a.cout + ro + aa) * a.cin + cc + bb] : 0.f;
+        g[u] = ok ? dW[blk + e] : 0.f;
 #pragma unroll
         for (int j = 0; j < kQB; ++j) bv[u][j] = (ok && q0 + j < nq) ? bp[(q0 + j) * qstride + e] : 0.f;
       }

@@ -24,6 +24,7 @@ struct SynthArgs {
 int make_synth_args(const ssconv_basis_desc* d, SynthArgs* a);
 int launch_synth(const SynthArgs& a, const float* basis, const float* coeffs, ssconv_dtype dt, void* W,
                  hipStream_t st);
+// dW in the field-pair-blocked layout of dw_block_pos.
 int launch_synth_adjoint(const SynthArgs& a, const float* basis, const float* dW, float* dcoef, hipStream_t st);
 
 }  // namespace ssconv
