@@ -155,6 +155,61 @@ __global__ __launch_bounds__(256) void synth_adjoint_kernel(SynthArgs a, const f
   }
 }
 
+// The same sums with one wavefront per (out field, in field) pair, four pairs per workgroup, for
+// small offset counts (a pair's K*(2k+1)*(2l+1) values are then at most a few hundred): four times
+// as many pairs in flight per compute unit and no workgroup barrier.  Lane partial sums in element
+// order, then the fixed butterfly.
+__global__ __launch_bounds__(256) void synth_adjoint_wave_kernel(SynthArgs a, const float* __restrict__ basis,
+                                                                 const float* __restrict__ dW,
+                                                                 float* __restrict__ dcoef) {
+  const int lane = threadIdx.x & 63;
+  const int pair = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (pair >= a.n_in_fields * a.n_out_fields) return;  // uniform per wavefront
+  const int fi_all = pair % a.n_in_fields, fo_all = pair / a.n_in_fields;
+  int eo = 0, ei = 0;
+  while (eo + 1 < a.out.n && fo_all >= a.out.f0[eo + 1]) ++eo;
+  while (ei + 1 < a.in.n && fi_all >= a.in.f0[ei + 1]) ++ei;
+  const int fo = fo_all - a.out.f0[eo], fi = fi_all - a.in.f0[ei];
+  const int k = a.out.l[eo], l = a.in.l[ei], dk = 2 * k + 1, dl = 2 * l + 1;
+  const int nq = a.nq[k][l];
+  if (nq == 0) return;
+  const int ro = a.out.ch0[eo] + fo * dk, cc = a.in.ch0[ei] + fi * dl;
+  const int64_t off = coeff_off(a, eo, fo, k, ei, fi);
+  const int n = a.K * dk * dl;
+  const int64_t qstride = (int64_t)a.K * dk * dl;
+  const float* bp = basis + a.base[k][l];
+  const int64_t blk = (int64_t)a.K * ((int64_t)ro * a.cin + (int64_t)dk * cc);
+  for (int q0 = 0; q0 < nq; q0 += kQB) {
+    float acc[kQB];
+#pragma unroll
+    for (int j = 0; j < kQB; ++j) acc[j] = 0.f;
+    for (int e0 = lane; e0 < n; e0 += 64 * kEU) {
+      float g[kEU], bv[kEU][kQB];
+#pragma unroll
+      for (int u = 0; u < kEU; ++u) {
+        const int e = e0 + u * 64;
+        const bool ok = e < n;
+        g[u] = ok ? dW[blk + e] : 0.f;
+#pragma unroll
+        for (int j = 0; j < kQB; ++j) bv[u][j] = (ok && q0 + j < nq) ? bp[(q0 + j) * qstride + e] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kEU; ++u)
+#pragma unroll
+        for (int j = 0; j < kQB; ++j) acc[j] = fmaf(g[u], bv[u][j], acc[j]);
+    }
+    float mine = 0.f;  // lane j keeps coefficient j's sum
+#pragma unroll
+    for (int j = 0; j < kQB; ++j) {
+      float v = acc[j];
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+      if (lane == j) mine = v;
+    }
+    if (lane < kQB && q0 + lane < nq) dcoef[off + q0 + lane] = mine;
+  }
+}
+
 }  // namespace
 
 int launch_synth(const SynthArgs& a, const float* basis, const float* coeffs, ssconv_dtype dt, void* W,
@@ -173,8 +228,13 @@ int launch_synth(const SynthArgs& a, const float* basis, const float* coeffs, ss
 
 int launch_synth_adjoint(const SynthArgs& a, const float* basis, const float* dW, float* dcoef, hipStream_t st) {
   if (a.n_coeff == 0) return SSCONV_OK;
-  dim3 g(a.n_in_fields, a.n_out_fields);
-  synth_adjoint_kernel<<<g, 256, 0, st>>>(a, basis, dW, dcoef);
+  if (a.K <= 27) {
+    const int64_t pairs = (int64_t)a.n_in_fields * a.n_out_fields;
+    synth_adjoint_wave_kernel<<<(unsigned)cdiv(pairs, 4), 256, 0, st>>>(a, basis, dW, dcoef);
+  } else {
+    dim3 g(a.n_in_fields, a.n_out_fields);
+    synth_adjoint_kernel<<<g, 256, 0, st>>>(a, basis, dW, dcoef);
+  }
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;
 }
