@@ -11,6 +11,8 @@ Modules
     rulebook  output site sets and rule books (Sec. 3.2.2, Eq. 10; Sec. 3.2.3, Alg. 1)
     conv      kernel synthesis, sparse convolution forward/backward, dense
               reference convolution, gated nonlinearity (Alg. 1; Sec. 3.3, Eq. 12)
+    norm_pool steerable normalisation (Sec. 3.3, Eq. 11) and 2x2x2 / stride-2
+              sparse average pooling (footnote of Sec. 3.1), forward and backward
 
 Readings of the paper that it takes (all pinned by invariants in tests/):
     real SH without Condon-Shortley phase, components ordered m = -l..l;
@@ -19,7 +21,9 @@ Readings of the paper that it takes (all pinned by invariants in tests/):
     with the first significant entry positive;
     stride-2 pairing 2x - y = s (a zero-padded strided convolution);
     generated output sets in lexicographic (b, x, y, z) order;
-    gate = extra scalar output channel of the same convolution.
+    gate = extra scalar output channel of the same convolution;
+    Norm: eps = 1e-5, population statistics over every active site, no affine;
+    pooling divides window sums by 8 (zero-filled dense semantics).
 
 Parity status: every function here is pinned by at least one invariant test
 (brute force, dense convolution, exact equivariance, adjointness, closed
