@@ -11,7 +11,7 @@ Prints ONE JSON line: throughput in M active output sites/s, the roofline of
 the dominant kernel (timed with events on the stream it runs on) and the CPU
 oracle timed on a bounded sample on this host.
 
-    python bench.py [--steps K] [--warmup W] [--config {1..5}] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--config {1..6}] [--no-cpu-baseline]
 """
 import argparse
 import json
@@ -149,7 +149,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload index 1..5 (default: the 64^3 5x5x5 layer)")
+    ap.add_argument("--config", type=int, default=2, help="workload index 1..6 (default: the 64^3 5x5x5 layer; 6: the "
+                    "downsampling block conv + norm + gate + pooling)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work to aim for")
     ap.add_argument("--only", choices=["step", "forward"], default="step",
@@ -329,6 +330,122 @@ class StackBench:
                 "step": "5 x (rulebook+synth+forward+gate) + backward"}
 
 
+class BlockBench:
+    """The paper's downsampling block (workload 6): stride-1 submanifold SS-Conv -> Norm -> gate
+    -> 2x2x2 average pooling, forward and backward (feature and coefficient gradients).  The
+    same calls, in the same order, as ``stack.DownBlock``, with an event between every two."""
+    NAMES = ["synth", "rulebook", "conv_forward", "norm_forward", "gate_forward", "pool_rulebook",
+             "pool_forward", "pool_backward", "gate_backward", "norm_backward", "conv_backward"]
+
+    def __init__(self, i, dev):
+        import torch
+        import paper_2111_07383_amd as P
+        from paper_2111_07383_amd.stack import regular_fields
+        from workloads import CONFIGS
+        from workloads.gen import make_coeffs, make_coords, make_features, make_grad
+        self.P, self.torch = P, torch
+        spec = CONFIGS[i]
+        self.spec, self.L = spec, spec.layers[0]
+        self.regular = regular_fields(self.L)
+        self.desc = P.layer_desc(self.L)
+        self.basis = torch.from_numpy(P.basis_build(self.desc)).to(dev)
+        self.n_coeff = P.basis_info(self.desc)[1]
+        coords = make_coords(spec)
+        self.coords = torch.from_numpy(coords).to(dev)
+        self.feats = torch.from_numpy(make_features(spec, len(coords), self.L.cin)).to(dev)
+        self.coeffs = torch.from_numpy(make_coeffs(spec, [self.n_coeff])[0]).to(dev)
+        rb = P.Rulebook(self.coords, spec.grid, self.L.ksize, 1, True)
+        self.n_pairs = rb.n_pairs
+        self.ws = torch.empty((P.backward_workspace_size(rb, torch.float32, self.L.cin, self.L.cout),),
+                              dtype=torch.uint8, device=dev)
+        rb.close()
+        prb = P.Rulebook(self.coords, spec.grid, 2, 2, False)
+        self.n_out = prb.n_out
+        prb.close()
+        self.grad = torch.from_numpy(make_grad(spec, self.n_out, P.n_channels(self.regular))).to(dev)
+        self.events = None
+
+    def step(self):
+        P, L, torch = self.P, self.L, self.torch
+        ev = None
+        if self.events is not None:
+            ev = [torch.cuda.Event(enable_timing=True) for _ in range(len(self.NAMES) + 1)]
+            self.events.append(ev)
+            ev[0].record()
+        marks = iter(ev[1:] if ev else [])
+
+        def mark():
+            if ev:
+                next(marks).record()
+        W = P.synth_kernel(self.desc, self.basis, self.coeffs, torch.float32)
+        mark()
+        rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, 1, True)
+        mark()
+        y = P.forward(self.feats, rb, W)
+        mark()
+        z = P.norm_forward(L.fields_out, y)
+        mark()
+        h = P.gate_forward(self.regular, z)
+        mark()
+        prb = P.Rulebook(self.coords, self.spec.grid, 2, 2, False)
+        mark()
+        out = P.pool_forward(h, prb)
+        mark()
+        g = P.pool_backward(self.grad, prb)
+        mark()
+        g = P.gate_backward(self.regular, z, g)
+        mark()
+        g = P.norm_backward(L.fields_out, y, g)
+        mark()
+        P.backward(self.feats, g, rb, W, self.desc, self.basis, n_coeff=self.n_coeff, workspace=self.ws)
+        mark()
+        rb.close()
+        prb.close()
+        return out
+
+    def phase_report(self):
+        """Per-phase medians against HBM (norm, gate, pooling: algorithmic bytes = one read of each
+        operand and one write of each result) or MFMA (the convolution GEMMs) roofline times."""
+        if not self.events:
+            return None
+        L = self.L
+        t = np.array([[a.elapsed_time(b) for a, b in zip(ev, ev[1:])] for ev in self.events])
+        med = np.median(t, 0)
+        n_in, n_out, P_ = int(self.coords.shape[0]), int(self.n_out), int(self.n_pairs)
+        C, Cg, Cin = L.cout, self.P.n_channels(self.regular), L.cin
+        hbm, peak = HBM_PEAK_GBS * 1e9, PEAK["f32"] * 1e12
+        flops = 2.0 * P_ * Cin * C
+        roof = {"norm_forward": 2 * n_in * C * 4 / hbm, "gate_forward": (n_in * C + n_in * Cg) * 4 / hbm,
+                "pool_forward": ((n_in + n_out) * Cg * 4 + 32 * n_out) / hbm,
+                "pool_backward": ((n_in + n_out) * Cg * 4 + 32 * n_out) / hbm,
+                "gate_backward": (2 * n_in * C + n_in * Cg) * 4 / hbm, "norm_backward": 3 * n_in * C * 4 / hbm,
+                "conv_forward": flops / peak, "conv_backward": 2 * flops / peak}
+        out = {}
+        for n, m in zip(self.NAMES, med):
+            out[n] = {"ms": float(m)}
+            if n in roof:
+                out[n]["roofline_ms"] = roof[n] * 1e3
+                out[n]["frac"] = roof[n] * 1e3 / float(m)
+        step = t.sum(1)
+        out["step_ms"] = {"p10": float(np.percentile(step, 10)), "median": float(np.median(step)),
+                          "p90": float(np.percentile(step, 90))}
+        return out
+
+    def sites(self):
+        return self.n_out
+
+    def gather_flops(self, forward_only):
+        f = 2.0 * self.n_pairs * self.L.cin * self.L.cout
+        return 2 * f, 2
+
+    def config(self):
+        L = self.L
+        return {"workload": self.spec.name, "grid": self.spec.grid, "batch": self.spec.batch, "ksize": L.ksize,
+                "cin": L.cin, "cout": L.cout, "n_in": int(self.coords.shape[0]), "n_out": int(self.n_out),
+                "pairs": int(self.n_pairs),
+                "step": "synth+rulebook+conv+norm+gate+pool rulebook+pool, then pool+gate+norm+conv backward"}
+
+
 # ---------------------------------------------------------------------------
 # CPU oracle baseline (bounded sample of the same workload)
 # ---------------------------------------------------------------------------
@@ -369,6 +486,51 @@ def cpu_baseline(i, budget_s):
                       f"synth + forward + backward (fp64 numpy), {t:.1f} s"}
 
 
+def cpu_baseline_block(i):
+    """The whole block on the oracle (Norm needs every row's statistics, so no row sample)."""
+    from threadpoolctl import threadpool_info
+    from oracle import conv as oc
+    from oracle import norm_pool as onp
+    from oracle import rulebook as orb
+    from workloads import CONFIGS
+    from workloads.gen import make_coeffs, make_coords, make_features, make_grad
+    spec = CONFIGS[i]
+    L = spec.layers[0]
+    coords = make_coords(spec)
+    lay = oc.Layer(L)
+    w = make_coeffs(spec, [lay.n_coeff])[0]
+    f = make_features(spec, len(coords), L.cin)
+    regular = L.fields_out[:-1]
+    t0 = time.perf_counter()
+    R = orb.rulebook(coords, coords, L.ksize, 1)
+    kap = lay.kappa(w)
+    y = oc.forward(f, R, kap, len(coords))
+    z = onp.norm_forward(y, L.fields_out)
+    h = oc.gate_forward(z, regular)
+    pc = onp.pool_sites(coords)
+    member = onp.pool_members(coords, pc)
+    onp.pool_forward(h, member, len(pc))
+    g = make_grad(spec, len(pc), h.shape[1])
+    g = oc.gate_backward(z, onp.pool_backward(g, member), regular)
+    g = onp.norm_backward(y, g, L.fields_out)
+    oc.grad_feats(g, R, kap, len(coords))
+    oc.synth_adjoint(L, lay.basis, oc.grad_kappa(f, g, R, kap.shape))
+    t = time.perf_counter() - t0
+    threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
+    return {"value": len(pc) / t / 1e6, "unit": "M active output sites/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{spec.name}: the whole block, {len(pc)} pooled sites; rule books (dict, 1 thread) + synth + "
+                      f"conv + norm + gate + pool, forward and backward (fp64 numpy), {t:.1f} s"}
+
+
+def step_text(spec):
+    if spec.index == 6:
+        return ("synthesis + rule book + conv + norm + gate + pooling rule book + pooling, then pooling, gate, norm "
+                "and conv backward")
+    if spec.index == 5:
+        return "per layer synthesis + rule book + forward (+ gate), then the backward of every layer"
+    return "synthesis + rule book + forward + backward"
+
+
 def write_stats_summary(args):
     """Tabulates a rocprofv3 --kernel-trace --stats run of this benchmark (directory
     args.stats_summary, with the benchmark's own JSON line in args.stats_log) into
@@ -393,8 +555,7 @@ def write_stats_summary(args):
 
     steps, warmup = (bench["steps"], bench["warmup"]) if bench else (args.steps, args.warmup)
     run = f"python3 bench.py --config {spec.index} --steps {steps} --warmup {warmup} --no-cpu-baseline"
-    out = [f"# rocprofv3 kernel statistics: {spec.name} ({spec.dtype}), one step = rule book + synthesis + "
-           "forward + backward",
+    out = [f"# rocprofv3 kernel statistics: {spec.name} ({spec.dtype}), one step = {step_text(spec)}",
            f"command: rocprofv3 --kernel-trace --stats --output-format csv -d {d} -o p -- {run} > {args.stats_log}",
            f"summary: python3 bench.py --config {spec.index} --stats-summary {d} --stats-log {args.stats_log}", "",
            f"{'kernel':70s} {'calls':>6s} {'avg_us':>9s} {'min_us':>9s} {'max_us':>9s} {'pct':>6s}"]
@@ -458,8 +619,7 @@ def write_counter_summary(args):
     cw = _per_dispatch(_counter_rows(os.path.join(dc, "copy_write")), COPY_KERNEL, "WRITE_SIZE")
     ff, fw = mb * 1024.0 / float(np.mean(cf)), mb * 1024.0 / float(np.mean(cw))
     run = f"python3 bench.py --config {spec.index} --steps 3 --warmup 1 --no-cpu-baseline"
-    lines = [f"# rocprofv3 counters per kernel: {spec.name} ({spec.dtype}), one step = rule book + synthesis + "
-             "forward + backward",
+    lines = [f"# rocprofv3 counters per kernel: {spec.name} ({spec.dtype}), one step = {step_text(spec)}",
              "commands (from the repository root, TMPDIR=/tmp, each under timeout -s KILL 120):",
              f"  rocprofv3 --pmc FETCH_SIZE --output-format csv -d {d}/fetch -o p -- {run}",
              f"  rocprofv3 --pmc WRITE_SIZE --output-format csv -d {d}/write -o p -- {run}",
@@ -526,9 +686,10 @@ def main():
         import paper_2111_07383_amd as P
         P.debug_set(3, args.variant)
     log(f"setting up {spec.name}")
-    b = StackBench(dev) if args.config == 5 else SingleLayer(args.config, dev)
-    if args.only == "forward" and args.config == 5:
+    if args.only == "forward" and args.config in (5, 6):
         raise SystemExit("--only forward applies to the single-layer workloads 1-4")
+    b = (StackBench(dev) if args.config == 5 else BlockBench(args.config, dev) if args.config == 6
+         else SingleLayer(args.config, dev))
     run = b.forward_only if args.only == "forward" else b.step
     for _ in range(args.warmup):
         run()
@@ -536,7 +697,7 @@ def main():
     log(f"warmup done ({args.warmup} steps); timing {args.steps} steps")
     import paper_2111_07383_amd as P
     P.debug_set(4, 1)                 # HIP events around each gather-GEMM launch, on its stream
-    if args.only == "step" and isinstance(b, SingleLayer):
+    if args.only == "step" and isinstance(b, (SingleLayer, BlockBench)):
         b.events = []                 # phase boundaries of every timed step (torch's stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -569,14 +730,15 @@ def main():
                        "launches_timed": n_timed, "algorithmic_flops_per_launch": flops_launch,
                        "kernel_ms_per_step": kern_ms / args.steps}
     log(f"gather-GEMM: {n_timed} launches, {avg_ms:.4f} ms avg, {achieved:.1f} TFLOP/s")
-    if isinstance(b, SingleLayer) and b.events:
+    if isinstance(b, (SingleLayer, BlockBench)) and b.events:
         out["phases"] = b.phase_report()
         ph = out["phases"]
         log("phases (median ms / roofline fraction): " +
-            ", ".join(f"{k} {ph[k]['ms']:.3f}/{ph[k]['frac']:.2f}" for k in ("rulebook", "synth", "forward", "backward", "layer")))
+            ", ".join(f"{k} {v['ms']:.3f}/{v.get('frac', float('nan')):.2f}" for k, v in ph.items() if "ms" in v))
     if not args.no_cpu_baseline and args.config != 5:
         log("timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = cpu_baseline(args.config, args.cpu_budget)
+        out["cpu_baseline"] = (cpu_baseline_block(args.config) if args.config == 6
+                               else cpu_baseline(args.config, args.cpu_budget))
     print(json.dumps(out), flush=True)
 
 

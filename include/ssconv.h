@@ -27,8 +27,9 @@
  *    outputs and to report device-detected errors.
  *  - Sites are int32 (b, x, y, z) with 0 <= x < grid[0], 0 <= y < grid[1],
  *    0 <= z < grid[2], b >= 0 and (max b + 1) * grid[0]*grid[1]*grid[2] < 2^32.
- *  - Kernel offsets s = (dx, dy, dz) in S = {-h..h}^3, h = (ksize-1)/2, are
- *    indexed s_idx = ((dx+h)*ksize + (dy+h))*ksize + (dz+h)   (Sec. 3.2, Eq. 6).
+ *  - Kernel offsets s = (dx, dy, dz) in S = {-h..ksize-1-h}^3, h = ksize/2
+ *    ({-h..h}^3 for the odd convolution kernels), are indexed
+ *    s_idx = ((dx+h)*ksize + (dy+h))*ksize + (dz+h)   (Sec. 3.2, Eq. 6).
  *  - Channel layout (Sec. 3.1, Eq. 5): a feature row stacks irreducible fields
  *    in the order of an ssconv_fields list; the fields of one entry are
  *    consecutive and each field's 2l+1 components are contiguous, ordered
@@ -127,7 +128,8 @@ int ssconv_basis_build(const ssconv_basis_desc* desc /*host*/, float* basis /*ho
 
 /* ---- rule book (Sec. 3.2.2, Eq. 10; Sec. 3.2.3, rule book of Alg. 1) -----
  * coords: [n, 4] int32 (b, x, y, z), n >= 0, no duplicates.
- * grid (host): input grid extent per axis.  ksize: odd, 1..5.
+ * grid (host): input grid extent per axis.  ksize: odd, 1..5, or 2 with
+ * stride 2 (the 2x2x2 pooling windows of ssconv_pool_*, offsets {-1, 0}^3).
  * stride: 1 or 2.  submanifold = 1 keeps H_{n+1} = H_n (stride must be 1, rows
  * unchanged); otherwise H_{n+1} = { x : exists y in H_n, stride*x - y in S }
  * clipped to the output grid ceil(grid/stride), rows in lexicographic
@@ -171,7 +173,7 @@ int ssconv_synth_kernel(const ssconv_basis_desc* desc /*host*/, const float* bas
  * exactly once (rows with no pair become 0).  feats [n_in, cin], W
  * [ksize^3, cout, cin], out [n_out, cout], all in `dtype` (bf16 inputs are
  * multiplied exactly and accumulated in fp32).  Buffers must be 16-byte
- * aligned.  feats and out must not overlap. */
+ * aligned.  feats and out must not overlap.  rb must have an odd ksize. */
 int ssconv_forward(const void* feats, ssconv_dtype dtype, int cin, ssconv_rulebook_t rb,
                    const void* W, int cout, void* out, hipStream_t stream);
 
@@ -199,6 +201,39 @@ int ssconv_gate_forward(const ssconv_fields* fields /*host*/, const void* x, ssc
                         int64_t n, void* y, hipStream_t stream);
 int ssconv_gate_backward(const ssconv_fields* fields /*host*/, const void* x, const void* dy,
                          ssconv_dtype dtype, int64_t n, void* dx, hipStream_t stream);
+
+/* ---- steerable normalisation (Sec. 3.3, Eq. 11) ------------------------------
+ * x, y: [n, C] in `dtype`, C = channels of `fields` (1..1024).  Every field is
+ * normalised on its own with population statistics over all n rows:
+ *   l = 0:  y = (f - mean) / sqrt(var + eps)            (var: biased)
+ *   l > 0:  y = f / sqrt(mean over rows of |f|^2 + eps)
+ * No affine parameters.  Statistics are accumulated in fp64 in a fixed order
+ * (deterministic); the elementwise step runs in fp32.  Backward: dx [n, C] =
+ * the exact gradient of <y, dy> with respect to x (through the statistics).
+ * y may alias x, and dx may alias x or dy, element for element.  n = 0 is a
+ * no-op.  Temporary sums come from the library's device memory cache.
+ * Errors: E_DTYPE, E_INVALID (fields, eps <= 0, null buffers), E_NOMEM, E_HIP. */
+int ssconv_norm_forward(const ssconv_fields* fields /*host*/, const void* x, ssconv_dtype dtype, int64_t n,
+                        double eps, void* y, hipStream_t stream);
+int ssconv_norm_backward(const ssconv_fields* fields /*host*/, const void* x, const void* dy, ssconv_dtype dtype,
+                         int64_t n, double eps, void* dx, hipStream_t stream);
+
+/* ---- sparse average pooling (Sec. 3.1, footnote: downsampling is a stride-1
+ * convolution followed by average pooling) -----------------------------------
+ * rb must be built with ksize = 2, stride = 2, submanifold = 0: its offsets
+ * are {-1, 0}^3 under 2x - y = s, so output x is active when an input lies in
+ * the window 2x + {0,1}^3 (outputs = the distinct floor(y/2), lexicographic),
+ * and nbr[s][x] lists the window's members.
+ * Forward: out[x] = (sum of the window's active rows of feats) / 8, the dense
+ * 2x2x2 average of the zero-filled grid at active outputs.  feats [n_in, C],
+ * out [n_out, C].  Backward: grad_feats[y] = grad_out[x(y)] / 8 (every input
+ * lies in exactly one window).  Sums in fp32, one rounding to bf16.
+ * Errors: E_DTYPE, E_INVALID (not a pooling rule book, C < 1, null buffers),
+ * E_HIP. */
+int ssconv_pool_forward(const void* feats, ssconv_dtype dtype, int channels, ssconv_rulebook_t rb, void* out,
+                        hipStream_t stream);
+int ssconv_pool_backward(const void* grad_out, ssconv_dtype dtype, int channels, ssconv_rulebook_t rb,
+                         void* grad_feats, hipStream_t stream);
 
 /* ---- test hooks --------------------------------------------------------
  * Forces failure paths from the host so they can be tested without faulting

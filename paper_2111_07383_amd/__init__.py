@@ -22,5 +22,9 @@ from .binding import (  # noqa: F401
     layer_desc,
     make_fields,
     n_channels,
+    norm_backward,
+    norm_forward,
+    pool_backward,
+    pool_forward,
     synth_kernel,
 )

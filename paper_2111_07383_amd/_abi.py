@@ -50,6 +50,11 @@ SIGNATURES = {
                                 c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),
     "ssconv_gate_forward": (c_int, [POINTER(Fields), c_void_p, c_int, c_int64, c_void_p, c_void_p]),
     "ssconv_gate_backward": (c_int, [POINTER(Fields), c_void_p, c_void_p, c_int, c_int64, c_void_p, c_void_p]),
+    "ssconv_norm_forward": (c_int, [POINTER(Fields), c_void_p, c_int, c_int64, c_double, c_void_p, c_void_p]),
+    "ssconv_norm_backward": (c_int, [POINTER(Fields), c_void_p, c_void_p, c_int, c_int64, c_double, c_void_p,
+                                     c_void_p]),
+    "ssconv_pool_forward": (c_int, [c_void_p, c_int, c_int, c_void_p, c_void_p, c_void_p]),
+    "ssconv_pool_backward": (c_int, [c_void_p, c_int, c_int, c_void_p, c_void_p, c_void_p]),
     "ssconv_debug_set": (c_int, [c_int, c_int64]),
     "ssconv_debug_kernel_ms": (c_int, [POINTER(c_int64), POINTER(c_float)]),
 }

@@ -245,6 +245,62 @@ def gate_backward(fields: FieldList, x: torch.Tensor, dy: torch.Tensor, stream=N
     return dx
 
 
+NORM_EPS = 1e-5
+
+
+def norm_forward(fields: FieldList, x: torch.Tensor, eps: float = NORM_EPS, out: Optional[torch.Tensor] = None,
+                 stream=None) -> torch.Tensor:
+    """Steerable normalisation (Eq. 11) of x [n, C] with statistics over all rows."""
+    _need(x, "x")
+    f = make_fields(fields)
+    if x.dim() != 2 or x.shape[1] != n_channels(fields):
+        raise ValueError(f"x must be [n, {n_channels(fields)}]")
+    if out is None:
+        out = torch.empty_like(x)
+    _need(out, "out", x.dtype, tuple(x.shape))
+    check(lib().ssconv_norm_forward(byref(f), _ptr(x), _dtype(x), x.shape[0], float(eps), _ptr(out),
+                                    _stream(stream)), "ssconv_norm_forward")
+    return out
+
+
+def norm_backward(fields: FieldList, x: torch.Tensor, dy: torch.Tensor, eps: float = NORM_EPS,
+                  stream=None) -> torch.Tensor:
+    _need(x, "x")
+    _need(dy, "dy", x.dtype, tuple(x.shape))
+    if x.dim() != 2 or x.shape[1] != n_channels(fields):
+        raise ValueError(f"x must be [n, {n_channels(fields)}]")
+    f = make_fields(fields)
+    dx = torch.empty_like(x)
+    check(lib().ssconv_norm_backward(byref(f), _ptr(x), _ptr(dy), _dtype(x), x.shape[0], float(eps), _ptr(dx),
+                                     _stream(stream)), "ssconv_norm_backward")
+    return dx
+
+
+def pool_forward(feats: torch.Tensor, rb: Rulebook, out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """2x2x2 average pooling over a rule book built with ksize 2, stride 2."""
+    _need(feats, "feats")
+    if feats.dim() != 2 or feats.shape[0] != rb.n_in:
+        raise ValueError(f"feats must be [{rb.n_in}, C]")
+    C = feats.shape[1]
+    if out is None:
+        out = torch.empty((rb.n_out, C), dtype=feats.dtype, device=feats.device)
+    _need(out, "out", feats.dtype, (rb.n_out, C))
+    check(lib().ssconv_pool_forward(_ptr(feats), _dtype(feats), C, rb.handle, _ptr(out), _stream(stream)),
+          "ssconv_pool_forward")
+    return out
+
+
+def pool_backward(grad_out: torch.Tensor, rb: Rulebook, stream=None) -> torch.Tensor:
+    _need(grad_out, "grad_out")
+    if grad_out.dim() != 2 or grad_out.shape[0] != rb.n_out:
+        raise ValueError(f"grad_out must be [{rb.n_out}, C]")
+    C = grad_out.shape[1]
+    gf = torch.empty((rb.n_in, C), dtype=grad_out.dtype, device=grad_out.device)
+    check(lib().ssconv_pool_backward(_ptr(grad_out), _dtype(grad_out), C, rb.handle, _ptr(gf), _stream(stream)),
+          "ssconv_pool_backward")
+    return gf
+
+
 def debug_set(option: int, value: int) -> None:
     check(lib().ssconv_debug_set(int(option), int(value)), "ssconv_debug_set")
 

@@ -12,6 +12,7 @@ int check_conv_args(const void* a, const void* b, ssconv_dtype dt, int cin, int 
                     const void* W) {
   if (dt != SSCONV_F32 && dt != SSCONV_BF16) return fail(SSCONV_E_DTYPE, "unsupported dtype %d", (int)dt);
   if (!rb) return fail(SSCONV_E_INVALID, "NULL rule book");
+  if ((rb->ksize & 1) == 0) return fail(SSCONV_E_INVALID, "a ksize-2 rule book holds pooling windows (ssconv_pool_*)");
   if (cin < 1 || cout < 1) return fail(SSCONV_E_INVALID, "channel counts must be positive");
   if (!W) return fail(SSCONV_E_INVALID, "NULL kernel tensor");
   if (!aligned16(W) || (a && !aligned16(a)) || (b && !aligned16(b)))

@@ -109,13 +109,15 @@ __global__ void hash_insert_kernel(const int32_t* __restrict__ c, int64_t n, int
   atomicOr(flags, kFlagFull);
 }
 
-// Output-set marking: for input y and offset s, stride*x = y + s must divide exactly.
+// Output-set marking: for input y and offset s, stride*x = y + s must divide exactly.  Offsets run
+// over {-h .. ksize-1-h}^3 with h = ksize/2: {-h..h}^3 for odd kernels, {-1, 0}^3 for the 2x2x2
+// pooling windows (y = 2x + {0,1}^3).
 __global__ void mark_outputs(const int32_t* __restrict__ c, int64_t n, int ksize, int stride, int go0, int go1,
                              int go2, uint32_t* __restrict__ bits) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int s = blockIdx.y;
   if (i >= n) return;
-  int h = (ksize - 1) / 2;
+  int h = ksize / 2;
   int dx = s / (ksize * ksize) - h, dy = (s / ksize) % ksize - h, dz = s % ksize - h;
   int4 v = reinterpret_cast<const int4*>(c)[i];
   int tx = v.y + dx, ty = v.z + dy, tz = v.w + dz;
@@ -166,7 +168,7 @@ __global__ __launch_bounds__(256) void probe_kernel(const int32_t* __restrict__ 
   int nb = -1;
   if (kCount) {
     if (p < n_out) {
-      int h = (ksize - 1) / 2;
+      int h = ksize / 2;
       int dx = s / (ksize * ksize) - h, dy = (s / ksize) % ksize - h, dz = s % ksize - h;
       int4 v = reinterpret_cast<const int4*>(out_c)[p];
       int yx = stride * v.y - dx, yy = stride * v.z - dy, yz = stride * v.w - dz;
@@ -463,9 +465,13 @@ extern "C" int ssconv_build_rulebook(const int32_t* coords, int64_t n, const int
   if (n < 0 || (n > 0 && !coords)) return fail(SSCONV_E_INVALID, "bad coords/n");
   if (n > 0x7fffffffll) return fail(SSCONV_E_INVALID, "at most 2^31-1 sites");
   if (n > 0 && !aligned16(coords)) return fail(SSCONV_E_INVALID, "coords must be 16-byte aligned");
-  if (ksize < 1 || ksize > 5 || (ksize & 1) == 0) return fail(SSCONV_E_INVALID, "ksize must be odd, 1..5");
   if (stride != 1 && stride != 2) return fail(SSCONV_E_INVALID, "stride must be 1 or 2");
   if (submanifold && stride != 1) return fail(SSCONV_E_INVALID, "submanifold requires stride 1");
+  if (ksize == 2) {
+    if (stride != 2) return fail(SSCONV_E_INVALID, "ksize 2 (pooling windows) requires stride 2, not submanifold");
+  } else if (ksize < 1 || ksize > 5 || (ksize & 1) == 0) {
+    return fail(SSCONV_E_INVALID, "ksize must be odd, 1..5, or 2 with stride 2");
+  }
   for (int a = 0; a < 3; ++a)
     if (grid[a] < 1) return fail(SSCONV_E_INVALID, "grid extents must be positive");
   auto* rb = new ssconv_rulebook();

@@ -1,4 +1,5 @@
-"""A stack of SS-Conv layers with the gated nonlinearity between them (Sec. 3.2-3.3).
+"""A stack of SS-Conv layers with the gated nonlinearity between them (Sec. 3.2-3.3), and the
+paper's downsampling block (stride-1 SS-Conv, Norm, gate, average pooling).
 
 Every step calls the C ABI through ``binding``; this module only sequences the
 calls and keeps what the backward pass needs.  A layer object provides
@@ -88,3 +89,53 @@ class Stack:
             if L.rb is not None:
                 L.rb.close()
                 L.rb = None
+
+
+@dataclass
+class DownBlock:
+    """The paper's downsampling block: a stride-1 submanifold SS-Conv, steerable Norm (Eq. 11)
+    over every output field (gate channels included), the gated nonlinearity (Eq. 12), then
+    2x2x2 average pooling (the footnote of Sec. 3.1).  Rule books are rebuilt every call."""
+    state: LayerState
+    dtype: torch.dtype = torch.float32
+    norm_eps: float = B.NORM_EPS
+    pool_rb: Optional[B.Rulebook] = None
+    z: Optional[torch.Tensor] = None     # normalised convolution output (input of the gate)
+
+    @staticmethod
+    def create(layer_spec, coeffs, grid: int, device, dtype=torch.float32) -> "DownBlock":
+        if layer_spec.stride != 1 or not layer_spec.submanifold:
+            raise ValueError("the block's convolution is a stride-1 submanifold SS-Conv")
+        st = Stack.create([layer_spec], [coeffs], grid, device, dtype)
+        return DownBlock(st.layers[0], dtype)
+
+    def forward(self, coords: torch.Tensor, feats: torch.Tensor):
+        """Returns (pooled coords, pooled features)."""
+        L, s = self.state, self.state.layer
+        for rb in (L.rb, self.pool_rb):
+            if rb is not None:
+                rb.close()
+        L.W = B.synth_kernel(L.desc, L.basis, L.coeffs, self.dtype)
+        L.rb = B.Rulebook(coords, L.grid, s.ksize, 1, True)
+        L.x = feats
+        L.y = B.forward(feats, L.rb, L.W)
+        self.z = B.norm_forward(s.fields_out, L.y, self.norm_eps)
+        h = B.gate_forward(regular_fields(s), self.z) if s.gated else self.z
+        self.pool_rb = B.Rulebook(coords, L.grid, 2, 2, False)
+        return self.pool_rb.out_coords(), B.pool_forward(h, self.pool_rb)
+
+    def backward(self, grad: torch.Tensor, need_input_grad: bool = True):
+        """Returns (grad of the block input or None, grad_coeffs)."""
+        L, s = self.state, self.state.layer
+        g = B.pool_backward(grad, self.pool_rb)
+        if s.gated:
+            g = B.gate_backward(regular_fields(s), self.z, g)
+        g = B.norm_backward(s.fields_out, L.y, g, self.norm_eps)
+        return B.backward(L.x, g, L.rb, L.W, L.desc, L.basis, need_feats=need_input_grad, need_coeffs=True,
+                          n_coeff=L.n_coeff)
+
+    def close(self):
+        for rb in (self.state.rb, self.pool_rb):
+            if rb is not None:
+                rb.close()
+        self.state.rb = self.pool_rb = None

@@ -97,3 +97,31 @@ def stack_reference(i: int):
         grads[idx] = oc.synth_adjoint(L.spec, L.lay.basis, dk)
         g = oc.grad_feats(g, L.R, L.kappa, len(L.coords_in))
     return xs, ys, h, g, grads
+
+
+@lru_cache(maxsize=None)
+def block_reference(i: int):
+    """The downsampling block of workload i in fp64: SS-Conv -> Norm -> gate -> average pooling.
+
+    Returns (pooled coords, pooled output, upstream gradient, grad of the block input,
+    grad of the coefficients)."""
+    from oracle import norm_pool as onp
+    spec = CONFIGS[i]
+    L = layers_of(i)[0]
+    f = features_of(i).astype(np.float64)
+    fo = L.spec.fields_out
+    regular = fo[:-1] if L.spec.gated else fo
+    y = oc.forward(f, L.R, L.kappa, len(L.coords_out))
+    z = onp.norm_forward(y, fo)
+    h = oc.gate_forward(z, regular) if L.spec.gated else z
+    pc = onp.pool_sites(L.coords_out)
+    member = onp.pool_members(L.coords_out, pc)
+    out = onp.pool_forward(h, member, len(pc))
+    g = make_grad(spec, len(pc), h.shape[1]).astype(np.float64)
+    gh = onp.pool_backward(g, member)
+    gz = oc.gate_backward(z, gh, regular) if L.spec.gated else gh
+    gy = onp.norm_backward(y, gz, fo)
+    d_in = oc.grad_feats(gy, L.R, L.kappa, len(f))
+    dk = oc.grad_kappa(f, gy, L.R, L.kappa.shape)
+    dw = oc.synth_adjoint(L.spec, L.lay.basis, dk)
+    return pc, out, g, d_in, dw

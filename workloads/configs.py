@@ -1,4 +1,4 @@
-"""The five synthetic SS-Conv workloads (layer shapes, basis parameters, dtypes).
+"""The synthetic SS-Conv workloads (layer shapes, basis parameters, dtypes).
 
 Field lists are ``((l, multiplicity), ...)`` in channel order: all fields of an
 entry are consecutive and each field's ``2l+1`` components are contiguous.
@@ -99,6 +99,14 @@ CONFIGS = {
          LayerSpec(3, 1, True, F_208, gate_fields(F_208), shells=(0.0, 1.0), gated=True),
          LayerSpec(3, 2, False, F_208, F_208, shells=(0.0, 1.0))),
         geometry="objects_dense", params=dict(extent=(8.0, 24.0), scale=0.555, margin=2)),
+    # The paper's downsampling block on the objects of workload 3 (Sec. 3.1 footnote, Sec. 3.3):
+    # stride-1 submanifold SS-Conv -> Norm (Eq. 11, over every output field, gates included)
+    # -> gated nonlinearity (Eq. 12) -> 2x2x2 average pooling, 64^3 -> 32^3.
+    6: WorkloadSpec(
+        6, "objects64_b32_block_k3_sub_norm_gate_pool_60to120", 64, 32, "f32",
+        (LayerSpec(3, 1, True, ((0, 16), (1, 8), (2, 4)), gate_fields(((0, 32), (1, 16), (2, 8))),
+                   shells=(0.0, 1.0), gated=True),),
+        geometry="objects_sparse", params=dict(extent=(8.0, 24.0), n_points=1024, norm=True, pool=True)),
 }
 
 
