@@ -3,7 +3,8 @@
 // Instead of Alg. 1's all-pairs loop, every input site is inserted into an
 // open-addressing hash table in HBM (64-bit slots key<<32 | row, lock-free
 // atomicCAS, linear probing), and every (output site, offset) pair probes it
-// once for y = stride*x - s.  Results:
+// once for y = stride*x - s (submanifold layers: half the offsets, the other half mirrored).
+// Results:
 //   nbr[s][x]   neighbour map (input row or -1), offset-major so that the
 //               forward gather reads one coalesced index vector per offset;
 //   pairs       R_s for every offset, compacted with wavefront ballots and a
@@ -154,44 +155,97 @@ __global__ void emit_outputs(const uint32_t* __restrict__ bits, int64_t nw, cons
   }
 }
 
-// Pass 1 (count=true) writes nbr and per-(offset, block) counts; pass 2 writes the pairs.
-template <bool kCount>
+// Logical (row block, offset) of workgroup blockIdx.x in a 1-D launch of nblk * nS workgroups.
+// Workgroup ids are dispatched round-robin over the 8 XCDs (id % 8); each XCD is given one
+// contiguous range of logical ids, row block first, so an XCD looks up every offset of a
+// contiguous range of sites and the hash lines those lookups touch stay in its own L2.
+__device__ __forceinline__ void xcd_tile(int64_t total, int nS, int64_t* rblk, int* s) {
+  const int64_t w = blockIdx.x;
+  const int x = (int)(w & 7);
+  const int64_t q = total >> 3;
+  const int r = (int)(total & 7);
+  const int64_t L = x * q + min(x, r) + (w >> 3);
+  *rblk = L / nS;
+  *s = (int)(L - *rblk * nS);
+}
+
+__device__ __forceinline__ int lookup(const int32_t* __restrict__ out_c, int64_t p, int s, int ksize, int stride,
+                                      int g0, int g1, int g2, const uint64_t* __restrict__ slots, uint64_t mask) {
+  const int h = ksize / 2;
+  const int dx = s / (ksize * ksize) - h, dy = (s / ksize) % ksize - h, dz = s % ksize - h;
+  const int4 v = reinterpret_cast<const int4*>(out_c)[p];
+  const int yx = stride * v.y - dx, yy = stride * v.z - dy, yz = stride * v.w - dz;
+  if (yx < 0 || yy < 0 || yz < 0 || yx >= g0 || yy >= g1 || yz >= g2) return -1;
+  return hash_find(slots, mask, site_key(v.x, yx, yy, yz, g0, g1, g2));
+}
+
+// Neighbour-map passes over (offset s, block of 256 output rows):
+//   kLookupCount  looks every (site, offset) up, writes nbr and per-(offset, block) pair counts
+//                 (1-D XCD-ordered launch of nblk * K workgroups);
+//   kCount        counts the pairs of a finished nbr (grid (nblk, K));
+//   kWrite        writes the pairs at the scanned offsets (grid (nblk, K)).
+constexpr int kLookupCount = 0, kCount = 1, kWrite = 2;
+template <int kMode>
 __global__ __launch_bounds__(256) void probe_kernel(const int32_t* __restrict__ out_c, int64_t n_out, int ksize,
                                                     int stride, int g0, int g1, int g2,
-                                                    const uint64_t* __restrict__ slots, uint64_t mask,
+                                                    const uint64_t* __restrict__ slots, uint64_t mask, int nblk,
                                                     int32_t* __restrict__ nbr, int32_t* __restrict__ counts,
                                                     const int64_t* __restrict__ offs, int32_t* __restrict__ pairs) {
   __shared__ int wcount[4];
-  const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int s = blockIdx.y;
-  const int nblk = gridDim.x;
+  int64_t rblk = blockIdx.x;
+  int s = blockIdx.y;
+  if (kMode == kLookupCount) xcd_tile((int64_t)nblk * ksize * ksize * ksize, ksize * ksize * ksize, &rblk, &s);
+  const int64_t p = rblk * 256 + threadIdx.x;
   int nb = -1;
-  if (kCount) {
-    if (p < n_out) {
-      int h = ksize / 2;
-      int dx = s / (ksize * ksize) - h, dy = (s / ksize) % ksize - h, dz = s % ksize - h;
-      int4 v = reinterpret_cast<const int4*>(out_c)[p];
-      int yx = stride * v.y - dx, yy = stride * v.z - dy, yz = stride * v.w - dz;
-      if (yx >= 0 && yy >= 0 && yz >= 0 && yx < g0 && yy < g1 && yz < g2)
-        nb = hash_find(slots, mask, site_key(v.x, yx, yy, yz, g0, g1, g2));
+  if (p < n_out) {
+    if (kMode == kLookupCount) {
+      nb = lookup(out_c, p, s, ksize, stride, g0, g1, g2, slots, mask);
       nbr[(int64_t)s * n_out + p] = nb;
+    } else {
+      nb = nbr[(int64_t)s * n_out + p];
     }
-  } else if (p < n_out) {
-    nb = nbr[(int64_t)s * n_out + p];
   }
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const uint64_t ball = __ballot(nb >= 0);
   if (lane == 0) wcount[w] = __popcll(ball);
   __syncthreads();
-  if (kCount) {
-    if (threadIdx.x == 0) counts[(int64_t)s * nblk + blockIdx.x] = wcount[0] + wcount[1] + wcount[2] + wcount[3];
+  if (kMode != kWrite) {
+    if (threadIdx.x == 0) counts[(int64_t)s * nblk + rblk] = wcount[0] + wcount[1] + wcount[2] + wcount[3];
   } else if (nb >= 0) {
     int before = 0;
     for (int i = 0; i < w; ++i) before += wcount[i];
     const uint64_t lower = lane ? (ball & ((1ull << lane) - 1)) : 0ull;
-    int64_t at = offs[(int64_t)s * nblk + blockIdx.x] + before + __popcll(lower);
+    int64_t at = offs[(int64_t)s * nblk + rblk] + before + __popcll(lower);
     reinterpret_cast<int2*>(pairs)[at] = make_int2((int)p, nb);
   }
+}
+
+// Submanifold layers (one site set, rows shared): only the offsets s < c = (K-1)/2 are looked
+// up.  If site x has neighbour y at offset s (y = x - d(s)), then y has neighbour x at the
+// mirrored offset K-1-s (d(K-1-s) = -d(s)), so that entry is written from here; distinct x
+// give distinct y, so every entry is written at most once.  Rows c..K-1 are set beforehand by
+// mirror_init (c: the identity, above c: -1).  1-D XCD-ordered launch of nblk * c workgroups.
+__global__ __launch_bounds__(256) void mirror_lookup_kernel(const int32_t* __restrict__ c_in, int64_t n, int ksize,
+                                                            int g0, int g1, int g2,
+                                                            const uint64_t* __restrict__ slots, uint64_t mask,
+                                                            int nblk, int32_t* __restrict__ nbr) {
+  const int K = ksize * ksize * ksize, c = (K - 1) / 2;
+  int64_t rblk;
+  int s;
+  xcd_tile((int64_t)nblk * c, c, &rblk, &s);
+  const int64_t p = rblk * 256 + threadIdx.x;
+  if (p >= n) return;
+  const int nb = lookup(c_in, p, s, ksize, 1, g0, g1, g2, slots, mask);
+  nbr[(int64_t)s * n + p] = nb;
+  if (nb >= 0) nbr[(int64_t)(K - 1 - s) * n + nb] = (int32_t)p;
+}
+
+__global__ void mirror_init(int32_t* __restrict__ nbr, int64_t n, int K) {
+  const int c = (K - 1) / 2;
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (int64_t)(K - c) * n) return;
+  const int64_t p = i % n;
+  nbr[(int64_t)c * n + i] = i < n ? (int32_t)p : -1;
 }
 
 __global__ void gather_offsets(const int64_t* __restrict__ offs, int K, int nblk, const int64_t* __restrict__ total,
@@ -417,8 +471,21 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     int64_t* stmp = (int64_t*)(t1 + o_stmp);
     int64_t* dtotal = stmp + scan_tmp_elems(ncnt);
     dim3 gp(nblk, K);
-    probe_kernel<true><<<gp, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0], grid[1], grid[2],
-                                          rb->hash_in, (uint64_t)(rb->cap_in - 1), rb->nbr, counts, nullptr, nullptr);
+    const uint64_t mask_in = (uint64_t)(rb->cap_in - 1);
+    if (submanifold) {
+      const int c = (K - 1) / 2;
+      mirror_init<<<cdiv((int64_t)(K - c) * n_out, 256), 256, 0, st>>>(rb->nbr, n_out, K);
+      if (c > 0)
+        mirror_lookup_kernel<<<(unsigned)((int64_t)nblk * c), 256, 0, st>>>(rb->out_coords, n_out, ksize, grid[0],
+                                                                             grid[1], grid[2], rb->hash_in, mask_in,
+                                                                             nblk, rb->nbr);
+      probe_kernel<kCount><<<gp, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0], grid[1], grid[2],
+                                               rb->hash_in, mask_in, nblk, rb->nbr, counts, nullptr, nullptr);
+    } else {
+      probe_kernel<kLookupCount><<<(unsigned)ncnt, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0],
+                                                                  grid[1], grid[2], rb->hash_in, mask_in, nblk,
+                                                                  rb->nbr, counts, nullptr, nullptr);
+    }
     SSC_HIP(hipGetLastError());
     SSC_TRY(exclusive_scan(counts, ncnt, offs, dtotal, stmp, st));
     gather_offsets<<<1, 256, 0, st>>>(offs, K, nblk, dtotal, rb->pair_off_dev);
@@ -431,8 +498,8 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
       SSC_TRY(dev_alloc((void**)&rb->mem[2], (size_t)host[0] * 8, st));
       rb->pairs = (int32_t*)rb->mem[2];
     }
-    probe_kernel<false><<<gp, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0], grid[1], grid[2],
-                                           rb->hash_in, (uint64_t)(rb->cap_in - 1), rb->nbr, nullptr, offs, rb->pairs);
+    probe_kernel<kWrite><<<gp, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0], grid[1], grid[2],
+                                             rb->hash_in, mask_in, nblk, rb->nbr, nullptr, offs, rb->pairs);
     SSC_HIP(hipGetLastError());
   } else {
     SSC_HIP(hipMemsetAsync(rb->pair_off_dev, 0, (size_t)(K + 1) * 8, st));
