@@ -248,7 +248,9 @@ int ssconv_pool_backward(const void* grad_out, ssconv_dtype dtype, int channels,
  * fp32 kernel gradient loads rows into registers instead of an LDS ring; 8 = the
  * generic gather-GEMM kernel splits every tile's offsets three ways (fp32
  * partials added in split order), which it otherwise does only when its tiles
- * leave compute units idle; results
+ * leave compute units idle; 9 = fp32 convolutions take the pair-list path
+ * (one GEMM per offset over R_s, then a per-row sum in offset order) wherever
+ * it applies; 10 = never take it, which a cost model otherwise decides; results
  * agree within the dtype's tolerance for every value); option 4 = kernel
  * timing: a nonzero value switches it on and clears this thread's log, 0
  * switches it off; while on, every gather-GEMM kernel launch (the one of

@@ -354,6 +354,17 @@ struct KernelTimer {
 int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_rulebook* rb, const void* W, int cout,
                  void* out, hipStream_t st) {
   if (rb->n_out == 0) return SSCONV_OK;
+  if (dt == SSCONV_F32 && pair_path_wins(rb, dt, cin, cout, rb->n_out)) {
+    void* ws = nullptr;
+    SSC_TRY(dev_alloc(&ws, pair_path_bytes(rb, cin, cout, rb->n_out), st));
+    int rc;
+    {
+      KernelTimer timer(st);
+      rc = pair_gemm(feats, cin, W, cout, rb, 1, out, rb->n_out, ws, st);
+    }
+    dev_free(ws, st);
+    return rc;
+  }
   if (dt == SSCONV_F32) {
     KernelTimer timer(st);
     return dispatch_gg<float>(feats, rb->n_in, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st);
@@ -412,8 +423,11 @@ BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int co
     nparts = (size_t)L.nsplit * K;
   }
   size_t o = 0;
-  L.nbrT = o;  // inverse neighbour map: only generated output sets need one
-  if (!rb->submanifold) o += align256(K * (size_t)rb->n_in * 4);
+  L.pair_feats = dt == SSCONV_F32 && rb->n_in > 0 && pair_path_wins(rb, dt, cout, cin, rb->n_in);
+  L.nbrT = o;  // inverse neighbour map: only generated output sets on the gather kernels need one
+  if (!rb->submanifold && !L.pair_feats) o += align256(K * (size_t)rb->n_in * 4);
+  L.pair = o;
+  if (L.pair_feats) o += align256(pair_path_bytes(rb, cout, cin, rb->n_in));
   L.Wt = o;
   o += align256(K * (size_t)cin * cout * sz);
   L.part = o;
@@ -431,6 +445,15 @@ BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int co
 int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout, const ssconv_rulebook* rb,
                         const void* W, void* grad_feats, char* ws, const BwdLayout& L, hipStream_t st) {
   if (rb->n_in == 0) return SSCONV_OK;
+  if (L.pair_feats) {
+    // kappa^T in the same offset order: the pairs of R_s are walked with their roles swapped
+    const int64_t nw = (int64_t)rb->K * cin * cout;
+    transpose_kernel<float><<<cdiv(nw, 256), 256, 0, st>>>((const float*)W, rb->K, cout, cin, false,
+                                                            (float*)(ws + L.Wt));
+    SSC_HIP(hipGetLastError());
+    KernelTimer timer(st);
+    return pair_gemm(grad_out, cout, ws + L.Wt, cin, rb, 0, grad_feats, rb->n_in, ws + L.pair, st);
+  }
   const bool mirror = rb->submanifold != 0;
   const int32_t* nbrT = rb->nbr;
   void* Wt = ws + L.Wt;

@@ -6,9 +6,17 @@
 namespace ssconv {
 
 struct BwdLayout {
-  size_t nbrT = 0, Wt = 0, part = 0, dW = 0, total = 0;  // byte offsets in the workspace
+  size_t nbrT = 0, Wt = 0, part = 0, dW = 0, pair = 0, total = 0;  // byte offsets in the workspace
   int nsplit = 1;
+  bool pair_feats = false;  // feature gradient on the pair-list path
 };
+
+// Pair-list GEMM for sparse fp32 layers (pair_gemm.hip).
+bool pair_path_supported(const ssconv_rulebook* rb, ssconv_dtype dt, int ca, int cb);
+bool pair_path_wins(const ssconv_rulebook* rb, ssconv_dtype dt, int ca, int cb, int64_t n_dst);
+size_t pair_path_bytes(const ssconv_rulebook* rb, int ca, int cb, int64_t n_dst);
+int pair_gemm(const void* src, int ca, const void* Bt, int cb, const ssconv_rulebook* rb, int sel_in, void* dst,
+              int64_t n_dst, void* ws, hipStream_t st);
 
 int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_rulebook* rb, const void* W, int cout,
                  void* out, hipStream_t st);

@@ -538,7 +538,11 @@ int kgrad_f32_units_want(const ssconv_rulebook* rb, int cin, int cout) {
   // one full round of the 2048 wavefront slots (256 CUs x two four-wavefront workgroups): measured
   // against 1024, 1536, 3072 and 4096 tasks, fewer partials to add up outweigh the balance of
   // two rounds (C2 step -12 us, C5 -215 us against 4096)
-  return std::max(1, 2048 / (p.mtiles * p.ntiles));
+  const int64_t slots = std::max(1, 2048 / (p.mtiles * p.ntiles));
+  // at least ~256 pairs per unit: below that the partial tiles (written once, added up again)
+  // outweigh the gathered rows of the unit (C6: 1024 units of ~83 pairs made 35 MB of partials)
+  const int64_t by_pairs = std::max<int64_t>(rb->K, rb->n_pairs / 256);
+  return (int)std::max<int64_t>(1, std::min(slots, by_pairs));
 }
 
 int kgrad_f32(const void* grad_out, const void* feats, int cin, int cout, const ssconv_rulebook* rb,

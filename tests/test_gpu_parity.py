@@ -100,7 +100,7 @@ def _layer_io(i):
     return L, dt, desc, basis, rb, W, feats
 
 
-@pytest.mark.parametrize("i", [1, 2, 3, 4])
+@pytest.mark.parametrize("i", [1, 2, 3, 4, 6])
 def test_forward_matches_oracle(i):
     print(f"forward config {i}", flush=True)
     L, dt, desc, basis, rb, W, feats = _layer_io(i)
@@ -112,7 +112,7 @@ def test_forward_matches_oracle(i):
     rb.close()
 
 
-@pytest.mark.parametrize("i", [1, 2, 3, 4])
+@pytest.mark.parametrize("i", [1, 2, 3, 4, 6])
 def test_backward_matches_oracle(i):
     print(f"backward config {i}", flush=True)
     L, dt, desc, basis, rb, W, feats = _layer_io(i)
@@ -140,7 +140,7 @@ def test_forward_backward_deterministic():
 
 
 @pytest.mark.parametrize("i,variant", [(2, 1), (2, 2), (2, 3), (3, 3), (2, 7), (3, 7), (4, 5), (4, 6), (2, 8),
-                                       (3, 8)])
+                                       (3, 8), (1, 9), (2, 9), (3, 10), (6, 10)])
 def test_kernel_selection_overrides(i, variant):
     """Every alternative kernel configuration (forced from the host) stays within tolerance."""
     print(f"config {i} kernel variant {variant}", flush=True)
@@ -156,4 +156,15 @@ def test_kernel_selection_overrides(i, variant):
     errs = rel_err(out, want), rel_err(gf.float().cpu().numpy(), d_in), rel_err(gc.cpu().numpy(), dw)
     print(f"config {i} variant {variant} errors {errs}", flush=True)
     assert max(errs) < tol
+    rb.close()
+
+
+def test_pair_path_deterministic():
+    """The sparse stride-2 layer runs on the pair-list path: same bits on every call."""
+    L, dt, desc, basis, rb, W, feats = _layer_io(3)
+    g = torch.randn(rb.n_out, L.spec.cout, device=DEV, generator=torch.Generator(DEV).manual_seed(1))
+    o1, o2 = P.forward(feats, rb, W), P.forward(feats, rb, W)
+    a1, _ = P.backward(feats, g, rb, W, desc, basis, need_coeffs=False)
+    a2, _ = P.backward(feats, g, rb, W, desc, basis, need_coeffs=False)
+    assert torch.equal(o1, o2) and torch.equal(a1, a2)
     rb.close()
