@@ -130,29 +130,22 @@ __global__ void mark_outputs(const int32_t* __restrict__ c, int64_t n, int ksize
   atomicOr(&bits[bit >> 5], 1u << (bit & 31));
 }
 
-__global__ void popcount_words(const uint32_t* __restrict__ bits, int64_t nw, int32_t* __restrict__ cnt) {
-  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < nw) cnt[i] = __popc(bits[i]);
-}
-
-__global__ void emit_outputs(const uint32_t* __restrict__ bits, int64_t nw, const int64_t* __restrict__ offs,
+// One thread per bit of the output bitmap (bit index < 2^32: it is a 32-bit site key): a set bit
+// is output row woff[word] + (set bits below it in its word), so the rows come out in
+// lexicographic (b, x, y, z) order.
+__global__ void emit_outputs(const uint32_t* __restrict__ bits, int64_t nbits, const int64_t* __restrict__ woff,
                              int go0, int go1, int go2, int32_t* __restrict__ out) {
-  int64_t w = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (w >= nw) return;
-  uint32_t m = bits[w];
-  int64_t o = offs[w];
-  const int64_t per_b = (int64_t)go0 * go1 * go2;
-  while (m) {
-    int b = __ffs(m) - 1;
-    m &= m - 1;
-    int64_t bit = w * 32 + b;
-    int bb = (int)(bit / per_b);
-    int64_t r = bit - (int64_t)bb * per_b;
-    int z = (int)(r % go2);
-    int y = (int)((r / go2) % go1);
-    int x = (int)(r / ((int64_t)go1 * go2));
-    reinterpret_cast<int4*>(out)[o++] = make_int4(bb, x, y, z);
-  }
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= nbits) return;
+  const uint32_t bit = (uint32_t)i, b = bit & 31u;
+  const uint32_t m = bits[bit >> 5];
+  if (!((m >> b) & 1u)) return;
+  const int64_t o = woff[bit >> 5] + __popc(m & ((1u << b) - 1u));
+  const uint32_t g2 = (uint32_t)go2, g12 = (uint32_t)go1 * g2, per_b = (uint32_t)go0 * g12;
+  const uint32_t bb = bit / per_b, r = bit - bb * per_b;
+  const uint32_t x = r / g12, yz = r - x * g12;
+  const uint32_t y = yz / g2, z = yz - y * g2;
+  reinterpret_cast<int4*>(out)[o] = make_int4((int)bb, (int)x, (int)y, (int)z);
 }
 
 // Logical (row block, offset) of workgroup blockIdx.x in a 1-D launch of nblk * nS workgroups.
@@ -248,13 +241,6 @@ __global__ void mirror_init(int32_t* __restrict__ nbr, int64_t n, int K) {
   nbr[(int64_t)c * n + i] = i < n ? (int32_t)p : -1;
 }
 
-__global__ void gather_offsets(const int64_t* __restrict__ offs, int K, int nblk, const int64_t* __restrict__ total,
-                               int64_t* __restrict__ pair_off) {
-  int s = threadIdx.x;
-  if (s < K) pair_off[s] = offs[(int64_t)s * nblk];
-  if (s == 0) pair_off[K] = *total;
-}
-
 int64_t next_pow2(int64_t v) {
   int64_t c = 64;
   while (c < v) c <<= 1;
@@ -330,10 +316,12 @@ static int hash_capacity(int64_t n, int64_t* cap) {
 }
 
 // Fills the table (capacity cap, already allocated) and inserts the n sites; init_flags also
-// clears the build flags in the fill kernel.
+// clears the build flags in the fill kernel, validate also records the largest batch index in
+// flags[1] (and bounds violations in flags[0]) before the inserts.
 static int build_hash(const int32_t* coords, int64_t n, const int* g, hipStream_t st, uint64_t* slots, int64_t cap,
-                      int* flags, bool init_flags) {
+                      int* flags, bool init_flags, bool validate) {
   fill_slots<<<cdiv(cap, 256), 256, 0, st>>>(slots, cap, kEmpty, init_flags ? flags : nullptr);
+  if (validate && n > 0) validate_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, g[0], g[1], g[2], flags, flags + 1);
   if (n > 0)
     hash_insert_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, g[0], g[1], g[2], max_batch(g), slots,
                                                      (uint64_t)(cap - 1), flags);
@@ -386,21 +374,18 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     }
   }
 
+  // the input table's fill also clears the build flags; its inserts do not depend on the output
+  // set, so for generated sets they are queued before the synchronisation that sizes the bitmap
+  SSC_TRY(build_hash(coords, n, rb->grid, st, rb->hash_in, rb->cap_in, dflags, true, !submanifold));
   if (!submanifold) {
     // the output bitmap spans the batch: its extent is needed on the host before the next launch
-    SSC_HIP(hipMemsetAsync(dflags, 0, 4, st));
-    SSC_HIP(hipMemsetAsync(dflags + 1, 0xff, 4, st));  // max b = -1
-    if (n > 0) validate_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, grid[0], grid[1], grid[2], dflags, dflags + 1);
-    SSC_HIP(hipGetLastError());
     SSC_HIP(hipMemcpyAsync(host, dflags, 8, hipMemcpyDeviceToHost, st));
     SSC_HIP(hipStreamSynchronize(st));
     const int flags0 = ((int*)host)[0], maxb = ((int*)host)[1];
-    if (flags0 & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid or has b < 0");
+    if (flags0 & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid, has b < 0, or (max b + 1) * grid volume exceeds the 32-bit key space");
     if (maxb > max_batch(grid)) return fail(SSCONV_E_BOUNDS, "(max b + 1) * grid volume exceeds the 32-bit key space");
     rb->nbatch = maxb + 1;
   }
-
-  SSC_TRY(build_hash(coords, n, rb->grid, st, rb->hash_in, rb->cap_in, dflags, submanifold != 0));
 
   // ---- output site set ----
   Scratch tmp(st);
@@ -414,12 +399,11 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     const int64_t nbits = rb->nbatch * (int64_t)go[0] * go[1] * go[2];
     const int64_t nw = (nbits + 31) / 32;
     Carve c;
-    const size_t o_bits = c.take((size_t)nw * 4), o_wcnt = c.take((size_t)nw * 4), o_woff = c.take((size_t)nw * 8),
+    const size_t o_bits = c.take((size_t)nw * 4), o_woff = c.take((size_t)nw * 8),
                  o_stmp = c.take((size_t)scan_tmp_elems(nw) * 8 + 8);
     char* t0 = nullptr;
     SSC_TRY(tmp.alloc((void**)&t0, c.at));
     uint32_t* bits = (uint32_t*)(t0 + o_bits);
-    int32_t* wcnt = (int32_t*)(t0 + o_wcnt);
     int64_t* woff = (int64_t*)(t0 + o_woff);
     int64_t* stmp = (int64_t*)(t0 + o_stmp);
     int64_t* dtotal = stmp + scan_tmp_elems(nw);
@@ -429,8 +413,7 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
       mark_outputs<<<gm, 256, 0, st>>>(coords, n, ksize, stride, go[0], go[1], go[2], bits);
     }
     if (nw) {
-      popcount_words<<<cdiv(nw, 256), 256, 0, st>>>(bits, nw, wcnt);
-      SSC_TRY(exclusive_scan(wcnt, nw, woff, dtotal, stmp, st));
+      SSC_TRY(exclusive_scan_popc(bits, nw, woff, dtotal, stmp, st));
     } else {
       SSC_HIP(hipMemsetAsync(dtotal, 0, 8, st));
     }
@@ -451,9 +434,9 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     rb->hash_out = (uint64_t*)(b1 + o_hash);
     rb->nbr = (int32_t*)(b1 + o_nbr);
     if (bound <= ((size_t)1 << 30)) rb->pairs = (int32_t*)(b1 + o_pairs);
-    if (nw) emit_outputs<<<cdiv(nw, 256), 256, 0, st>>>(bits, nw, woff, go[0], go[1], go[2], rb->out_coords);
+    if (nbits) emit_outputs<<<cdiv(nbits, 256), 256, 0, st>>>(bits, nbits, woff, go[0], go[1], go[2], rb->out_coords);
     SSC_HIP(hipGetLastError());
-    SSC_TRY(build_hash(rb->out_coords, rb->n_out, go, st, rb->hash_out, rb->cap_out, dflags, false));
+    SSC_TRY(build_hash(rb->out_coords, rb->n_out, go, st, rb->hash_out, rb->cap_out, dflags, false, false));
   }
 
   // ---- neighbour map and per-offset pair lists ----
@@ -487,8 +470,7 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
                                                                   rb->nbr, counts, nullptr, nullptr);
     }
     SSC_HIP(hipGetLastError());
-    SSC_TRY(exclusive_scan(counts, ncnt, offs, dtotal, stmp, st));
-    gather_offsets<<<1, 256, 0, st>>>(offs, K, nblk, dtotal, rb->pair_off_dev);
+    SSC_TRY(exclusive_scan_pair_off(counts, K, nblk, offs, dtotal, stmp, rb->pair_off_dev, st));
     // the pair lists are written at their upper bound (every output has at most K neighbours), so
     // the write pass follows without a round trip to the host and the counts come back once,
     // below; past 1 GB the exact size is read back first

@@ -41,5 +41,12 @@ __device__ __forceinline__ V block_excl_scan(V v, V* total) {
 // may not alias.  tmp must hold scan_tmp_elems(n) int64 values.
 int64_t scan_tmp_elems(int64_t n);
 int exclusive_scan(const int32_t* in, int64_t n, int64_t* out, int64_t* total, int64_t* tmp, hipStream_t stream);
+// The same over the population counts of n bitmap words.
+int exclusive_scan_popc(const uint32_t* words, int64_t n, int64_t* out, int64_t* total, int64_t* tmp,
+                        hipStream_t stream);
+// The scan of K*nblk offset-major counts, followed by pair_off[s] = out[s*nblk] (s < K) and
+// pair_off[K] = *total.
+int exclusive_scan_pair_off(const int32_t* counts, int K, int nblk, int64_t* out, int64_t* total, int64_t* tmp,
+                            int64_t* pair_off, hipStream_t stream);
 
 }  // namespace ssconv
