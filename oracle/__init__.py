@@ -13,6 +13,7 @@ Modules
               reference convolution, gated nonlinearity (Alg. 1; Sec. 3.3, Eq. 12)
     norm_pool steerable normalisation (Sec. 3.3, Eq. 11) and 2x2x2 / stride-2
               sparse average pooling (footnote of Sec. 3.1), forward and backward
+    voxel     point-cloud voxelisation with per-cell feature averaging (Sec. 4.1)
 
 Readings of the paper that it takes (all pinned by invariants in tests/):
     real SH without Condon-Shortley phase, components ordered m = -l..l;
@@ -23,7 +24,9 @@ Readings of the paper that it takes (all pinned by invariants in tests/):
     generated output sets in lexicographic (b, x, y, z) order;
     gate = extra scalar output channel of the same convolution;
     Norm: eps = 1e-5, population statistics over every active site, no affine;
-    pooling divides window sums by 8 (zero-filled dense semantics).
+    pooling divides window sums by 8 (zero-filled dense semantics);
+    voxel cells floor((p - origin) / voxel) taken in fp32, points outside the
+    grid dropped, sites lexicographic.
 
 Parity status: every function here is pinned by at least one invariant test
 (brute force, dense convolution, exact equivariance, adjointness, closed
