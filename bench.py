@@ -11,7 +11,7 @@ Prints ONE JSON line: throughput in M active output sites/s, the roofline of
 the dominant kernel (timed with events on the stream it runs on) and the CPU
 oracle timed on a bounded sample on this host.
 
-    python bench.py [--steps K] [--warmup W] [--config {1..6}] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--config {1..7}] [--no-cpu-baseline]
 """
 import argparse
 import json
@@ -149,8 +149,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload index 1..6 (default: the 64^3 5x5x5 layer; 6: the "
-                    "downsampling block conv + norm + gate + pooling)")
+    ap.add_argument("--config", type=int, default=2, help="workload index 1..7 (default: the 64^3 5x5x5 layer; 6: the "
+                    "downsampling block conv + norm + gate + pooling; 7: input voxelisation)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work to aim for")
     ap.add_argument("--only", choices=["step", "forward"], default="step",
@@ -446,6 +446,51 @@ class BlockBench:
                 "step": "synth+rulebook+conv+norm+gate+pool rulebook+pool, then pool+gate+norm+conv backward"}
 
 
+class VoxelBench:
+    """Input voxelisation (workload 7, Sec. 4.1): one step = ssconv_voxelize over the object
+    point clouds (cells, site order, per-cell averages of (R, G, B, 1)); bandwidth-bound."""
+
+    def __init__(self, i, dev):
+        import torch
+        import paper_2111_07383_amd as P
+        from workloads import CONFIGS
+        from workloads.gen import make_point_cloud
+        self.P, self.torch = P, torch
+        self.spec = CONFIGS[i]
+        pts, bat, feats = make_point_cloud(self.spec)
+        self.points = torch.from_numpy(pts).to(dev)
+        self.batch = torch.from_numpy(bat).to(dev)
+        self.feats = torch.from_numpy(feats).to(dev)
+        self.events = None
+        c, _, _ = self.step()
+        self.n_sites = int(c.shape[0])
+
+    def step(self):
+        P, torch = self.P, self.torch
+        if self.events is not None:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+        out = P.voxelize(self.points, self.feats, self.batch, self.spec.batch, (0.0, 0.0, 0.0), 1.0, self.spec.grid)
+        if self.events is not None:
+            e1.record()
+            self.events.append((e0, e1))
+        return out
+
+    def sites(self):
+        return self.n_sites
+
+    def algorithmic_bytes(self):
+        """Points (12 B), batch index (4 B) and features (4 C B) read once; site coordinates
+        (16 B) and averages (4 C B) written once; the site row of every point (4 B) written."""
+        n, C = int(self.points.shape[0]), int(self.feats.shape[1])
+        return n * (12 + 4 + 4 * C + 4) + self.n_sites * (16 + 4 * C)
+
+    def config(self):
+        return {"workload": self.spec.name, "grid": self.spec.grid, "batch": self.spec.batch,
+                "points": int(self.points.shape[0]), "channels": int(self.feats.shape[1]), "n_out": self.n_sites,
+                "step": "voxelise (cells, lexicographic sites, per-cell averages); includes its one synchronisation"}
+
+
 # ---------------------------------------------------------------------------
 # CPU oracle baseline (bounded sample of the same workload)
 # ---------------------------------------------------------------------------
@@ -523,12 +568,28 @@ def cpu_baseline_block(i):
 
 
 def step_text(spec):
+    if spec.index == 7:
+        return "voxelisation of the object point clouds (cells, sites, per-cell averages)"
     if spec.index == 6:
         return ("synthesis + rule book + conv + norm + gate + pooling rule book + pooling, then pooling, gate, norm "
                 "and conv backward")
     if spec.index == 5:
         return "per layer synthesis + rule book + forward (+ gate), then the backward of every layer"
     return "synthesis + rule book + forward + backward"
+
+
+def cpu_baseline_voxel(i):
+    from oracle import voxel as ov
+    from workloads import CONFIGS
+    from workloads.gen import make_point_cloud
+    spec = CONFIGS[i]
+    pts, bat, feats = make_point_cloud(spec)
+    t0 = time.perf_counter()
+    c, _, _ = ov.voxelize(pts, bat, feats, (0.0, 0.0, 0.0), 1.0, spec.grid)
+    t = time.perf_counter() - t0
+    return {"value": len(c) / t / 1e6, "unit": "M active output sites/s", "cores": 1, "kind": "oracle",
+            "sample": f"{spec.name}: all {len(pts)} points, {len(c)} sites (numpy cells + dict averaging, "
+                      f"1 thread), {t:.1f} s"}
 
 
 def write_stats_summary(args):
@@ -650,6 +711,35 @@ def write_counter_summary(args):
     log(f"wrote {os.path.relpath(path, ROOT)}")
 
 
+def run_voxel_bench(args, dev):
+    import torch
+    b = VoxelBench(args.config, dev)
+    for _ in range(args.warmup):
+        b.step()
+    torch.cuda.synchronize()
+    b.events = []
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        b.step()
+    torch.cuda.synchronize()
+    t = time.perf_counter() - t0
+    ms = t / args.steps * 1e3
+    value = b.sites() / (ms / 1e3) / 1e6
+    ev_ms = float(np.median([a.elapsed_time(c) for a, c in b.events]))
+    achieved = b.algorithmic_bytes() / (ev_ms / 1e3) / 1e9
+    out = {"metric": METRIC, "value": value, "unit": "M active output sites/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "f32", "data": "synthetic", "config": b.config(),
+           "roofline": {"kernel": "ssconv_voxelize (all its launches)", "bound": "hbm", "achieved": achieved,
+                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                        "traffic_source": "not measured", "avg_launch_ms": ev_ms,
+                        "algorithmic_bytes_per_launch": b.algorithmic_bytes()}}
+    log(f"voxelise: {ms:.3f} ms/step, {value:.1f} M sites/s, {achieved:.0f} GB/s algorithmic")
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_voxel(args.config)
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.counter_summary:
@@ -686,8 +776,10 @@ def main():
         import paper_2111_07383_amd as P
         P.debug_set(3, args.variant)
     log(f"setting up {spec.name}")
-    if args.only == "forward" and args.config in (5, 6):
+    if args.only == "forward" and args.config in (5, 6, 7):
         raise SystemExit("--only forward applies to the single-layer workloads 1-4")
+    if args.config == 7:
+        return run_voxel_bench(args, dev)
     b = (StackBench(dev) if args.config == 5 else BlockBench(args.config, dev) if args.config == 6
          else SingleLayer(args.config, dev))
     run = b.forward_only if args.only == "forward" else b.step

@@ -235,6 +235,30 @@ int ssconv_pool_forward(const void* feats, ssconv_dtype dtype, int channels, ssc
 int ssconv_pool_backward(const void* grad_out, ssconv_dtype dtype, int channels, ssconv_rulebook_t rb,
                          void* grad_feats, hipStream_t stream);
 
+/* ---- voxelisation (Sec. 4.1) -------------------------------------------------
+ * A site is active when its grid cell encloses an input point; its feature is
+ * the average of the features of the points its cell encloses (the paper's
+ * points carry (R, G, B, 1); Feature-Steering merges re-voxelised sites the
+ * same way).  The cell of point p is floor((p - origin) / voxel) per axis, the
+ * subtraction and division in fp32 with round-to-nearest; points whose cell is
+ * outside [0, grid) or whose coordinates are not finite are dropped.
+ * points [n, 3] fp32; batch [n] int32 in [0, nbatch) or NULL (all 0);
+ * feats [n, channels] fp32 (channels >= 0; NULL when 0); origin [3] and grid
+ * [3] on the host; nbatch * grid volume < 2^32.
+ * Outputs (caller buffers sized for n sites, the upper bound): coords_out
+ * [n, 4] int32 (b, x, y, z), 16-byte aligned; feats_out [n, channels] fp32;
+ * point_row [n] int32 = the site row of each point or -1 (may be NULL);
+ * *n_sites (host) = the number of sites, rows [0, n_sites) are written in
+ * lexicographic (b, x, y, z) order.  Averages add each cell's points in point
+ * order in fp32 (deterministic).  Synchronises the stream once; temporaries
+ * come from the device memory cache.  Errors: E_INVALID, E_BOUNDS (a batch
+ * index outside [0, nbatch), or the key space exceeded), E_NOMEM, E_HIP; on
+ * error the outputs are unspecified and *n_sites is 0. */
+int ssconv_voxelize(const float* points, const int32_t* batch, const float* feats, int64_t n, int channels,
+                    const float* origin /*host [3]*/, float voxel, const int32_t* grid /*host [3]*/, int nbatch,
+                    int32_t* coords_out, float* feats_out, int32_t* point_row, int64_t* n_sites /*host*/,
+                    hipStream_t stream);
+
 /* ---- test hooks --------------------------------------------------------
  * Forces failure paths from the host so they can be tested without faulting
  * a device: option 1 = hash capacity (slots) used by the next rule book builds

@@ -38,7 +38,8 @@ def voxelize(points: np.ndarray, batch: np.ndarray, feats: np.ndarray, origin, v
     cells = point_cells(points, origin, voxel, grid)
     n = len(cells)
     b = np.zeros(n, np.int64) if batch is None else np.asarray(batch, np.int64).reshape(n)
-    f = np.asarray(feats, np.float64).reshape(n, -1)
+    f = np.asarray(feats, np.float64)
+    f = f.reshape(n, f.shape[-1] if f.ndim == 2 else 1)
     sums, counts = {}, {}
     for i in range(n):
         if cells[i, 0] < 0:

@@ -27,4 +27,5 @@ from .binding import (  # noqa: F401
     pool_backward,
     pool_forward,
     synth_kernel,
+    voxelize,
 )

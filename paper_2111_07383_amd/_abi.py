@@ -55,6 +55,8 @@ SIGNATURES = {
                                      c_void_p]),
     "ssconv_pool_forward": (c_int, [c_void_p, c_int, c_int, c_void_p, c_void_p, c_void_p]),
     "ssconv_pool_backward": (c_int, [c_void_p, c_int, c_int, c_void_p, c_void_p, c_void_p]),
+    "ssconv_voxelize": (c_int, [c_void_p, c_void_p, c_void_p, c_int64, c_int, POINTER(c_float), c_float,
+                                POINTER(c_int), c_int, c_void_p, c_void_p, c_void_p, POINTER(c_int64), c_void_p]),
     "ssconv_debug_set": (c_int, [c_int, c_int64]),
     "ssconv_debug_kernel_ms": (c_int, [POINTER(c_int64), POINTER(c_float)]),
 }

@@ -301,6 +301,35 @@ def pool_backward(grad_out: torch.Tensor, rb: Rulebook, stream=None) -> torch.Te
     return gf
 
 
+def voxelize(points: torch.Tensor, feats: Optional[torch.Tensor] = None, batch: Optional[torch.Tensor] = None,
+             nbatch: int = 1, origin=(0.0, 0.0, 0.0), voxel: float = 1.0, grid=64, stream=None):
+    """Voxelisation with per-cell feature averaging (Sec. 4.1).  Returns (coords [m, 4] int32,
+    averaged feats [m, C] fp32 or None, point_row [n] int32); with a batch tensor, nbatch
+    must cover its indices."""
+    _need(points, "points", torch.float32)
+    if points.dim() != 2 or points.shape[1] != 3:
+        raise ValueError("points must be [n, 3]")
+    n = points.shape[0]
+    C = 0
+    if feats is not None:
+        _need(feats, "feats", torch.float32)
+        if feats.dim() != 2 or feats.shape[0] != n:
+            raise ValueError(f"feats must be [{n}, C]")
+        C = feats.shape[1]
+    if batch is not None:
+        _need(batch, "batch", torch.int32, (n,))
+    g = (c_int * 3)(*([int(grid)] * 3 if np.isscalar(grid) else [int(v) for v in grid]))
+    o = (c_float * 3)(*[float(v) for v in origin])
+    coords = torch.empty((n, 4), dtype=torch.int32, device=points.device)
+    fo = torch.empty((n, C), dtype=torch.float32, device=points.device) if C else None
+    rows = torch.empty((n,), dtype=torch.int32, device=points.device)
+    m = c_int64()
+    check(lib().ssconv_voxelize(_ptr(points), _ptr(batch), _ptr(feats), n, C, o, float(voxel), g, int(nbatch),
+                                _ptr(coords), _ptr(fo), _ptr(rows), byref(m), _stream(stream)), "ssconv_voxelize")
+    k = m.value
+    return coords[:k], (fo[:k] if fo is not None else None), rows
+
+
 def debug_set(option: int, value: int) -> None:
     check(lib().ssconv_debug_set(int(option), int(value)), "ssconv_debug_set")
 

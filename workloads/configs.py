@@ -107,6 +107,12 @@ CONFIGS = {
         (LayerSpec(3, 1, True, ((0, 16), (1, 8), (2, 4)), gate_fields(((0, 32), (1, 16), (2, 8))),
                    shells=(0.0, 1.0), gated=True),),
         geometry="objects_sparse", params=dict(extent=(8.0, 24.0), n_points=1024, norm=True, pool=True)),
+    # Input voxelisation (Sec. 4.1): raw point clouds of 32 objects (the object recipe of
+    # workload 3 with 16 384 area-uniform points each) carrying (R, G, B, 1), voxelised into a
+    # 64^3 grid per object with per-cell feature averaging.  No convolution layer.
+    7: WorkloadSpec(
+        7, "points64_b32_voxelise_rgb1", 64, 32, "f32", (),
+        geometry="points", params=dict(extent=(8.0, 24.0), n_points=16384)),
 }
 
 

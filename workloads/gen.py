@@ -262,6 +262,30 @@ def make_workload(i, coeff_counts: Optional[List[int]] = None) -> Workload:
     return Workload(spec, coords, feats, coeffs)
 
 
+def make_point_cloud(spec: WorkloadSpec):
+    """Raw object point clouds (no voxelisation): (points float32 [n, 3] in voxel units, batch
+    int32 [n], features float32 [n, 4] = (R, G, B, 1) with R, G, B ~ U(0, 1)).  Objects follow
+    the sparse-object recipe (box / cylinder / ellipsoid, random rotation, centre 32 + U(-4, 4)^3)
+    with params["n_points"] area-uniform points each; points are listed object by object."""
+    rng = np.random.default_rng(_streams(spec)["geometry"])
+    lo, hi = spec.params["extent"]
+    n = spec.params["n_points"]
+    pts, bat = [], []
+    for b in range(spec.batch):
+        kind = rng.integers(0, 3)
+        ext = rng.uniform(lo, hi, 3)
+        R = random_rotation(rng)
+        c = 32.0 + rng.uniform(-4, 4, 3)
+        p = (ellipsoid_uniform(rng, ext, n), box_uniform(rng, ext, n), cylinder_uniform(rng, ext, n))[kind]
+        pts.append(p @ R.T + c)
+        bat.append(np.full(len(p), b, np.int32))
+    points = np.concatenate(pts).astype(np.float32)
+    frng = np.random.default_rng(_streams(spec)["features"])
+    rgb = frng.uniform(0.0, 1.0, (len(points), 3)).astype(np.float32)
+    feats = np.concatenate([rgb, np.ones((len(points), 1), np.float32)], 1)
+    return points, np.concatenate(bat), feats
+
+
 def shuffle_rows(seed: int, n: int) -> np.ndarray:
     """A seeded permutation of n rows (used to test row-order independence)."""
     return np.random.default_rng(seed).permutation(n)
