@@ -14,6 +14,8 @@ Modules
     norm_pool steerable normalisation (Sec. 3.3, Eq. 11) and 2x2x2 / stride-2
               sparse average pooling (footnote of Sec. 3.1), forward and backward
     voxel     point-cloud voxelisation with per-cell feature averaging (Sec. 4.1)
+    steer     Feature-Steering: Wigner-D rotation of the fields, rigid motion of the
+              site centres, re-voxelisation with averaging of merged sites (Sec. 4.1)
 
 Readings of the paper that it takes (all pinned by invariants in tests/):
     real SH without Condon-Shortley phase, components ordered m = -l..l;
