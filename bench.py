@@ -11,7 +11,7 @@ Prints ONE JSON line: throughput in M active output sites/s, the roofline of
 the dominant kernel (timed with events on the stream it runs on) and the CPU
 oracle timed on a bounded sample on this host.
 
-    python bench.py [--steps K] [--warmup W] [--config {1..7}] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--config {1..8}] [--no-cpu-baseline]
 """
 import argparse
 import json
@@ -149,8 +149,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload index 1..7 (default: the 64^3 5x5x5 layer; 6: the "
-                    "downsampling block conv + norm + gate + pooling; 7: input voxelisation)")
+    ap.add_argument("--config", type=int, default=2, help="workload index 1..8 (default: the 64^3 5x5x5 layer; 6: the "
+                    "downsampling block conv + norm + gate + pooling; 7: input voxelisation; "
+                    "8: Feature-Steering)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work to aim for")
     ap.add_argument("--only", choices=["step", "forward"], default="step",
@@ -491,6 +492,54 @@ class VoxelBench:
                 "step": "voxelise (cells, lexicographic sites, per-cell averages); includes its one synchronisation"}
 
 
+class SteerBench:
+    """Feature-Steering (workload 8, Sec. 4.1): one step = ssconv_steer of the 64^3 map with 104
+    channels by its seeded rigid motion (Wigner-D rotation of the fields, moved cell centres,
+    re-voxelisation averaging merged sites); bandwidth-bound."""
+
+    def __init__(self, i, dev):
+        import torch
+        import paper_2111_07383_amd as P
+        from workloads import CONFIGS
+        from workloads.gen import make_coords, make_features, make_motion
+        self.P, self.torch = P, torch
+        self.spec = CONFIGS[i]
+        self.fields = self.spec.layers[0].fields_in
+        coords = make_coords(self.spec)
+        self.coords = torch.from_numpy(coords).to(dev)
+        self.feats = torch.from_numpy(make_features(self.spec, len(coords), self.spec.layers[0].cin)).to(dev)
+        self.R, self.t = make_motion(self.spec)
+        self.events = None
+        c, _, _ = self.step()
+        self.n_sites = int(c.shape[0])
+
+    def step(self):
+        P, torch = self.P, self.torch
+        if self.events is not None:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+        out = P.steer(self.coords, self.feats, self.fields, self.R, self.t, 1, (0.0, 0.0, 0.0), 1.0, self.spec.grid)
+        if self.events is not None:
+            e1.record()
+            self.events.append((e0, e1))
+        return out
+
+    def sites(self):
+        return self.n_sites
+
+    def algorithmic_bytes(self):
+        """Input sites (16 B) and features (4 C B) read once, output sites and averaged
+        features written once, the new row of every input site (4 B) written."""
+        n, C = int(self.coords.shape[0]), int(self.feats.shape[1])
+        return n * (16 + 4 * C + 4) + self.n_sites * (16 + 4 * C)
+
+    def config(self):
+        return {"workload": self.spec.name, "grid": self.spec.grid, "n_in": int(self.coords.shape[0]),
+                "channels": int(self.feats.shape[1]), "n_out": self.n_sites,
+                "step": "steer (Wigner-D rotation, moved cell centres, re-voxelisation with averaging); "
+                        "includes its one synchronisation"}
+
+
 # ---------------------------------------------------------------------------
 # CPU oracle baseline (bounded sample of the same workload)
 # ---------------------------------------------------------------------------
@@ -568,6 +617,8 @@ def cpu_baseline_block(i):
 
 
 def step_text(spec):
+    if spec.index == 8:
+        return "Feature-Steering of the 64^3 104-channel map (Wigner-D rotation, moved centres, re-voxelisation)"
     if spec.index == 7:
         return "voxelisation of the object point clouds (cells, sites, per-cell averages)"
     if spec.index == 6:
@@ -590,6 +641,22 @@ def cpu_baseline_voxel(i):
     return {"value": len(c) / t / 1e6, "unit": "M active output sites/s", "cores": 1, "kind": "oracle",
             "sample": f"{spec.name}: all {len(pts)} points, {len(c)} sites (numpy cells + dict averaging, "
                       f"1 thread), {t:.1f} s"}
+
+
+def cpu_baseline_steer(i):
+    from oracle import steer as ost
+    from workloads import CONFIGS
+    from workloads.gen import make_coords, make_features, make_motion
+    spec = CONFIGS[i]
+    coords = make_coords(spec)
+    feats = make_features(spec, len(coords), spec.layers[0].cin)
+    R, t = make_motion(spec)
+    t0 = time.perf_counter()
+    c, _, _ = ost.steer(coords, feats, spec.layers[0].fields_in, R, t, (0.0, 0.0, 0.0), 1.0, spec.grid)
+    dt = time.perf_counter() - t0
+    return {"value": len(c) / dt / 1e6, "unit": "M active output sites/s", "cores": 1, "kind": "oracle",
+            "sample": f"{spec.name}: all {len(coords)} sites -> {len(c)} (numpy Wigner-D product, fp32 centres, "
+                      f"dict averaging, 1 thread), {dt:.2f} s"}
 
 
 def write_stats_summary(args):
@@ -713,7 +780,7 @@ def write_counter_summary(args):
 
 def run_voxel_bench(args, dev):
     import torch
-    b = VoxelBench(args.config, dev)
+    b = VoxelBench(args.config, dev) if args.config == 7 else SteerBench(args.config, dev)
     for _ in range(args.warmup):
         b.step()
     torch.cuda.synchronize()
@@ -730,13 +797,14 @@ def run_voxel_bench(args, dev):
     out = {"metric": METRIC, "value": value, "unit": "M active output sites/s", "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "f32", "data": "synthetic", "config": b.config(),
-           "roofline": {"kernel": "ssconv_voxelize (all its launches)", "bound": "hbm", "achieved": achieved,
+           "roofline": {"kernel": ("ssconv_voxelize" if args.config == 7 else "ssconv_steer") + " (all its launches)",
+                        "bound": "hbm", "achieved": achieved,
                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
                         "traffic_source": "not measured", "avg_launch_ms": ev_ms,
                         "algorithmic_bytes_per_launch": b.algorithmic_bytes()}}
-    log(f"voxelise: {ms:.3f} ms/step, {value:.1f} M sites/s, {achieved:.0f} GB/s algorithmic")
+    log(f"{b.spec.name}: {ms:.3f} ms/step, {value:.1f} M sites/s, {achieved:.0f} GB/s algorithmic")
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline_voxel(args.config)
+        out["cpu_baseline"] = cpu_baseline_voxel(args.config) if args.config == 7 else cpu_baseline_steer(args.config)
     print(json.dumps(out), flush=True)
 
 
@@ -776,9 +844,9 @@ def main():
         import paper_2111_07383_amd as P
         P.debug_set(3, args.variant)
     log(f"setting up {spec.name}")
-    if args.only == "forward" and args.config in (5, 6, 7):
+    if args.only == "forward" and args.config in (5, 6, 7, 8):
         raise SystemExit("--only forward applies to the single-layer workloads 1-4")
-    if args.config == 7:
+    if args.config in (7, 8):
         return run_voxel_bench(args, dev)
     b = (StackBench(dev) if args.config == 5 else BlockBench(args.config, dev) if args.config == 6
          else SingleLayer(args.config, dev))

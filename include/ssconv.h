@@ -259,6 +259,33 @@ int ssconv_voxelize(const float* points, const int32_t* batch, const float* feat
                     int32_t* coords_out, float* feats_out, int32_t* point_row, int64_t* n_sites /*host*/,
                     hipStream_t stream);
 
+/* ---- Wigner-D matrices (host; Sec. 3.1, Eq. 4-5) ----------------------------
+ * D (host [(2l+1)^2], row-major) = D^l(rot) of the real harmonic basis used
+ * throughout (Y^l(rot u) = D^l(rot) Y^l(u)), 0 <= l <= SSCONV_MAX_L; rot is a
+ * host [9] row-major rotation.  A field of order l of a feature transforms as
+ * f -> D^l(rot) f.  Errors: E_INVALID. */
+int ssconv_wigner_d(int l, const double* rot /*host [9]*/, double* D /*host*/);
+
+/* ---- Feature-Steering (Sec. 4.1) -------------------------------------------
+ * Moves a sparse tensor (coords [n, 4], feats [n, C] fp32, C = channels of
+ * `fields`) by the rigid motion p -> rot p + trans (rot: host [9] row-major
+ * rotation, trans: host [3], world units): every field of order l is rotated
+ * by its Wigner-D matrix D^l(rot) of the real harmonic basis (the block-diagonal
+ * rho(rot) of Eq. 5, computed on the host by an exact quadrature), every site
+ * is taken to the centre of its cell origin + (x + 1/2) voxel, moved, and the
+ * moved points are re-voxelised exactly as ssconv_voxelize does (grid, nbatch,
+ * dropping, lexicographic sites, averages of merged sites in a fixed order).
+ * The centre and the moved point are computed in fp32 with every product and
+ * sum rounded to nearest in the order ((r0 p0 + r1 p1) + r2 p2) + t.
+ * Outputs as ssconv_voxelize: coords_out [n, 4], feats_out [n, C],
+ * site_row [n] (new row of each input site or -1; may be NULL), *n_sites.
+ * Errors: E_INVALID (fields, rot not orthonormal with det +1, non-finite
+ * trans, null buffers), E_BOUNDS, E_NOMEM, E_HIP. */
+int ssconv_steer(const int32_t* coords, const float* feats, int64_t n, const ssconv_fields* fields /*host*/,
+                 const double* rot /*host [9]*/, const double* trans /*host [3]*/, const float* origin /*host [3]*/,
+                 float voxel, const int32_t* grid /*host [3]*/, int nbatch, int32_t* coords_out, float* feats_out,
+                 int32_t* site_row, int64_t* n_sites /*host*/, hipStream_t stream);
+
 /* ---- test hooks --------------------------------------------------------
  * Forces failure paths from the host so they can be tested without faulting
  * a device: option 1 = hash capacity (slots) used by the next rule book builds

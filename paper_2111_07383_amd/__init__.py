@@ -26,6 +26,8 @@ from .binding import (  # noqa: F401
     norm_forward,
     pool_backward,
     pool_forward,
+    steer,
     synth_kernel,
     voxelize,
+    wigner_d,
 )

@@ -330,6 +330,40 @@ def voxelize(points: torch.Tensor, feats: Optional[torch.Tensor] = None, batch: 
     return coords[:k], (fo[:k] if fo is not None else None), rows
 
 
+def wigner_d(l: int, rot) -> np.ndarray:
+    """D^l(rot) of the real harmonic basis (host computation)."""
+    d = 2 * int(l) + 1
+    r = (ctypes.c_double * 9)(*[float(v) for v in np.asarray(rot, np.float64).reshape(9)])
+    out = (ctypes.c_double * (d * d))()
+    check(lib().ssconv_wigner_d(int(l), r, out), "ssconv_wigner_d")
+    return np.array(out[:], np.float64).reshape(d, d)
+
+
+def steer(coords: torch.Tensor, feats: torch.Tensor, fields: FieldList, rot, trans, nbatch: int = 1,
+          origin=(0.0, 0.0, 0.0), voxel: float = 1.0, grid=64, stream=None):
+    """Feature-Steering (Sec. 4.1) by p -> rot p + trans.  Returns (coords' [m, 4] int32,
+    feats' [m, C] fp32, site_row [n] int32)."""
+    _need(coords, "coords", torch.int32)
+    _need(feats, "feats", torch.float32)
+    n = coords.shape[0]
+    C = n_channels(fields)
+    if coords.dim() != 2 or coords.shape[1] != 4 or tuple(feats.shape) != (n, C):
+        raise ValueError(f"coords must be [n, 4] and feats [n, {C}]")
+    f = make_fields(fields)
+    r = (ctypes.c_double * 9)(*[float(v) for v in np.asarray(rot, np.float64).reshape(9)])
+    t = (ctypes.c_double * 3)(*[float(v) for v in np.asarray(trans, np.float64).reshape(3)])
+    g = (c_int * 3)(*([int(grid)] * 3 if np.isscalar(grid) else [int(v) for v in grid]))
+    o = (c_float * 3)(*[float(v) for v in origin])
+    co = torch.empty((n, 4), dtype=torch.int32, device=coords.device)
+    fo = torch.empty((n, C), dtype=torch.float32, device=coords.device)
+    rows = torch.empty((n,), dtype=torch.int32, device=coords.device)
+    m = c_int64()
+    check(lib().ssconv_steer(_ptr(coords), _ptr(feats), n, byref(f), r, t, o, float(voxel), g, int(nbatch), _ptr(co),
+                             _ptr(fo), _ptr(rows), byref(m), _stream(stream)), "ssconv_steer")
+    k = m.value
+    return co[:k], fo[:k], rows
+
+
 def debug_set(option: int, value: int) -> None:
     check(lib().ssconv_debug_set(int(option), int(value)), "ssconv_debug_set")
 

@@ -85,3 +85,20 @@ def test_kernel_timing_without_timed_call(abi):
     with pytest.raises(abi.SSConvError) as e:       # nothing timed on this thread: no device call made
         B.debug_kernel_ms()
     assert e.value.code == abi.E_INVALID
+
+
+def test_wigner_d_matches_oracle(abi):
+    """The library's Wigner-D (projection by an exact sphere quadrature) against the oracle's
+    (least squares over random directions) for random rotations and every order up to 4."""
+    from oracle import sh
+    from paper_2111_07383_amd.binding import wigner_d
+    rng = np.random.default_rng(11)
+    for k in range(6):
+        q = rng.standard_normal(4)
+        q /= np.linalg.norm(q)
+        w, x, y, z = q
+        R = np.array([[1 - 2 * (y * y + z * z), 2 * (x * y - z * w), 2 * (x * z + y * w)],
+                      [2 * (x * y + z * w), 1 - 2 * (x * x + z * z), 2 * (y * z - x * w)],
+                      [2 * (x * z - y * w), 2 * (y * z + x * w), 1 - 2 * (x * x + y * y)]])
+        for l in range(5):
+            np.testing.assert_allclose(wigner_d(l, R), sh.wigner_d(l, R), atol=1e-12)

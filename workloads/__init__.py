@@ -11,6 +11,7 @@ from .gen import (  # noqa: F401
     make_features,
     make_coeffs,
     make_grad,
+    make_motion,
     make_point_cloud,
     round_bf16,
     shuffle_rows,

@@ -113,6 +113,13 @@ CONFIGS = {
     7: WorkloadSpec(
         7, "points64_b32_voxelise_rgb1", 64, 32, "f32", (),
         geometry="points", params=dict(extent=(8.0, 24.0), n_points=16384)),
+    # Feature-Steering (Sec. 4.1) of a backbone feature map: the ellipsoid scene recipe of
+    # workload 2 (its own seed) with 104 channels of orders 0, 1, 2, moved by a seeded random
+    # rotation about the grid centre and a translation of up to 2 voxels, then re-voxelised.
+    8: WorkloadSpec(
+        8, "steer_ellipsoids64_104", 64, 1, "f32",
+        (LayerSpec(5, 1, True, F_104, F_104, shells=(0.0, 1.0, 2.0), jmax=2),),
+        geometry="ellipsoids", params=dict(n=4, axes=(8.0, 24.0), centre=(24.0, 40.0), tau=0.75)),
 }
 
 

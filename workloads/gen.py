@@ -286,6 +286,16 @@ def make_point_cloud(spec: WorkloadSpec):
     return points, np.concatenate(bat), feats
 
 
+def make_motion(spec: WorkloadSpec):
+    """A seeded rigid motion (rotation R [3, 3], translation t [3]) that turns the grid about its
+    centre (uniform random rotation) and shifts it by U(-2, 2) voxels per axis."""
+    rng = transform_rng(spec)
+    R = random_rotation(rng)
+    c = np.full(3, spec.grid / 2.0)
+    t = c - R @ c + rng.uniform(-2.0, 2.0, 3)
+    return R, t
+
+
 def shuffle_rows(seed: int, n: int) -> np.ndarray:
     """A seeded permutation of n rows (used to test row-order independence)."""
     return np.random.default_rng(seed).permutation(n)
