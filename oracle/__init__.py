@@ -16,6 +16,8 @@ Modules
     voxel     point-cloud voxelisation with per-cell feature averaging (Sec. 4.1)
     steer     Feature-Steering: Wigner-D rotation of the fields, rigid motion of the
               site centres, re-voxelisation with averaging of merged sites (Sec. 4.1)
+    interp    Tensor-to-Point: trilinear interpolation of the zero-filled site grid at
+              points, and its adjoint (Sec. 4.1)
 
 Readings of the paper that it takes (all pinned by invariants in tests/):
     real SH without Condon-Shortley phase, components ordered m = -l..l;
