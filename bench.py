@@ -11,7 +11,7 @@ Prints ONE JSON line: throughput in M active output sites/s, the roofline of
 the dominant kernel (timed with events on the stream it runs on) and the CPU
 oracle timed on a bounded sample on this host.
 
-    python bench.py [--steps K] [--warmup W] [--config {1..8}] [--no-cpu-baseline]
+    python bench.py [--steps K] [--warmup W] [--config {1..9}] [--no-cpu-baseline]
 """
 import argparse
 import json
@@ -149,9 +149,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload index 1..8 (default: the 64^3 5x5x5 layer; 6: the "
+    ap.add_argument("--config", type=int, default=2, help="workload index 1..9 (default: the 64^3 5x5x5 layer; 6: the "
                     "downsampling block conv + norm + gate + pooling; 7: input voxelisation; "
-                    "8: Feature-Steering)")
+                    "8: Feature-Steering; 9: Tensor-to-Point)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work to aim for")
     ap.add_argument("--only", choices=["step", "forward"], default="step",
@@ -540,6 +540,57 @@ class SteerBench:
                         "includes its one synchronisation"}
 
 
+class InterpBench:
+    """Tensor-to-Point (workload 9, Sec. 4.1): one step = ssconv_interpolate and
+    ssconv_interpolate_backward of the 64^3 104-channel map at 4 points per site, over the map's
+    rule-book hash (built once per map, outside the step)."""
+
+    def __init__(self, i, dev):
+        import torch
+        import paper_2111_07383_amd as P
+        from workloads import CONFIGS
+        from workloads.gen import make_coords, make_features, make_query_points
+        self.P, self.torch = P, torch
+        self.spec = CONFIGS[i]
+        coords = make_coords(self.spec)
+        self.rb = P.Rulebook(torch.from_numpy(coords).to(dev), self.spec.grid, 1, 1, True)
+        self.feats = torch.from_numpy(make_features(self.spec, len(coords), self.spec.layers[0].cin)).to(dev)
+        pts, b = make_query_points(self.spec, coords)
+        self.points = torch.from_numpy(pts).to(dev)
+        self.batch = torch.from_numpy(b).to(dev)
+        g = torch.Generator(dev).manual_seed(0)
+        self.grad = torch.randn((len(pts), self.feats.shape[1]), device=dev, generator=g)
+        self.events = None
+        self.n_sites = len(pts)
+
+    def step(self):
+        P, torch = self.P, self.torch
+        if self.events is not None:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+        out = P.interpolate(self.rb, self.feats, self.points, self.batch)
+        P.interpolate_backward(self.rb, self.grad, self.points, self.batch)
+        if self.events is not None:
+            e1.record()
+            self.events.append((e0, e1))
+        return out
+
+    def sites(self):
+        return self.n_sites
+
+    def algorithmic_bytes(self):
+        """Forward: points (12 B) and batch (4 B) read, the 8 corner slots of the hash (8 B each),
+        site features read once (n C 4 B), point features written (m C 4 B); backward: the same
+        lookups, point gradients read once, site gradients written once."""
+        m, C, n = int(self.points.shape[0]), int(self.feats.shape[1]), int(self.feats.shape[0])
+        return 2 * (m * (16 + 64) + (n + m) * C * 4)
+
+    def config(self):
+        return {"workload": self.spec.name, "grid": self.spec.grid, "sites": int(self.feats.shape[0]),
+                "points": int(self.points.shape[0]), "channels": int(self.feats.shape[1]), "n_out": self.n_sites,
+                "step": "interpolate + interpolate_backward at every point (rule book of the map prebuilt)"}
+
+
 # ---------------------------------------------------------------------------
 # CPU oracle baseline (bounded sample of the same workload)
 # ---------------------------------------------------------------------------
@@ -617,6 +668,8 @@ def cpu_baseline_block(i):
 
 
 def step_text(spec):
+    if spec.index == 9:
+        return "Tensor-to-Point interpolation and its adjoint at 4 points per site of the 64^3 104-channel map"
     if spec.index == 8:
         return "Feature-Steering of the 64^3 104-channel map (Wigner-D rotation, moved centres, re-voxelisation)"
     if spec.index == 7:
@@ -657,6 +710,25 @@ def cpu_baseline_steer(i):
     return {"value": len(c) / dt / 1e6, "unit": "M active output sites/s", "cores": 1, "kind": "oracle",
             "sample": f"{spec.name}: all {len(coords)} sites -> {len(c)} (numpy Wigner-D product, fp32 centres, "
                       f"dict averaging, 1 thread), {dt:.2f} s"}
+
+
+def cpu_baseline_interp(i):
+    from oracle import interp as oi
+    from workloads import CONFIGS
+    from workloads.gen import make_coords, make_features, make_query_points
+    spec = CONFIGS[i]
+    coords = make_coords(spec)
+    feats = make_features(spec, len(coords), spec.layers[0].cin)
+    pts, b = make_query_points(spec, coords)
+    m = min(len(pts), 20000)
+    g = np.random.default_rng(0).standard_normal((m, feats.shape[1]))
+    t0 = time.perf_counter()
+    oi.interpolate(coords, feats, pts[:m], b[:m], (0.0, 0.0, 0.0), 1.0)
+    oi.interpolate_backward(coords, len(coords), pts[:m], b[:m], g, (0.0, 0.0, 0.0), 1.0)
+    dt = time.perf_counter() - t0
+    return {"value": m / dt / 1e6, "unit": "M active output sites/s", "cores": 1, "kind": "oracle",
+            "sample": f"{spec.name}: first {m} of {len(pts)} points, forward + backward (dict corner lookups, "
+                      f"1 thread), {dt:.1f} s"}
 
 
 def write_stats_summary(args):
@@ -780,7 +852,7 @@ def write_counter_summary(args):
 
 def run_voxel_bench(args, dev):
     import torch
-    b = VoxelBench(args.config, dev) if args.config == 7 else SteerBench(args.config, dev)
+    b = {7: VoxelBench, 8: SteerBench, 9: InterpBench}[args.config](args.config, dev)
     for _ in range(args.warmup):
         b.step()
     torch.cuda.synchronize()
@@ -797,14 +869,16 @@ def run_voxel_bench(args, dev):
     out = {"metric": METRIC, "value": value, "unit": "M active output sites/s", "n_gpus": 1, "steps": args.steps,
            "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "f32", "data": "synthetic", "config": b.config(),
-           "roofline": {"kernel": ("ssconv_voxelize" if args.config == 7 else "ssconv_steer") + " (all its launches)",
+           "roofline": {"kernel": {7: "ssconv_voxelize", 8: "ssconv_steer",
+                                   9: "ssconv_interpolate + _backward"}[args.config] + " (all their launches)",
                         "bound": "hbm", "achieved": achieved,
                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
                         "traffic_source": "not measured", "avg_launch_ms": ev_ms,
                         "algorithmic_bytes_per_launch": b.algorithmic_bytes()}}
     log(f"{b.spec.name}: {ms:.3f} ms/step, {value:.1f} M sites/s, {achieved:.0f} GB/s algorithmic")
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline_voxel(args.config) if args.config == 7 else cpu_baseline_steer(args.config)
+        out["cpu_baseline"] = {7: cpu_baseline_voxel, 8: cpu_baseline_steer, 9: cpu_baseline_interp}[args.config](
+            args.config)
     print(json.dumps(out), flush=True)
 
 
@@ -844,9 +918,9 @@ def main():
         import paper_2111_07383_amd as P
         P.debug_set(3, args.variant)
     log(f"setting up {spec.name}")
-    if args.only == "forward" and args.config in (5, 6, 7, 8):
+    if args.only == "forward" and args.config in (5, 6, 7, 8, 9):
         raise SystemExit("--only forward applies to the single-layer workloads 1-4")
-    if args.config in (7, 8):
+    if args.config in (7, 8, 9):
         return run_voxel_bench(args, dev)
     b = (StackBench(dev) if args.config == 5 else BlockBench(args.config, dev) if args.config == 6
          else SingleLayer(args.config, dev))

@@ -286,6 +286,28 @@ int ssconv_steer(const int32_t* coords, const float* feats, int64_t n, const ssc
                  float voxel, const int32_t* grid /*host [3]*/, int nbatch, int32_t* coords_out, float* feats_out,
                  int32_t* site_row, int64_t* n_sites /*host*/, hipStream_t stream);
 
+/* ---- Tensor-to-Point interpolation (Sec. 4.1) --------------------------------
+ * rb: any rule book built on the sites (its input hash table and grid are
+ * used); feats [n_in, channels] fp32 in its input rows.  points [m, 3] fp32,
+ * batch [m] int32 or NULL (all 0), origin host [3], voxel > 0.
+ * The features live at the cell centres origin + (x + 1/2) voxel and are zero
+ * off the active sites; out [m, channels] = the trilinear interpolant of that
+ * zero-filled grid at each point: u = (p - origin)/voxel - 1/2 in fp32,
+ * x0 = floor(u), corner x0 + c weighted prod_a (c_a ? w_a : 1 - w_a) with
+ * w = u - x0, corners inactive or outside the grid (or of another batch
+ * entry) contributing nothing, corners added in the order 4cx + 2cy + cz.
+ * Backward: grad_feats [n_in, channels] = the exact adjoint (every point
+ * scatters weight * grad to its corners), summed per site in (point, corner)
+ * order (deterministic, every row written).  Temporaries come from the device
+ * memory cache.  Errors: E_INVALID (m >= 2^28, bad origin / voxel, null
+ * buffers), E_NOMEM, E_HIP. */
+int ssconv_interpolate(ssconv_rulebook_t rb, const float* feats, int channels, const float* points,
+                       const int32_t* batch, int64_t m, const float* origin /*host [3]*/, float voxel, float* out,
+                       hipStream_t stream);
+int ssconv_interpolate_backward(ssconv_rulebook_t rb, const float* grad, int channels, const float* points,
+                                const int32_t* batch, int64_t m, const float* origin /*host [3]*/, float voxel,
+                                float* grad_feats, hipStream_t stream);
+
 /* ---- test hooks --------------------------------------------------------
  * Forces failure paths from the host so they can be tested without faulting
  * a device: option 1 = hash capacity (slots) used by the next rule book builds

@@ -21,7 +21,8 @@ def point_corners(points: np.ndarray, origin, voxel: float):
     o = np.asarray(origin, np.float32).reshape(3)
     u = (p - o) / np.float32(voxel) - np.float32(0.5)
     x0 = np.floor(u)
-    return x0.astype(np.int64), (u.astype(np.float64) - x0.astype(np.float64))
+    with np.errstate(invalid="ignore"):      # non-finite points: their corners are never read
+        return np.where(np.isfinite(x0), x0, 0).astype(np.int64), (u.astype(np.float64) - x0.astype(np.float64))
 
 
 def corner_table(coords, points, batch, origin, voxel: float):

@@ -19,6 +19,8 @@ from .binding import (  # noqa: F401
     forward,
     gate_backward,
     gate_forward,
+    interpolate,
+    interpolate_backward,
     layer_desc,
     make_fields,
     n_channels,

@@ -61,6 +61,10 @@ SIGNATURES = {
     "ssconv_steer": (c_int, [c_void_p, c_void_p, c_int64, POINTER(Fields), POINTER(c_double), POINTER(c_double),
                              POINTER(c_float), c_float, POINTER(c_int), c_int, c_void_p, c_void_p, c_void_p,
                              POINTER(c_int64), c_void_p]),
+    "ssconv_interpolate": (c_int, [c_void_p, c_void_p, c_int, c_void_p, c_void_p, c_int64, POINTER(c_float), c_float,
+                                   c_void_p, c_void_p]),
+    "ssconv_interpolate_backward": (c_int, [c_void_p, c_void_p, c_int, c_void_p, c_void_p, c_int64, POINTER(c_float),
+                                            c_float, c_void_p, c_void_p]),
     "ssconv_debug_set": (c_int, [c_int, c_int64]),
     "ssconv_debug_kernel_ms": (c_int, [POINTER(c_int64), POINTER(c_float)]),
 }

@@ -364,6 +364,45 @@ def steer(coords: torch.Tensor, feats: torch.Tensor, fields: FieldList, rot, tra
     return co[:k], fo[:k], rows
 
 
+def _interp_args(rb, points, batch, C):
+    _need(points, "points", torch.float32)
+    if points.dim() != 2 or points.shape[1] != 3:
+        raise ValueError("points must be [m, 3]")
+    if batch is not None:
+        _need(batch, "batch", torch.int32, (points.shape[0],))
+    if C < 1:
+        raise ValueError("channels must be positive")
+
+
+def interpolate(rb: Rulebook, feats: torch.Tensor, points: torch.Tensor, batch: Optional[torch.Tensor] = None,
+                origin=(0.0, 0.0, 0.0), voxel: float = 1.0, stream=None) -> torch.Tensor:
+    """Tensor-to-Point (Sec. 4.1): trilinear interpolation of the sites' features at points."""
+    _need(feats, "feats", torch.float32)
+    if feats.dim() != 2 or feats.shape[0] != rb.n_in:
+        raise ValueError(f"feats must be [{rb.n_in}, C]")
+    C = feats.shape[1]
+    _interp_args(rb, points, batch, C)
+    out = torch.empty((points.shape[0], C), dtype=torch.float32, device=points.device)
+    o = (c_float * 3)(*[float(v) for v in origin])
+    check(lib().ssconv_interpolate(rb.handle, _ptr(feats), C, _ptr(points), _ptr(batch), points.shape[0], o,
+                                   float(voxel), _ptr(out), _stream(stream)), "ssconv_interpolate")
+    return out
+
+
+def interpolate_backward(rb: Rulebook, grad: torch.Tensor, points: torch.Tensor, batch: Optional[torch.Tensor] = None,
+                         origin=(0.0, 0.0, 0.0), voxel: float = 1.0, stream=None) -> torch.Tensor:
+    _need(grad, "grad", torch.float32)
+    if grad.dim() != 2 or grad.shape[0] != points.shape[0]:
+        raise ValueError("grad must be [m, C]")
+    C = grad.shape[1]
+    _interp_args(rb, points, batch, C)
+    gf = torch.empty((rb.n_in, C), dtype=torch.float32, device=points.device)
+    o = (c_float * 3)(*[float(v) for v in origin])
+    check(lib().ssconv_interpolate_backward(rb.handle, _ptr(grad), C, _ptr(points), _ptr(batch), points.shape[0], o,
+                                            float(voxel), _ptr(gf), _stream(stream)), "ssconv_interpolate_backward")
+    return gf
+
+
 def debug_set(option: int, value: int) -> None:
     check(lib().ssconv_debug_set(int(option), int(value)), "ssconv_debug_set")
 

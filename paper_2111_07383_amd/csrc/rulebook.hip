@@ -14,38 +14,14 @@
 // and emitted in lexicographic (b, x, y, z) order by a scan of popcounts.
 #include <algorithm>
 
+#include "hash.hpp"
 #include "scan.hpp"
 
 namespace ssconv {
 
 namespace {
 
-constexpr uint64_t kEmpty = ~0ull;
 constexpr int kFlagBounds = 1, kFlagDup = 2, kFlagFull = 4;
-
-__device__ __forceinline__ uint32_t mix32(uint32_t h) {
-  h ^= h >> 16;
-  h *= 0x85ebca6bu;
-  h ^= h >> 13;
-  h *= 0xc2b2ae35u;
-  h ^= h >> 16;
-  return h;
-}
-
-__device__ __forceinline__ uint32_t site_key(int b, int x, int y, int z, int g0, int g1, int g2) {
-  return (uint32_t)((((uint64_t)b * g0 + x) * g1 + y) * g2 + z);
-}
-
-__device__ __forceinline__ int hash_find(const uint64_t* __restrict__ slots, uint64_t mask, uint32_t key) {
-  uint64_t pos = mix32(key) & mask;
-  for (uint64_t probe = 0; probe <= mask; ++probe) {
-    uint64_t v = slots[pos];
-    if (v == kEmpty) return -1;
-    if ((uint32_t)(v >> 32) == key) return (int)(uint32_t)v;
-    pos = (pos + 1) & mask;
-  }
-  return -1;
-}
 
 __global__ void validate_kernel(const int32_t* __restrict__ c, int64_t n, int g0, int g1, int g2,
                                 int* __restrict__ flags, int* __restrict__ maxb) {

@@ -12,6 +12,7 @@
 #include <algorithm>
 #include <cmath>
 
+#include "bucket_sort.hpp"
 #include "scan.hpp"
 
 namespace ssconv {
@@ -87,47 +88,6 @@ __global__ void vox_fill_kernel(const int32_t* __restrict__ point_row, int64_t n
   idx[start[r] + atomicAdd(&fill[r], 1)] = (int32_t)i;
 }
 
-constexpr int kRegSort = 16;  // buckets up to this size are sorted in registers
-
-// One thread per site: its bucket of point indices is put in ascending order, in registers for up
-// to kRegSort points (odd-even transposition over padded slots), else by an insertion sort in
-// place.  Cells hold few points at the paper's resolution; a bucket of m points costs O(m^2)
-// only above kRegSort.
-__global__ void vox_sort_kernel(const int64_t* __restrict__ n_rows, const int64_t* __restrict__ start,
-                                const int32_t* __restrict__ cnt, int32_t* __restrict__ idx) {
-  const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (r >= *n_rows) return;
-  int32_t* a = idx + start[r];
-  const int m = cnt[r];
-  if (m <= 1) return;
-  if (m <= kRegSort) {
-    int32_t v[kRegSort];
-#pragma unroll
-    for (int j = 0; j < kRegSort; ++j) v[j] = j < m ? a[j] : 0x7fffffff;  // padding sorts last
-#pragma unroll
-    for (int round = 0; round < kRegSort; ++round) {
-#pragma unroll
-      for (int j = round & 1; j + 1 < kRegSort; j += 2) {
-        const int32_t lo = min(v[j], v[j + 1]), hi = max(v[j], v[j + 1]);
-        v[j] = lo;
-        v[j + 1] = hi;
-      }
-    }
-#pragma unroll
-    for (int j = 0; j < kRegSort; ++j)
-      if (j < m) a[j] = v[j];
-    return;
-  }
-  for (int j = 1; j < m; ++j) {
-    const int32_t v = a[j];
-    int k = j - 1;
-    while (k >= 0 && a[k] > v) {
-      a[k + 1] = a[k];
-      --k;
-    }
-    a[k + 1] = v;
-  }
-}
 
 // feats_out[r][c] = (sum over the sorted bucket of feats[i][c], in point order) / count; one
 // thread per (site, channel), so the threads of a site read its points' rows together.
@@ -208,7 +168,7 @@ extern "C" int ssconv_voxelize(const float* points, const int32_t* batch, const 
       // rows past the site count have zero counts, so the scan over n rows is exact
       SSC_TRY(exclusive_scan(cnt, n, start, d_pts, stmp, st));
       vox_fill_kernel<<<cdiv(n, 256), 256, 0, st>>>(prow, n, start, fillc, idx);
-      vox_sort_kernel<<<cdiv(n, 256), 256, 0, st>>>(d_sites, start, cnt, idx);
+      bucket_sort_kernel<<<cdiv(n, 4), 256, 0, st>>>(d_sites, 0, start, cnt, idx);
       vox_mean_kernel<<<cdiv(n * channels, 256), 256, 0, st>>>(feats, channels, d_sites, start, cnt, idx, feats_out);
     }
     SSC_HIP(hipGetLastError());

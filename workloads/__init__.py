@@ -13,6 +13,7 @@ from .gen import (  # noqa: F401
     make_grad,
     make_motion,
     make_point_cloud,
+    make_query_points,
     round_bf16,
     shuffle_rows,
 )

@@ -120,6 +120,12 @@ CONFIGS = {
         8, "steer_ellipsoids64_104", 64, 1, "f32",
         (LayerSpec(5, 1, True, F_104, F_104, shells=(0.0, 1.0, 2.0), jmax=2),),
         geometry="ellipsoids", params=dict(n=4, axes=(8.0, 24.0), centre=(24.0, 40.0), tau=0.75)),
+    # Tensor-to-Point (Sec. 4.1): the feature map of workload 8's recipe (its own seed) read at 4
+    # query points per site, each its cell centre plus U(-1, 1) voxels per axis.
+    9: WorkloadSpec(
+        9, "interp_ellipsoids64_104_4pps", 64, 1, "f32",
+        (LayerSpec(5, 1, True, F_104, F_104, shells=(0.0, 1.0, 2.0), jmax=2),),
+        geometry="ellipsoids", params=dict(n=4, axes=(8.0, 24.0), centre=(24.0, 40.0), tau=0.75, per_site=4)),
 }
 
 

@@ -296,6 +296,16 @@ def make_motion(spec: WorkloadSpec):
     return R, t
 
 
+def make_query_points(spec: WorkloadSpec, coords: np.ndarray):
+    """params["per_site"] points per site: its cell centre (x + 1/2, voxel units, origin 0) plus
+    U(-1, 1) per axis; returns (points float32 [m, 3], batch int32 [m])."""
+    rng = transform_rng(spec)
+    k = spec.params["per_site"]
+    c = np.repeat(np.asarray(coords, np.int64), k, axis=0)
+    pts = (c[:, 1:] + 0.5 + rng.uniform(-1.0, 1.0, (len(c), 3))).astype(np.float32)
+    return pts, c[:, 0].astype(np.int32)
+
+
 def shuffle_rows(seed: int, n: int) -> np.ndarray:
     """A seeded permutation of n rows (used to test row-order independence)."""
     return np.random.default_rng(seed).permutation(n)
