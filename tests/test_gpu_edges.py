@@ -188,3 +188,41 @@ def test_device_memory_cache():
     torch.testing.assert_close(rb.neighbours(), ref.neighbours(), rtol=0, atol=0)
     rb.close()
     ref.close()
+
+
+@pytest.mark.parametrize("ksize,stride,sub", [(3, 1, True), (5, 1, True), (3, 2, False), (1, 1, True)])
+@pytest.mark.parametrize("fields_out", [((0, 4), (1, 3), (2, 1)), ((0, 4), (1, 2), (2, 2))])
+def test_pair_path_ragged(ksize, stride, sub, fields_out):
+    """The pair-list path forced on small layers: 12 input channels; 18 outputs (a partial column
+    block and the scalar per-row sum) or 20 (both directions on the pair path), several batch
+    entries, against the oracle."""
+    spec = LayerSpec(ksize, stride, sub, ((0, 4), (1, 1), (2, 1)), fields_out,
+                     shells=tuple(float(m) for m in range(ksize // 2 + 1)))
+    grid = 12
+    c = _coords(ksize * 11 + stride, 400, grid, batch=3)
+    lay = oc.Layer(spec)
+    rng = np.random.default_rng(ksize + spec.cout)
+    w = rng.standard_normal(lay.n_coeff).astype(np.float32)
+    f = rng.standard_normal((len(c), spec.cin)).astype(np.float32)
+    co = orb.output_sites(c, grid, ksize, stride, sub)
+    R = orb.rulebook(c, co, ksize, stride)
+    kap = lay.kappa(w)
+    g = rng.standard_normal((len(co), spec.cout)).astype(np.float32)
+    want = oc.forward(f, R, kap, len(co))
+    d_in = oc.grad_feats(g, R, kap, len(c))
+    dw = oc.synth_adjoint(spec, lay.basis, oc.grad_kappa(f, g, R, kap.shape))
+    desc = P.layer_desc(spec)
+    basis = torch.from_numpy(P.basis_build(desc)).to(DEV)
+    rb = P.Rulebook(torch.from_numpy(c).to(DEV), grid, ksize, stride, sub)
+    W = P.synth_kernel(desc, basis, torch.from_numpy(w).to(DEV))
+    ft = torch.from_numpy(f).to(DEV)
+    P.debug_set(3, 9)
+    try:
+        out = P.forward(ft, rb, W).cpu().numpy()
+        gf, gc = P.backward(ft, torch.from_numpy(g).to(DEV), rb, W, desc, basis)
+    finally:
+        P.debug_set(3, 0)
+    errs = rel_err(out, want), rel_err(gf.cpu().numpy(), d_in), rel_err(gc.cpu().numpy(), dw)
+    print(f"pair path k{ksize} s{stride} cout {spec.cout}: {errs}", flush=True)
+    assert max(errs) < 1e-4
+    rb.close()
