@@ -323,7 +323,10 @@ int ssconv_interpolate_backward(ssconv_rulebook_t rb, const float* grad, int cha
  * partials added in split order), which it otherwise does only when its tiles
  * leave compute units idle; 9 = fp32 convolutions take the pair-list path
  * (one GEMM per offset over R_s, then a per-row sum in offset order) wherever
- * it applies; 10 = never take it, which a cost model otherwise decides; results
+ * it applies; 10 = never take it, which a cost model otherwise decides;
+ * 11 = run the coefficient gradient of ssconv_backward on the caller's
+ * stream instead of forking it onto the library's second stream next to a
+ * pair-list feature gradient; results
  * agree within the dtype's tolerance for every value); option 4 = kernel
  * timing: a nonzero value switches it on and clears this thread's log, 0
  * switches it off; while on, every gather-GEMM kernel launch (the one of

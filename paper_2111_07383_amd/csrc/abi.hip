@@ -56,16 +56,33 @@ extern "C" int ssconv_backward(const void* feats, const void* grad_out, ssconv_d
       return fail(SSCONV_E_INVALID, "basis descriptor does not match cin/cout/ksize");
   }
   char* ws = (char*)workspace;
-  if (grad_feats) {
-    if (rb->n_out == 0 && rb->n_in > 0)
-      SSC_HIP(hipMemsetAsync(grad_feats, 0, (size_t)rb->n_in * cin * dtype_bytes(dtype), stream));
-    else
-      SSC_TRY(conv_backward_feats(grad_out, dtype, cin, cout, rb, W, grad_feats, ws, L, stream));
-  }
+  // The coefficient gradient (kernel gradient, its reduction, the synthesis adjoint) does not
+  // depend on the feature gradient.  When the feature gradient takes the pair-list path (a chain
+  // of small launches) the coefficient gradient runs on the library's second stream, forked from
+  // and joined back to the caller's, so the two overlap (disjoint workspace regions).  Next to
+  // the output-stationary gather kernels it is not forked: measured, the bf16 gather and the
+  // kernel gradient slow each other down (C4 step 1.49 -> 1.56 ms), and the fp32 gain is 1%.
+  // Kernel-selection override 11 switches the fork off.
+  hipStream_t dw_stream = stream;
+  const bool fork = grad_feats && grad_coeffs && rb->n_out > 0 && L.pair_feats && debug_gather_variant() != 11;
+  if (fork) SSC_TRY(aux_fork(stream, &dw_stream));
+  int rc = SSCONV_OK;
   if (grad_coeffs) {
     float* dW = nullptr;
-    SSC_TRY(conv_backward_dw(feats, grad_out, dtype, cin, cout, rb, sa.out, sa.in, ws, L, &dW, stream));
-    SSC_TRY(launch_synth_adjoint(sa, basis, dW, grad_coeffs, stream));
+    rc = conv_backward_dw(feats, grad_out, dtype, cin, cout, rb, sa.out, sa.in, ws, L, &dW, dw_stream);
+    if (rc == SSCONV_OK) rc = launch_synth_adjoint(sa, basis, dW, grad_coeffs, dw_stream);
   }
-  return SSCONV_OK;
+  if (rc == SSCONV_OK && grad_feats) {
+    if (rb->n_out == 0 && rb->n_in > 0) {
+      if (hipMemsetAsync(grad_feats, 0, (size_t)rb->n_in * cin * dtype_bytes(dtype), stream) != hipSuccess)
+        rc = fail(SSCONV_E_HIP, "hipMemsetAsync failed");
+    } else {
+      rc = conv_backward_feats(grad_out, dtype, cin, cout, rb, W, grad_feats, ws, L, stream);
+    }
+  }
+  if (fork) {
+    const int jr = aux_join(stream, dw_stream);  // always joined, so nothing stays pending on the side stream
+    if (rc == SSCONV_OK) rc = jr;
+  }
+  return rc;
 }

@@ -275,3 +275,44 @@ extern "C" int ssconv_debug_kernel_ms(int64_t* count, float* total_ms) {
   *total_ms = (float)sum;
   return SSCONV_OK;
 }
+
+namespace ssconv {
+
+// A second stream per device (default priority, non-blocking) and a pair of events per calling
+// thread, for work the library forks off the caller's stream and joins back before returning.
+namespace {
+std::mutex g_aux_mu;
+hipStream_t g_aux[64] = {};
+struct AuxEvents {
+  hipEvent_t fork = nullptr, join = nullptr;
+};
+thread_local AuxEvents g_aux_ev[64];
+}  // namespace
+
+int aux_fork(hipStream_t caller, hipStream_t* side) {
+  int dev = 0;
+  SSC_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return fail(SSCONV_E_INVALID, "device index %d out of range", dev);
+  {
+    std::lock_guard<std::mutex> lk(g_aux_mu);
+    if (!g_aux[dev]) SSC_HIP(hipStreamCreateWithFlags(&g_aux[dev], hipStreamNonBlocking));
+  }
+  AuxEvents& e = g_aux_ev[dev];
+  if (!e.fork) SSC_HIP(hipEventCreateWithFlags(&e.fork, hipEventDisableTiming));
+  if (!e.join) SSC_HIP(hipEventCreateWithFlags(&e.join, hipEventDisableTiming));
+  SSC_HIP(hipEventRecord(e.fork, caller));
+  SSC_HIP(hipStreamWaitEvent(g_aux[dev], e.fork, 0));
+  *side = g_aux[dev];
+  return SSCONV_OK;
+}
+
+int aux_join(hipStream_t caller, hipStream_t side) {
+  int dev = 0;
+  SSC_HIP(hipGetDevice(&dev));
+  AuxEvents& e = g_aux_ev[dev];
+  SSC_HIP(hipEventRecord(e.join, side));
+  SSC_HIP(hipStreamWaitEvent(caller, e.join, 0));
+  return SSCONV_OK;
+}
+
+}  // namespace ssconv

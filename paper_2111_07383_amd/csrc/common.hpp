@@ -38,6 +38,12 @@ int dev_alloc(void** p, size_t bytes, hipStream_t stream);
 void dev_free(void* p, hipStream_t stream);
 int64_t debug_hash_capacity();
 int64_t debug_gather_variant();
+// Fork / join of work onto the library's second stream of the current device: aux_fork makes
+// the side stream wait for everything queued on caller so far; aux_join makes caller wait for
+// everything queued on the side stream so far.  Not reentrant across overlapping forks of one
+// thread.
+int aux_fork(hipStream_t caller, hipStream_t* side);
+int aux_join(hipStream_t caller, hipStream_t side);
 // Kernel timing hook (ssconv_debug_set option 4): returns the event pair to record around the
 // next timed kernel, or false when timing is off.
 bool debug_timing_events(hipEvent_t* start, hipEvent_t* stop);

@@ -168,3 +168,18 @@ def test_pair_path_deterministic():
     a2, _ = P.backward(feats, g, rb, W, desc, basis, need_coeffs=False)
     assert torch.equal(o1, o2) and torch.equal(a1, a2)
     rb.close()
+
+
+def test_backward_fork_bit_identical():
+    """The coefficient gradient forked onto the library's second stream (next to a pair-list
+    feature gradient) gives the same bits as on the caller's stream (override 11)."""
+    L, dt, desc, basis, rb, W, feats = _layer_io(3)
+    g = torch.randn(rb.n_out, L.spec.cout, device=DEV, generator=torch.Generator(DEV).manual_seed(2))
+    a1, b1 = P.backward(feats, g, rb, W, desc, basis)
+    P.debug_set(3, 11)
+    try:
+        a2, b2 = P.backward(feats, g, rb, W, desc, basis)
+    finally:
+        P.debug_set(3, 0)
+    assert torch.equal(a1, a2) and torch.equal(b1, b2)
+    rb.close()
