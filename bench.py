@@ -365,8 +365,23 @@ class BlockBench:
         prb.close()
         self.grad = torch.from_numpy(make_grad(spec, self.n_out, P.n_channels(self.regular))).to(dev)
         self.events = None
+        from paper_2111_07383_amd.stack import LayerState
+        self.state = LayerState(self.L, self.desc, self.basis, self.coeffs, self.n_coeff, spec.grid)
+        self.blk = None
 
     def step(self):
+        """One block forward + backward as DownBlock runs it (pooling rule book on a side
+        stream, overlapping the convolution, Norm and gate)."""
+        if self.blk is None:
+            from paper_2111_07383_amd.stack import DownBlock
+            self.blk = DownBlock(self.state, self.torch.float32)
+        _, out = self.blk.forward(self.coords, self.feats)
+        self.blk.backward(self.grad)
+        return out
+
+    def phase_step(self):
+        """The same calls one after another on one stream, with an event between every two (for
+        the per-phase report)."""
         P, L, torch = self.P, self.L, self.torch
         ev = None
         if self.events is not None:
@@ -931,7 +946,7 @@ def main():
     log(f"warmup done ({args.warmup} steps); timing {args.steps} steps")
     import paper_2111_07383_amd as P
     P.debug_set(4, 1)                 # HIP events around each gather-GEMM launch, on its stream
-    if args.only == "step" and isinstance(b, (SingleLayer, BlockBench)):
+    if args.only == "step" and isinstance(b, SingleLayer):
         b.events = []                 # phase boundaries of every timed step (torch's stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -964,6 +979,11 @@ def main():
                        "launches_timed": n_timed, "algorithmic_flops_per_launch": flops_launch,
                        "kernel_ms_per_step": kern_ms / args.steps}
     log(f"gather-GEMM: {n_timed} launches, {avg_ms:.4f} ms avg, {achieved:.1f} TFLOP/s")
+    if isinstance(b, BlockBench):
+        b.events = []                 # per-phase times from extra sequential steps, after the timed ones
+        for _ in range(10):
+            b.phase_step()
+        torch.cuda.synchronize()
     if isinstance(b, (SingleLayer, BlockBench)) and b.events:
         out["phases"] = b.phase_report()
         ph = out["phases"]

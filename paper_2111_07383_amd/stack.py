@@ -144,9 +144,14 @@ class DownBlock:
         st = Stack.create([layer_spec], [coeffs], grid, device, dtype)
         return DownBlock(st.layers[0], dtype)
 
-    def forward(self, coords: torch.Tensor, feats: torch.Tensor):
-        """Returns (pooled coords, pooled features)."""
+    def forward(self, coords: torch.Tensor, feats: torch.Tensor, overlap: bool = True):
+        """Returns (pooled coords, pooled features).  The pooling rule book depends on the
+        coordinates only: with ``overlap`` it is built on a side stream after the convolution,
+        Norm and gate are queued, so its host synchronisations overlap them."""
         L, s = self.state, self.state.layer
+        main = torch.cuda.current_stream()
+        side = self._side() if overlap else main
+        side.wait_stream(main)
         for rb in (L.rb, self.pool_rb):
             if rb is not None:
                 rb.close()
@@ -156,8 +161,18 @@ class DownBlock:
         L.y = B.forward(feats, L.rb, L.W)
         self.z = B.norm_forward(s.fields_out, L.y, self.norm_eps)
         h = B.gate_forward(regular_fields(s), self.z) if s.gated else self.z
-        self.pool_rb = B.Rulebook(coords, L.grid, 2, 2, False)
-        return self.pool_rb.out_coords(), B.pool_forward(h, self.pool_rb)
+        with torch.cuda.stream(side):
+            self.pool_rb = B.Rulebook(coords, L.grid, 2, 2, False)
+            pc = self.pool_rb.out_coords()
+        main.wait_stream(side)
+        if side is not main:
+            pc.record_stream(main)
+        return pc, B.pool_forward(h, self.pool_rb)
+
+    def _side(self) -> torch.cuda.Stream:
+        if getattr(self, "_side_stream", None) is None:
+            self._side_stream = torch.cuda.Stream()   # default priority
+        return self._side_stream
 
     def backward(self, grad: torch.Tensor, need_input_grad: bool = True):
         """Returns (grad of the block input or None, grad_coeffs)."""
@@ -170,6 +185,8 @@ class DownBlock:
                           n_coeff=L.n_coeff)
 
     def close(self):
+        if getattr(self, "_side_stream", None) is not None:
+            self._side_stream.wait_stream(torch.cuda.current_stream())
         for rb in (self.state.rb, self.pool_rb):
             if rb is not None:
                 rb.close()
