@@ -28,29 +28,46 @@ __device__ __forceinline__ void write_pair_off(const int64_t* out, int64_t total
 constexpr int kSmallNT = 1024;
 constexpr int64_t kSmallMax = 32768;  // elements staged in LDS (128 KB)
 
-// The whole scan in one workgroup (n <= kSmallMax): the elements are staged in LDS with coalesced
-// loads, then thread t scans its contiguous run [t*per, (t+1)*per) from LDS.
+// The whole scan in one workgroup (n <= kSmallMax).  The elements are staged in LDS with coalesced
+// loads, at index i + i/32 so that the contiguous runs [t*per, (t+1)*per) that thread t sums and
+// rescans fall in different banks; each run's local exclusive offsets go back into LDS in place (a
+// run's sum stays below 2^32 for every caller: popcounts, and counts bounded by a block's rows or
+// the point count), and the results leave with coalesced stores of run base + local offset.
+__device__ __forceinline__ int lds_pad(int i) { return i + (i >> 5); }
+
 template <bool kPopc>
 __global__ __launch_bounds__(kSmallNT) void scan_small(const void* __restrict__ in, int64_t n,
                                                        int64_t* __restrict__ out, int64_t* __restrict__ total,
                                                        int K, int nblk, int64_t* __restrict__ pair_off) {
-  __shared__ int32_t sh[kSmallMax];
+  __shared__ uint32_t sh[kSmallMax + kSmallMax / 32];
+  __shared__ int64_t base[kSmallNT];
   const int t = threadIdx.x, nn = (int)n;
+  // 16-byte loads where the input allows, so a thread has all its loads in flight at once
+  const int n4 = (reinterpret_cast<uintptr_t>(in) & 15u) == 0 ? nn >> 2 : 0;
 #pragma unroll 8
-  for (int i = t; i < nn; i += kSmallNT) sh[i] = (int32_t)elem<kPopc>(in, i);
+  for (int q = t; q < n4; q += kSmallNT) {
+    const uint4 w = reinterpret_cast<const uint4*>(in)[q];
+    const uint32_t v[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) sh[lds_pad(4 * q + k)] = kPopc ? (uint32_t)__popc(v[k]) : v[k];
+  }
+  for (int i = 4 * n4 + t; i < nn; i += kSmallNT) sh[lds_pad(i)] = (uint32_t)elem<kPopc>(in, i);
   __syncthreads();
   const int per = (nn + kSmallNT - 1) / kSmallNT;
-  const int b0 = t * per;
+  const int b0 = t * per, e0 = min(b0 + per, nn);
   int64_t s = 0;
-  for (int i = 0; i < per; ++i)
-    if (b0 + i < nn) s += sh[b0 + i];
+  for (int i = b0; i < e0; ++i) s += sh[lds_pad(i)];
   int64_t tot;
-  int64_t run = block_excl_scan<kSmallNT>(s, &tot);
-  for (int i = 0; i < per; ++i)
-    if (b0 + i < nn) {
-      out[b0 + i] = run;
-      run += sh[b0 + i];
-    }
+  base[t] = block_excl_scan<kSmallNT>(s, &tot);
+  uint32_t loc = 0;
+  for (int i = b0; i < e0; ++i) {
+    const uint32_t v = sh[lds_pad(i)];
+    sh[lds_pad(i)] = loc;
+    loc += v;
+  }
+  __syncthreads();
+#pragma unroll 8
+  for (int i = t; i < nn; i += kSmallNT) out[i] = base[i / per] + (int64_t)sh[lds_pad(i)];
   if (t == 0) *total = tot;
   if (pair_off) {
     __syncthreads();  // out[] of every thread is visible to the block after the barrier
