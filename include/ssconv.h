@@ -155,7 +155,10 @@ int ssconv_rulebook_pairs(ssconv_rulebook_t rb, int32_t* dst, hipStream_t stream
 int ssconv_rulebook_neighbours(ssconv_rulebook_t rb, int32_t* dst, hipStream_t stream);
 /* Copies a coordinate hash table (which = 0: H_n, 1: H_{n+1}) as its raw uint64
  * slots (key << 32 | row, key = ((b*G0 + x)*G1 + y)*G2 + z, empty = ~0) into dst
- * [capacity]; *capacity (host) is set when dst is NULL. */
+ * [capacity]; *capacity (host) is set when dst is NULL.  The table of a generated
+ * output set (which = 1, non-submanifold) is not needed to build the rule book; it
+ * is filled on the first call that asks for it, on stream, and that call then
+ * synchronises with the host (SSCONV_E_HASH_FULL if it overflows). */
 int ssconv_rulebook_hash(ssconv_rulebook_t rb, int which, uint64_t* dst, int64_t* capacity /*host*/,
                          hipStream_t stream);
 void ssconv_rulebook_destroy(ssconv_rulebook_t rb);

@@ -117,6 +117,7 @@ struct ssconv_rulebook {
   int64_t cap_in = 0;
   uint64_t* hash_out = nullptr;  // == hash_in for submanifold
   int64_t cap_out = 0;
+  bool hash_out_built = false;    // generated output sets: hash_out is filled on first request
   int32_t* out_coords = nullptr;  // [n_out, 4]
   int32_t* nbr = nullptr;         // [K, n_out]
   int32_t* pairs = nullptr;       // [n_pairs, 2] grouped by offset

@@ -2,8 +2,8 @@
 //
 // Instead of Alg. 1's all-pairs loop, every input site is inserted into an
 // open-addressing hash table in HBM (64-bit slots key<<32 | row, lock-free
-// atomicCAS, linear probing), and every (output site, offset) pair probes it
-// once for y = stride*x - s (submanifold layers: half the offsets, the other half mirrored).
+// atomicCAS, linear probing), and on submanifold layers every (output site, offset) pair
+// probes it once for y = stride*x - s (half the offsets; the other half mirrored).
 // Results:
 //   nbr[s][x]   neighbour map (input row or -1), offset-major so that the
 //               forward gather reads one coalesced index vector per offset;
@@ -11,7 +11,10 @@
 //               device-wide scan (count pass, scan, write pass), so the order
 //               is deterministic: grouped by s, output rows ascending.
 // Dilated / strided output sets are marked in a bitmap over the output grid
-// and emitted in lexicographic (b, x, y, z) order by a scan of popcounts.
+// and emitted in lexicographic (b, x, y, z) order by a scan of popcounts; their
+// neighbour map is written from the input side, the output row of each marked
+// (input, offset) being the rank of its bit, so no table of the outputs is
+// probed (it is built only if a caller asks for it).
 #include <algorithm>
 
 #include "hash.hpp"
@@ -124,6 +127,31 @@ __global__ void emit_outputs(const uint32_t* __restrict__ bits, int64_t nbits, c
   reinterpret_cast<int4*>(out)[o] = make_int4((int)bb, (int)x, (int)y, (int)z);
 }
 
+// Neighbour map of a generated output set, filled from the input side: the marking above already
+// names, for input y and offset s, the one output x with stride*x = y + d(s), and that output's
+// row is the rank of its bit (as in emit_outputs), so nbr[s][row(x)] = y needs no hash lookup.
+// Distinct inputs give distinct (x, s), so every entry is written at most once (duplicate inputs
+// fail the build).  nbr is preset to -1.  Grid (ceil(n / 256), K).
+__global__ void scatter_neighbours(const int32_t* __restrict__ c, int64_t n, int ksize, int stride, int go0, int go1,
+                                   int go2, const uint32_t* __restrict__ bits, const int64_t* __restrict__ woff,
+                                   int64_t n_out, int32_t* __restrict__ nbr) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int s = blockIdx.y;
+  if (i >= n) return;
+  const int h = ksize / 2;
+  const int dx = s / (ksize * ksize) - h, dy = (s / ksize) % ksize - h, dz = s % ksize - h;
+  const int4 v = reinterpret_cast<const int4*>(c)[i];
+  const int tx = v.y + dx, ty = v.z + dy, tz = v.w + dz;
+  if (tx < 0 || ty < 0 || tz < 0) return;
+  if (tx % stride || ty % stride || tz % stride) return;
+  const int x = tx / stride, y = ty / stride, z = tz / stride;
+  if (x >= go0 || y >= go1 || z >= go2) return;
+  const uint64_t bit = (((uint64_t)v.x * go0 + x) * go1 + y) * go2 + z;
+  const uint32_t b = (uint32_t)(bit & 31u), m = bits[bit >> 5];
+  const int64_t row = woff[bit >> 5] + __popc(m & ((1u << b) - 1u));
+  nbr[(int64_t)s * n_out + row] = (int32_t)i;
+}
+
 // Logical (row block, offset) of workgroup blockIdx.x in a 1-D launch of nblk * nS workgroups.
 // Workgroup ids are dispatched round-robin over the 8 XCDs (id % 8); each XCD is given one
 // contiguous range of logical ids, row block first, so an XCD looks up every offset of a
@@ -148,32 +176,19 @@ __device__ __forceinline__ int lookup(const int32_t* __restrict__ out_c, int64_t
   return hash_find(slots, mask, site_key(v.x, yx, yy, yz, g0, g1, g2));
 }
 
-// Neighbour-map passes over (offset s, block of 256 output rows):
-//   kLookupCount  looks every (site, offset) up, writes nbr and per-(offset, block) pair counts
-//                 (1-D XCD-ordered launch of nblk * K workgroups);
-//   kCount        counts the pairs of a finished nbr (grid (nblk, K));
-//   kWrite        writes the pairs at the scanned offsets (grid (nblk, K)).
-constexpr int kLookupCount = 0, kCount = 1, kWrite = 2;
+// Pair-list passes over (offset s, block of 256 output rows) of a finished neighbour map:
+//   kCount  counts the pairs per (offset, block) (grid (nblk, K));
+//   kWrite  writes the pairs at the scanned offsets (grid (nblk, K)).
+constexpr int kCount = 1, kWrite = 2;
 template <int kMode>
-__global__ __launch_bounds__(256) void probe_kernel(const int32_t* __restrict__ out_c, int64_t n_out, int ksize,
-                                                    int stride, int g0, int g1, int g2,
-                                                    const uint64_t* __restrict__ slots, uint64_t mask, int nblk,
-                                                    int32_t* __restrict__ nbr, int32_t* __restrict__ counts,
-                                                    const int64_t* __restrict__ offs, int32_t* __restrict__ pairs) {
+__global__ __launch_bounds__(256) void pair_list_kernel(int64_t n_out, int nblk, const int32_t* __restrict__ nbr,
+                                                        int32_t* __restrict__ counts, const int64_t* __restrict__ offs,
+                                                        int32_t* __restrict__ pairs) {
   __shared__ int wcount[4];
-  int64_t rblk = blockIdx.x;
-  int s = blockIdx.y;
-  if (kMode == kLookupCount) xcd_tile((int64_t)nblk * ksize * ksize * ksize, ksize * ksize * ksize, &rblk, &s);
+  const int64_t rblk = blockIdx.x;
+  const int s = blockIdx.y;
   const int64_t p = rblk * 256 + threadIdx.x;
-  int nb = -1;
-  if (p < n_out) {
-    if (kMode == kLookupCount) {
-      nb = lookup(out_c, p, s, ksize, stride, g0, g1, g2, slots, mask);
-      nbr[(int64_t)s * n_out + p] = nb;
-    } else {
-      nb = nbr[(int64_t)s * n_out + p];
-    }
-  }
+  const int nb = p < n_out ? nbr[(int64_t)s * n_out + p] : -1;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const uint64_t ball = __ballot(nb >= 0);
   if (lane == 0) wcount[w] = __popcll(ball);
@@ -365,6 +380,8 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
 
   // ---- output site set ----
   Scratch tmp(st);
+  uint32_t* obits = nullptr;  // generated sets: output bitmap and its word offsets (ranks)
+  int64_t* owoff = nullptr;
   if (submanifold) {
     rb->n_out = n;
     if (n) SSC_HIP(hipMemcpyAsync(rb->out_coords, coords, (size_t)n * 16, hipMemcpyDeviceToDevice, st));
@@ -383,6 +400,8 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     int64_t* woff = (int64_t*)(t0 + o_woff);
     int64_t* stmp = (int64_t*)(t0 + o_stmp);
     int64_t* dtotal = stmp + scan_tmp_elems(nw);
+    obits = bits;
+    owoff = woff;
     if (nw) SSC_HIP(hipMemsetAsync(bits, 0, (size_t)nw * 4, st));
     if (n > 0) {
       dim3 gm(cdiv(n, 256), K);
@@ -396,7 +415,8 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     SSC_HIP(hipMemcpyAsync(host, dtotal, 8, hipMemcpyDeviceToHost, st));
     SSC_HIP(hipStreamSynchronize(st));
     rb->n_out = host[0];
-    // second block: output coordinates, output hash, neighbour map, pairs (upper bound <= 1 GB)
+    // second block: output coordinates, output hash (filled only when a caller asks for it: the
+    // neighbour map below does not use it), neighbour map, pairs (upper bound <= 1 GB)
     SSC_TRY(hash_capacity(rb->n_out, &rb->cap_out));
     const size_t bound = (size_t)K * (size_t)rb->n_out * 8;
     Carve c1;
@@ -412,7 +432,6 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     if (bound <= ((size_t)1 << 30)) rb->pairs = (int32_t*)(b1 + o_pairs);
     if (nbits) emit_outputs<<<cdiv(nbits, 256), 256, 0, st>>>(bits, nbits, woff, go[0], go[1], go[2], rb->out_coords);
     SSC_HIP(hipGetLastError());
-    SSC_TRY(build_hash(rb->out_coords, rb->n_out, go, st, rb->hash_out, rb->cap_out, dflags, false, false));
   }
 
   // ---- neighbour map and per-offset pair lists ----
@@ -438,12 +457,13 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
         mirror_lookup_kernel<<<(unsigned)((int64_t)nblk * c), 256, 0, st>>>(rb->out_coords, n_out, ksize, grid[0],
                                                                              grid[1], grid[2], rb->hash_in, mask_in,
                                                                              nblk, rb->nbr);
-      probe_kernel<kCount><<<gp, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0], grid[1], grid[2],
-                                               rb->hash_in, mask_in, nblk, rb->nbr, counts, nullptr, nullptr);
+      pair_list_kernel<kCount><<<gp, 256, 0, st>>>(n_out, nblk, rb->nbr, counts, nullptr, nullptr);
     } else {
-      probe_kernel<kLookupCount><<<(unsigned)ncnt, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0],
-                                                                  grid[1], grid[2], rb->hash_in, mask_in, nblk,
-                                                                  rb->nbr, counts, nullptr, nullptr);
+      SSC_HIP(hipMemsetAsync(rb->nbr, 0xFF, (size_t)K * n_out * 4, st));
+      const int* go = rb->grid_out;
+      scatter_neighbours<<<dim3(cdiv(n, 256), K), 256, 0, st>>>(coords, n, ksize, stride, go[0], go[1], go[2], obits,
+                                                              owoff, n_out, rb->nbr);
+      pair_list_kernel<kCount><<<gp, 256, 0, st>>>(n_out, nblk, rb->nbr, counts, nullptr, nullptr);
     }
     SSC_HIP(hipGetLastError());
     SSC_TRY(exclusive_scan_pair_off(counts, K, nblk, offs, dtotal, stmp, rb->pair_off_dev, st));
@@ -456,8 +476,7 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
       SSC_TRY(dev_alloc((void**)&rb->mem[2], (size_t)host[0] * 8, st));
       rb->pairs = (int32_t*)rb->mem[2];
     }
-    probe_kernel<kWrite><<<gp, 256, 0, st>>>(rb->out_coords, n_out, ksize, stride, grid[0], grid[1], grid[2],
-                                             rb->hash_in, mask_in, nblk, rb->nbr, nullptr, offs, rb->pairs);
+    pair_list_kernel<kWrite><<<gp, 256, 0, st>>>(n_out, nblk, rb->nbr, nullptr, offs, rb->pairs);
     SSC_HIP(hipGetLastError());
   } else {
     SSC_HIP(hipMemsetAsync(rb->pair_off_dev, 0, (size_t)(K + 1) * 8, st));
@@ -542,6 +561,16 @@ extern "C" int ssconv_rulebook_neighbours(ssconv_rulebook_t rb, int32_t* dst, hi
 extern "C" int ssconv_rulebook_hash(ssconv_rulebook_t rb, int which, uint64_t* dst, int64_t* capacity,
                                     hipStream_t stream) {
   if (!rb || (which != 0 && which != 1)) return fail(SSCONV_E_INVALID, "bad argument");
+  if (which && rb->hash_out != rb->hash_in && !rb->hash_out_built) {
+    // a generated output set's table is filled on first request, on the caller's stream
+    int* dflags = (int*)(rb->pair_off_dev + rb->K + 1);
+    SSC_TRY(build_hash(rb->out_coords, rb->n_out, rb->grid_out, stream, rb->hash_out, rb->cap_out, dflags, true, false));
+    int flags = 0;
+    SSC_HIP(hipMemcpyAsync(&flags, dflags, 4, hipMemcpyDeviceToHost, stream));
+    SSC_HIP(hipStreamSynchronize(stream));
+    if (flags & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
+    rb->hash_out_built = true;
+  }
   const uint64_t* src = which ? rb->hash_out : rb->hash_in;
   int64_t cap = which ? rb->cap_out : rb->cap_in;
   if (capacity) *capacity = cap;
