@@ -470,10 +470,13 @@ KgradPlan kgrad_plan(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int co
   if (dt == SSCONV_F32) {
     p.wmb = round_wb(tile_blocks(cout));
     p.wnb = round_wb(tile_blocks(cin));
-    // few pairs (at most ~256 per work unit, so fewer than 1024 units): a whole-tile task leaves
-    // most SIMDs idle while each wavefront runs its MFMAs serially, so split the output rows
-    // in two tiles (the gathered input rows are then read twice, from L2)
-    if (p.wmb == 8 && std::max<int64_t>(rb->K, rb->n_pairs / 256) < 1024) p.wmb = 4;
+    // few pairs (at least ~256 per work unit, so few units): when the (unit, tile) tasks number
+    // under 1024, most SIMDs idle while each wavefront runs its tile's MFMAs serially, so the
+    // output rows are cut into 4-block tiles (the gathered input rows are then read once per
+    // tile, from L2)
+    const int64_t units = std::max<int64_t>(rb->K, rb->n_pairs / 256);
+    const int64_t tiles_now = (int64_t)((cout + 16 * p.wmb - 1) / (16 * p.wmb)) * ((cin + 16 * p.wnb - 1) / (16 * p.wnb));
+    if (p.wmb >= 7 && units * tiles_now < 1024) p.wmb = 4;
     p.mtiles = (cout + 16 * p.wmb - 1) / (16 * p.wmb);
     p.ntiles = (cin + 16 * p.wnb - 1) / (16 * p.wnb);
   } else {
