@@ -226,3 +226,33 @@ def test_pair_path_ragged(ksize, stride, sub, fields_out):
     print(f"pair path k{ksize} s{stride} cout {spec.cout}: {errs}", flush=True)
     assert max(errs) < 1e-4
     rb.close()
+
+
+@pytest.mark.parametrize("ksize,stride", [(3, 2), (3, 1)])
+def test_generated_output_table_on_request(ksize, stride):
+    """A generated output set's coordinate table is filled only when asked for: the rule book
+    built without it matches the oracle's pairs, and the table, read twice, holds exactly the
+    output sites with their rows."""
+    grid = 19
+    c = _coords(21, 1500, grid, batch=3)
+    rb = P.Rulebook(torch.from_numpy(c).to(DEV), grid, ksize, stride, False)
+    try:
+        oc_out = rb.out_coords().cpu().numpy()
+        ref = orb.rulebook(c, oc_out, ksize, stride)
+        got = rb.pairs().cpu().numpy()
+        counts = [len(r) for r in ref]
+        off = np.concatenate([[0], np.cumsum(counts)])
+        assert got.shape[0] == off[-1]
+        for s, r in enumerate(ref):
+            assert np.array_equal(got[off[s]:off[s + 1]], np.asarray(r, dtype=np.int32).reshape(-1, 2))
+        t1 = rb.hash_slots(1).cpu().numpy().view(np.uint64)
+        t2 = rb.hash_slots(1).cpu().numpy().view(np.uint64)
+        assert np.array_equal(t1, t2)
+        full = t1[t1 != np.uint64(0xFFFFFFFFFFFFFFFF)]
+        go = -(-grid // stride)
+        b, x, y, z = (oc_out[:, i].astype(np.uint64) for i in range(4))
+        keys = ((b * go + x) * go + y) * go + z
+        want = np.sort((keys << np.uint64(32)) | np.arange(len(oc_out), dtype=np.uint64))
+        assert np.array_equal(np.sort(full), want)
+    finally:
+        rb.close()
