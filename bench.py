@@ -149,9 +149,13 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2, help="workload index 1..9 (default: the 64^3 5x5x5 layer; 6: the "
+    ap.add_argument("--config", type=int, default=4, help="workload index 1..9 (default: the 128^3 3x3x3 208-channel "
+                    "bf16 layer; 2: the 64^3 5x5x5 104-channel fp32 layer; 5: the five-layer stack; 6: the "
                     "downsampling block conv + norm + gate + pooling; 7: input voxelisation; "
                     "8: Feature-Steering; 9: Tensor-to-Point)")
+    ap.add_argument("--secondary", type=int, default=-1,
+                    help="a second workload measured after the first and reported in the same line under "
+                         "'secondary' (default: 2 after the bf16 layer 4, none otherwise; 0: none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle work to aim for")
     ap.add_argument("--only", choices=["step", "forward"], default="step",
@@ -610,7 +614,29 @@ class InterpBench:
 # CPU oracle baseline (bounded sample of the same workload)
 # ---------------------------------------------------------------------------
 
+def cpu_model():
+    """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        txt = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in txt.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(i, budget_s):
+    """The fp64 oracle on this host's cores over the first m output rows of the workload (all their
+    offsets), m grown until the work fills about half the budget; timed per phase."""
     from threadpoolctl import threadpool_info
     from oracle import conv as oc
     from oracle import rulebook as orb
@@ -625,25 +651,36 @@ def cpu_baseline(i, budget_s):
     t0 = time.perf_counter()
     co = orb.output_sites(coords, spec.grid, L.ksize, L.stride, L.submanifold)
     t_sites = time.perf_counter() - t0
-    # sample: the first m output rows, grown until the timed work fills about half the budget
     m = min(len(co), 256)
     while True:
         g = make_grad(spec, len(co), L.cout)[:m]
-        t0 = time.perf_counter()
+        t = [time.perf_counter()]
         R = orb.rulebook(coords, co[:m], L.ksize, L.stride)
-        kap = lay.kappa(w)
+        t.append(time.perf_counter())
+        kap = lay.kappa(w, bf16=spec.dtype == "bf16")
+        t.append(time.perf_counter())
         oc.forward(f, R, kap, m)
+        t.append(time.perf_counter())
         oc.grad_feats(g, R, kap, len(coords))
         dk = oc.grad_kappa(f, g, R, kap.shape)
         oc.synth_adjoint(L, lay.basis, dk)
-        t = time.perf_counter() - t0 + t_sites * m / max(len(co), 1)
-        if m == len(co) or t >= 0.5 * budget_s:
+        t.append(time.perf_counter())
+        ph = np.diff(t)
+        ph[0] += t_sites * m / max(len(co), 1)          # the output-site pass, pro rata
+        tot = float(ph.sum())
+        if m == len(co) or tot >= 0.5 * budget_s:
             break
-        m = int(min(len(co), max(2 * m, m * 0.8 * budget_s / max(t, 1e-3))))
+        m = int(min(len(co), max(2 * m, m * 0.8 * budget_s / max(tot, 1e-3))))
     threads = max([p.get("num_threads", 1) for p in threadpool_info()] + [1])
-    return {"value": m / t / 1e6, "unit": "M active output sites/s", "cores": int(threads), "kind": "oracle",
+    names = ("rulebook", "synth", "forward", "backward")
+    phases = {n: {"s": float(x), "M_sites_per_s": m / float(x) / 1e6} for n, x in zip(names, ph)}
+    phases["rulebook"]["threads"] = 1
+    phases["synth"]["what"] = "the whole kernel (independent of the sample size)"
+    phases["backward"]["what"] = "feature gradient + kernel gradient + coefficient gradient"
+    return {"value": m / tot / 1e6, "unit": "M active output sites/s", "cores": int(threads), "kind": "oracle",
+            "cpu_model": cpu_model(), "phases": phases,
             "sample": f"{spec.name}: first {m} of {len(co)} output rows, all offsets; rulebook (dict, 1 thread) + "
-                      f"synth + forward + backward (fp64 numpy), {t:.1f} s"}
+                      f"synth + forward + backward (fp64 numpy, BLAS on {threads} threads), {tot:.1f} s"}
 
 
 def cpu_baseline_block(i):
@@ -897,6 +934,71 @@ def run_voxel_bench(args, dev):
     print(json.dumps(out), flush=True)
 
 
+def measure(args, i, steps, warmup, dev):
+    """Warm up, time `steps` whole steps of workload i between two device synchronisations, and
+    return the JSON fields of that measurement (value, roofline of the gather-GEMM kernel from
+    the library's launch events, per-phase report, CPU oracle baseline)."""
+    import torch
+    import paper_2111_07383_amd as P
+    from workloads import CONFIGS
+    spec = CONFIGS[i]
+    log(f"setting up {spec.name}")
+    b = (StackBench(dev) if i == 5 else BlockBench(i, dev) if i == 6 else SingleLayer(i, dev))
+    run = b.forward_only if args.only == "forward" else b.step
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    log(f"warmup done ({warmup} steps); timing {steps} steps")
+    P.debug_set(4, 1)                 # HIP events around each gather-GEMM launch, on its stream
+    if args.only == "step" and isinstance(b, SingleLayer):
+        b.events = []                 # phase boundaries of every timed step (torch's stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        run()
+    torch.cuda.synchronize()
+    t = time.perf_counter() - t0
+    P.debug_set(4, 0)
+    ms = t / steps * 1e3
+    value = b.sites() / (ms / 1e3) / 1e6
+    log(f"{spec.name}: {ms:.3f} ms/step, {value:.2f} M sites/s")
+
+    out = {"metric": METRIC, "value": value, "unit": "M active output sites/s", "n_gpus": 1, "steps": steps,
+           "warmup": warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": spec.dtype, "data": "synthetic", "config": b.config()}
+    if args.only == "forward":
+        out["metric"] = METRIC + " (forward gather-GEMM only)"
+        out["config"]["step"] = "forward gather-MFMA only (rule book and kernel prebuilt)"
+    n_timed, kern_ms = P.debug_kernel_ms()
+    flops_step, launches_step = b.gather_flops(args.only == "forward")
+    if n_timed != launches_step * steps:
+        log(f"warning: {n_timed} gather-GEMM launches timed, expected {launches_step * steps}")
+    avg_ms = kern_ms / max(n_timed, 1)
+    flops_launch = flops_step / launches_step
+    achieved = flops_step * steps / (kern_ms / 1e3) / 1e12
+    traffic, tsrc = traffic_from_summary(spec)
+    out["roofline"] = {"kernel": kernel_name(spec.dtype), "bound": "mfma", "achieved": achieved,
+                       "peak": PEAK[spec.dtype], "unit": "TFLOP/s", "frac": achieved / PEAK[spec.dtype],
+                       "traffic": traffic, "traffic_source": tsrc, "avg_launch_ms": avg_ms,
+                       "launches_timed": n_timed, "algorithmic_flops_per_launch": flops_launch,
+                       "kernel_ms_per_step": kern_ms / steps}
+    log(f"gather-GEMM: {n_timed} launches, {avg_ms:.4f} ms avg, {achieved:.1f} TFLOP/s")
+    if isinstance(b, BlockBench):
+        b.events = []                 # per-phase times from extra sequential steps, after the timed ones
+        for _ in range(10):
+            b.phase_step()
+        torch.cuda.synchronize()
+    if isinstance(b, (SingleLayer, BlockBench)) and b.events:
+        out["phases"] = b.phase_report()
+        ph = out["phases"]
+        log("phases (median ms / roofline fraction): " +
+            ", ".join(f"{k} {v['ms']:.3f}/{v.get('frac', float('nan')):.2f}" for k, v in ph.items() if "ms" in v))
+    if not args.no_cpu_baseline and i != 5:
+        log("timing the CPU oracle on a bounded sample")
+        out["cpu_baseline"] = (cpu_baseline_block(i) if i == 6 else cpu_baseline(i, args.cpu_budget))
+    return out
+
+
 def main():
     args = parse()
     if args.counter_summary:
@@ -927,72 +1029,20 @@ def main():
         torch.cuda.synchronize()
         log(f"copied {args.copy_mb} MiB x {max(args.steps, 1)}")
         return
-    from workloads import CONFIGS
-    spec = CONFIGS[args.config]
     if args.variant:
         import paper_2111_07383_amd as P
         P.debug_set(3, args.variant)
-    log(f"setting up {spec.name}")
     if args.only == "forward" and args.config in (5, 6, 7, 8, 9):
         raise SystemExit("--only forward applies to the single-layer workloads 1-4")
     if args.config in (7, 8, 9):
         return run_voxel_bench(args, dev)
-    b = (StackBench(dev) if args.config == 5 else BlockBench(args.config, dev) if args.config == 6
-         else SingleLayer(args.config, dev))
-    run = b.forward_only if args.only == "forward" else b.step
-    for _ in range(args.warmup):
-        run()
-    torch.cuda.synchronize()
-    log(f"warmup done ({args.warmup} steps); timing {args.steps} steps")
-    import paper_2111_07383_amd as P
-    P.debug_set(4, 1)                 # HIP events around each gather-GEMM launch, on its stream
-    if args.only == "step" and isinstance(b, SingleLayer):
-        b.events = []                 # phase boundaries of every timed step (torch's stream)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        run()
-    torch.cuda.synchronize()
-    t = time.perf_counter() - t0
-    P.debug_set(4, 0)
-    ms = t / args.steps * 1e3
-    value = b.sites() / (ms / 1e3) / 1e6
-    log(f"{ms:.3f} ms/step, {value:.2f} M sites/s")
-
-    out = {"metric": METRIC, "value": value, "unit": "M active output sites/s", "n_gpus": 1, "steps": args.steps,
-           "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-           "vs_baseline": None, "dtype": spec.dtype, "data": "synthetic", "config": b.config()}
-    if args.only == "forward":
-        out["metric"] = METRIC + " (forward gather-GEMM only)"
-        out["config"]["step"] = "forward gather-MFMA only (rule book and kernel prebuilt)"
-    n_timed, kern_ms = P.debug_kernel_ms()
-    flops_step, launches_step = b.gather_flops(args.only == "forward")
-    if n_timed != launches_step * args.steps:
-        log(f"warning: {n_timed} gather-GEMM launches timed, expected {launches_step * args.steps}")
-    avg_ms = kern_ms / max(n_timed, 1)
-    flops_launch = flops_step / launches_step
-    achieved = flops_step * args.steps / (kern_ms / 1e3) / 1e12
-    traffic, tsrc = traffic_from_summary(spec)
-    out["roofline"] = {"kernel": kernel_name(spec.dtype), "bound": "mfma", "achieved": achieved,
-                       "peak": PEAK[spec.dtype], "unit": "TFLOP/s", "frac": achieved / PEAK[spec.dtype],
-                       "traffic": traffic, "traffic_source": tsrc, "avg_launch_ms": avg_ms,
-                       "launches_timed": n_timed, "algorithmic_flops_per_launch": flops_launch,
-                       "kernel_ms_per_step": kern_ms / args.steps}
-    log(f"gather-GEMM: {n_timed} launches, {avg_ms:.4f} ms avg, {achieved:.1f} TFLOP/s")
-    if isinstance(b, BlockBench):
-        b.events = []                 # per-phase times from extra sequential steps, after the timed ones
-        for _ in range(10):
-            b.phase_step()
-        torch.cuda.synchronize()
-    if isinstance(b, (SingleLayer, BlockBench)) and b.events:
-        out["phases"] = b.phase_report()
-        ph = out["phases"]
-        log("phases (median ms / roofline fraction): " +
-            ", ".join(f"{k} {v['ms']:.3f}/{v.get('frac', float('nan')):.2f}" for k, v in ph.items() if "ms" in v))
-    if not args.no_cpu_baseline and args.config != 5:
-        log("timing the CPU oracle on a bounded sample")
-        out["cpu_baseline"] = (cpu_baseline_block(args.config) if args.config == 6
-                               else cpu_baseline(args.config, args.cpu_budget))
+    out = measure(args, args.config, args.steps, args.warmup, dev)
+    second = args.secondary if args.secondary >= 0 else (2 if args.config == 4 and args.only == "step" else 0)
+    if second:
+        # a second workload in the same line: same step, its own timed region, not part of "value"
+        sec = measure(args, second, max(args.steps // 2, 5), max(args.warmup // 2, 2), dev)
+        out["secondary"] = {k: sec[k] for k in ("value", "unit", "ms_per_step", "steps", "warmup", "dtype", "config",
+                                                 "roofline", "phases", "cpu_baseline") if k in sec}
     print(json.dumps(out), flush=True)
 
 
