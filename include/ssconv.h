@@ -180,6 +180,30 @@ int ssconv_synth_kernel(const ssconv_basis_desc* desc /*host*/, const float* bas
 int ssconv_forward(const void* feats, ssconv_dtype dtype, int cin, ssconv_rulebook_t rb,
                    const void* W, int cout, void* out, hipStream_t stream);
 
+/* ---- allocation-free forward ----------------------------------------------
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * operation, arguments and results as ssconv_forward, but the call allocates
+ * nothing — no hipMalloc / hipFree / hipMallocAsync, no library cache block.
+ * The scratch the kernels need (the packed bf16 kernel, fp32 offset-split
+ * partials, the pair-list path's buffers) is carved from one fixed region of
+ * SSCONV_NOALLOC_SCRATCH_BYTES per device, built into the library and held by
+ * every device the library runs on until the process ends.  Scratch use per
+ * call: bf16 2*ksize^3*cin*cout bytes; fp32 nothing on the output-stationary
+ * kernel (offset splits are reduced until their partials fit) and the
+ * pair-list buffers only where they fit (otherwise the output-stationary
+ * kernel runs: same sums, another order of the fp32 additions).
+ * Errors: as ssconv_forward, plus SSCONV_E_INVALID when the call would need
+ * more scratch than the region holds (bf16 with 2*ksize^3*cin*cout above it).
+ * Every call on one device uses that device's one region: calls that overlap
+ * in time on one device (another stream, another thread) race and give
+ * undefined results; the region keeps the last call's contents, and nothing in
+ * it needs to start at zero.  The device address is looked up on the first
+ * call on each device (with that device current). */
+#define SSCONV_NOALLOC_SCRATCH_BYTES (64u << 20)
+int ssconv_forward_noalloc(const void* feats, ssconv_dtype dtype, int cin, ssconv_rulebook_t rb,
+                           const void* W, int cout, void* out, hipStream_t stream);
+
 /* ---- backward (adjoint of the forward and of the synthesis) ---------------
  * For L = <out, grad_out>:
  *   grad_feats[y] = sum_s sum_{(x,y) in R_s} kappa(s)^T grad_out[x]       (dtype)

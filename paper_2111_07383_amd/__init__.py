@@ -17,6 +17,8 @@ from .binding import (  # noqa: F401
     debug_set,
     empty_cache,
     forward,
+    forward_noalloc,
+    NOALLOC_SCRATCH_BYTES,
     gate_backward,
     gate_forward,
     interpolate,

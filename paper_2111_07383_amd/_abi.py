@@ -45,6 +45,7 @@ SIGNATURES = {
     "ssconv_rulebook_destroy": (None, [c_void_p]),
     "ssconv_synth_kernel": (c_int, [POINTER(BasisDesc), c_void_p, c_void_p, c_int, c_void_p, c_void_p]),
     "ssconv_forward": (c_int, [c_void_p, c_int, c_int, c_void_p, c_void_p, c_int, c_void_p, c_void_p]),
+    "ssconv_forward_noalloc": (c_int, [c_void_p, c_int, c_int, c_void_p, c_void_p, c_int, c_void_p, c_void_p]),
     "ssconv_backward_workspace_size": (c_size_t, [c_void_p, c_int, c_int, c_int]),
     "ssconv_backward": (c_int, [c_void_p, c_void_p, c_int, c_int, c_int, c_void_p, c_void_p, POINTER(BasisDesc),
                                 c_void_p, c_void_p, c_void_p, c_void_p, c_size_t, c_void_p]),

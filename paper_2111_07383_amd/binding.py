@@ -193,6 +193,23 @@ def forward(feats: torch.Tensor, rb: Rulebook, W: torch.Tensor, out: Optional[to
     return out
 
 
+def forward_noalloc(feats: torch.Tensor, rb: Rulebook, W: torch.Tensor, out: torch.Tensor, stream=None) -> torch.Tensor:
+    """ssconv_forward_noalloc: forward into a caller-given out with no device allocation (scratch
+    from the library's fixed per-device region)."""
+    _need(feats, "feats")
+    _need(W, "W", feats.dtype)
+    K, cout, cin = W.shape
+    if feats.shape != (rb.n_in, cin):
+        raise ValueError(f"feats must be [{rb.n_in}, {cin}]")
+    _need(out, "out", feats.dtype, (rb.n_out, cout))
+    check(lib().ssconv_forward_noalloc(_ptr(feats), _dtype(feats), cin, rb.handle, _ptr(W), cout, _ptr(out),
+                                       _stream(stream)), "ssconv_forward_noalloc")
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20
+
+
 def backward_workspace_size(rb: Rulebook, dtype: torch.dtype, cin: int, cout: int) -> int:
     return lib().ssconv_backward_workspace_size(rb.handle, BF16 if dtype == torch.bfloat16 else F32, cin, cout)
 

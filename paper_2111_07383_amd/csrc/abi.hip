@@ -1,5 +1,6 @@
 // C ABI entry points of the convolution: argument checks and launches.
 #include <algorithm>
+#include <mutex>
 
 #include "conv.hpp"
 #include "synth.hpp"
@@ -31,6 +32,61 @@ extern "C" int ssconv_forward(const void* feats, ssconv_dtype dtype, int cin, ss
     return SSCONV_OK;
   }
   return conv_forward(feats, dtype, cin, rb, W, cout, out, stream);
+}
+
+// ---------------------------------------------------------------------------
+// allocation-free forward
+// ---------------------------------------------------------------------------
+// The scratch of ssconv_forward_noalloc: one fixed region per device, part of the library's code
+// object (each device that loads the library holds its own copy until the process ends).  Host
+// code never uses this name as a device address: it is a host-side stand-in; the device address
+// comes from hipGetSymbolAddress, taken once per device with that device current.
+static __device__ __align__(256) char scratch[SSCONV_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of this device's scratch region (looked up on the first call per device).
+int scratch_region(char** out) {
+  int dev = 0;
+  SSC_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(SSCONV_E_INVALID, "device %d is beyond the %d supported", dev, kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    SSC_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return fail(SSCONV_E_HIP, "hipGetSymbolAddress returned no address for the scratch region");
+    g_scratch_ptr[dev] = (char*)p;
+  }
+  *out = g_scratch_ptr[dev];
+  return SSCONV_OK;
+}
+
+__global__ void zero_halves_kernel(uint16_t* __restrict__ p, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
+}  // namespace
+
+extern "C" int ssconv_forward_noalloc(const void* feats, ssconv_dtype dtype, int cin, ssconv_rulebook_t rb,
+                                      const void* W, int cout, void* out, hipStream_t stream) {
+  SSC_TRY(check_conv_args(feats, out, dtype, cin, cout, rb, W));
+  if ((rb->n_in > 0 && !feats) || (rb->n_out > 0 && !out)) return fail(SSCONV_E_INVALID, "NULL feature buffer");
+  if (rb->n_out == 0) return SSCONV_OK;
+  if (rb->n_in == 0) {  // no input rows: every output row is 0 (a fill kernel, no memset node)
+    const int64_t halves = (int64_t)rb->n_out * cout * (int64_t)dtype_bytes(dtype) / 2;  // exactly the buffer
+    zero_halves_kernel<<<cdiv(halves, 256), 256, 0, stream>>>((uint16_t*)out, halves);
+    SSC_HIP(hipGetLastError());
+    return SSCONV_OK;
+  }
+  CallScratch sc;
+  SSC_TRY(scratch_region(&sc.base));
+  sc.cap = SSCONV_NOALLOC_SCRATCH_BYTES;
+  return conv_forward(feats, dtype, cin, rb, W, cout, out, stream, &sc);
 }
 
 extern "C" size_t ssconv_backward_workspace_size(ssconv_rulebook_t rb, ssconv_dtype dtype, int cin, int cout) {

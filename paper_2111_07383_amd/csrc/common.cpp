@@ -144,6 +144,23 @@ int dev_alloc(void** p, size_t bytes, hipStream_t stream) {
   return SSCONV_OK;
 }
 
+int scratch_take(CallScratch* sc, void** p, size_t bytes, hipStream_t stream) {
+  if (!sc || !sc->fixed()) return dev_alloc(p, bytes, stream);
+  const size_t at = (sc->used + 255) & ~(size_t)255;
+  if (at > sc->cap || bytes > sc->cap - at) {
+    *p = nullptr;
+    return fail(SSCONV_E_INVALID, "the call needs %zu more bytes of scratch; %zu of %zu are left", bytes,
+                sc->cap > at ? sc->cap - at : (size_t)0, sc->cap);
+  }
+  *p = sc->base + at;
+  sc->used = at + bytes;
+  return SSCONV_OK;
+}
+
+void scratch_give(CallScratch* sc, void* p, hipStream_t stream) {
+  if (!sc || !sc->fixed()) dev_free(p, stream);
+}
+
 void dev_free(void* p, hipStream_t stream) {
   if (!p) return;
   std::lock_guard<std::mutex> lk(g_cache_mu);

@@ -36,6 +36,19 @@ int fail(int code, const char* fmt, ...);
 // stream-ordered device allocation with the test hook for forced failures
 int dev_alloc(void** p, size_t bytes, hipStream_t stream);
 void dev_free(void* p, hipStream_t stream);
+// Device scratch of one call, handed down to the kernels that need it.  base == nullptr: every
+// request is a block of the device memory cache (dev_alloc / dev_free).  Otherwise requests are
+// carved, 256-byte aligned, from [base, base + cap) in order and never freed (the
+// allocation-free entry points pass their fixed per-device region this way); a request that
+// does not fit fails with SSCONV_E_INVALID.
+struct CallScratch {
+  char* base = nullptr;
+  size_t cap = 0, used = 0;
+  bool fixed() const { return base != nullptr; }
+  size_t left() const { return cap > ((used + 255) & ~(size_t)255) ? cap - ((used + 255) & ~(size_t)255) : 0; }
+};
+int scratch_take(CallScratch* sc, void** p, size_t bytes, hipStream_t stream);
+void scratch_give(CallScratch* sc, void* p, hipStream_t stream);
 int64_t debug_hash_capacity();
 int64_t debug_gather_variant();
 // Fork / join of work onto the library's second stream of the current device: aux_fork makes

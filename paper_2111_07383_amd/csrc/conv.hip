@@ -289,10 +289,10 @@ int pick_wnb(int cb) {
 
 template <typename T>
 int dispatch_gg(const void* src, int64_t n_src, int ca, const void* Bt, int cb, const int32_t* nbr, int64_t n_rows, int K,
-                void* out, hipStream_t st) {
+                void* out, hipStream_t st, CallScratch* sc = nullptr) {
   const ssconv_dtype dt = sizeof(T) == 4 ? SSCONV_F32 : SSCONV_BF16;
   if (gather_mfma_supported(dt, ca, cb, K))
-    return gather_mfma(src, n_src, dt, ca, Bt, cb, nbr, nullptr, n_rows, K, out, st);
+    return gather_mfma(src, n_src, dt, ca, Bt, cb, nbr, nullptr, n_rows, K, out, st, sc);
   switch (pick_wnb(cb)) {
     case 1: launch_gg<T, 1>(src, ca, Bt, cb, nbr, n_rows, K, out, st); break;
     case 2: launch_gg<T, 2>(src, ca, Bt, cb, nbr, n_rows, K, out, st); break;
@@ -352,37 +352,40 @@ struct KernelTimer {
 };
 
 int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_rulebook* rb, const void* W, int cout,
-                 void* out, hipStream_t st) {
+                 void* out, hipStream_t st, CallScratch* sc) {
   if (rb->n_out == 0) return SSCONV_OK;
-  if (dt == SSCONV_F32 && pair_path_wins(rb, dt, cin, cout, rb->n_out)) {
+  // the pair-list path needs its Y buffer; with a fixed scratch region too small for it the
+  // output-stationary kernel runs instead (same sums, another order of the fp32 additions)
+  const bool pair_fits = !(sc && sc->fixed()) || pair_path_bytes(rb, cin, cout, rb->n_out) <= sc->left();
+  if (dt == SSCONV_F32 && pair_fits && pair_path_wins(rb, dt, cin, cout, rb->n_out)) {
     void* ws = nullptr;
-    SSC_TRY(dev_alloc(&ws, pair_path_bytes(rb, cin, cout, rb->n_out), st));
+    SSC_TRY(scratch_take(sc, &ws, pair_path_bytes(rb, cin, cout, rb->n_out), st));
     int rc;
     {
       KernelTimer timer(st);
       rc = pair_gemm(feats, cin, W, cout, rb, 1, out, rb->n_out, ws, st);
     }
-    dev_free(ws, st);
+    scratch_give(sc, ws, st);
     return rc;
   }
   if (dt == SSCONV_F32) {
     KernelTimer timer(st);
-    return dispatch_gg<float>(feats, rb->n_in, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st);
+    return dispatch_gg<float>(feats, rb->n_in, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st, sc);
   }
   if (use_bf16_kernel(dt, rb->n_in, cin, cout, rb->K)) {
     // kappa packed for the bf16 kernel in a stream-ordered scratch buffer
     void* Bp = nullptr;
-    SSC_TRY(dev_alloc(&Bp, (size_t)rb->K * cin * cout * 2, st));
+    SSC_TRY(scratch_take(sc, &Bp, (size_t)rb->K * cin * cout * 2, st));
     int rc = pack_b_bf16(W, rb->K, cin, cout, false, false, Bp, st);
     if (rc == SSCONV_OK) {
       KernelTimer timer(st);
       rc = gather_bf16(feats, rb->n_in, cin, Bp, cout, rb->nbr, nullptr, rb->n_out, rb->K, out, st);
     }
-    dev_free(Bp, st);
+    scratch_give(sc, Bp, st);
     return rc;
   }
   KernelTimer timer(st);
-  return dispatch_gg<uint16_t>(feats, rb->n_in, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st);
+  return dispatch_gg<uint16_t>(feats, rb->n_in, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st, sc);
 }
 
 int dw_nsplit(const ssconv_rulebook* rb) {

@@ -18,8 +18,9 @@ size_t pair_path_bytes(const ssconv_rulebook* rb, int ca, int cb, int64_t n_dst)
 int pair_gemm(const void* src, int ca, const void* Bt, int cb, const ssconv_rulebook* rb, int sel_in, void* dst,
               int64_t n_dst, void* ws, hipStream_t st);
 
+// sc: where the call's scratch comes from (nullptr: the device memory cache).
 int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_rulebook* rb, const void* W, int cout,
-                 void* out, hipStream_t st);
+                 void* out, hipStream_t st, CallScratch* sc = nullptr);
 BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout);
 int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout, const ssconv_rulebook* rb,
                         const void* W, void* grad_feats, char* ws, const BwdLayout& L, hipStream_t st);

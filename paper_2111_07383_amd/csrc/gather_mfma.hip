@@ -351,13 +351,15 @@ int pick_nsplit(int64_t tiles, int K) {
 
 template <typename T, int WMB, int WNB, int S, int NW, typename IX>
 int launch(const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, const int32_t* order, int64_t n_pos,
-           int K, void* out, hipStream_t st) {
+           int K, void* out, hipStream_t st, CallScratch* sc) {
   using SH = Shape<T, WMB, WNB, S, NW>;
   const size_t smem = smem_bytes<T, WMB, WNB, S, NW, IX>(K);
   auto kern = gather_mfma_kernel<T, WMB, WNB, S, NW, IX>;
   SSC_HIP(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem));
   const int64_t mt = cdiv(n_pos, SH::BM), nt = cdiv(cb, SH::BN);
-  const int nsplit = debug_gather_variant() == 8 ? std::min(K, 3) : pick_nsplit(mt * nt, K);
+  int nsplit = debug_gather_variant() == 8 ? std::min(K, 3) : pick_nsplit(mt * nt, K);
+  if (sc && sc->fixed())
+    while (nsplit > 1 && (size_t)nsplit * n_pos * cb * 4 > sc->left()) --nsplit;
   if (nsplit == 1) {
     kern<<<dim3(mt, nt, 1), SH::NT, smem, st>>>((const T*)src, ca, (const T*)Bt, cb, nbr, order, n_pos, K, (T*)out,
                                                  nullptr);
@@ -365,7 +367,7 @@ int launch(const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, 
     return SSCONV_OK;
   }
   float* part = nullptr;
-  SSC_TRY(dev_alloc((void**)&part, (size_t)nsplit * n_pos * cb * 4, st));
+  SSC_TRY(scratch_take(sc, (void**)&part, (size_t)nsplit * n_pos * cb * 4, st));
   kern<<<dim3(mt, nt, nsplit), SH::NT, smem, st>>>((const T*)src, ca, (const T*)Bt, cb, nbr, order, n_pos, K,
                                                     (T*)out, part);
   hipError_t e = hipGetLastError();
@@ -373,7 +375,7 @@ int launch(const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, 
     split_reduce_kernel<T><<<cdiv(n_pos * cb, 256), 256, 0, st>>>(part, nsplit, n_pos, cb, order, (T*)out);
     e = hipGetLastError();
   }
-  dev_free(part, st);
+  scratch_give(sc, part, st);
   if (e != hipSuccess) return fail(SSCONV_E_HIP, "gather launch: %s", hipGetErrorString(e));
   return SSCONV_OK;
 }
@@ -422,17 +424,17 @@ bool pick_cfg(ssconv_dtype dt, int cb, int K, int64_t n_src, Cfg* out) {
 
 template <typename T, int WMB, int S, int NW, typename IX>
 int launch_wnb(int wnb, const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, const int32_t* order,
-               int64_t n_pos, int K, void* out, hipStream_t st) {
+               int64_t n_pos, int K, void* out, hipStream_t st, CallScratch* sc) {
   switch (wnb) {
-    case 1: return launch<T, WMB, 1, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 2: return launch<T, WMB, 2, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 3: return launch<T, WMB, 3, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 4: return launch<T, WMB, 4, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 5: return launch<T, WMB, 5, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 6: return launch<T, WMB, 6, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 7: return launch<T, WMB, 7, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    case 8: return launch<T, WMB, 8, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
-    default: return launch<T, WMB, 13, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st);
+    case 1: return launch<T, WMB, 1, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
+    case 2: return launch<T, WMB, 2, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
+    case 3: return launch<T, WMB, 3, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
+    case 4: return launch<T, WMB, 4, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
+    case 5: return launch<T, WMB, 5, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
+    case 6: return launch<T, WMB, 6, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
+    case 7: return launch<T, WMB, 7, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
+    case 8: return launch<T, WMB, 8, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
+    default: return launch<T, WMB, 13, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
   }
 }
 
@@ -444,7 +446,7 @@ bool gather_mfma_supported(ssconv_dtype dt, int ca, int cb, int K) {
 }
 
 int gather_mfma(const void* src, int64_t n_src, ssconv_dtype dt, int ca, const void* Bt, int cb, const int32_t* nbr,
-                const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st) {
+                const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st, CallScratch* sc) {
   if (n_pos == 0) return SSCONV_OK;
   // tuning overrides (same results): 1 = four wavefronts of 32 rows, 2 = four of 16 rows,
   // 3 = no 16-bit index table, 8 = three offset splits (in launch)
@@ -454,7 +456,7 @@ int gather_mfma(const void* src, int64_t n_src, ssconv_dtype dt, int ca, const v
     return fail(SSCONV_E_INVALID, "no gather tile fits the LDS for K=%d", K);
   if (variant == 1 && cfg_smem<float>({2, c.wnb, 3, 4, false}, K) <= (size_t)kLdsLimit) c = {2, c.wnb, 3, 4, false};
   if (variant == 2) c = {1, c.wnb, 3, 4, false};
-#define SSC_GO(T, WMB, S, NW, IX) return launch_wnb<T, WMB, S, NW, IX>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st)
+#define SSC_GO(T, WMB, S, NW, IX) return launch_wnb<T, WMB, S, NW, IX>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc)
   if (dt == SSCONV_F32) {
     if (c.nw == 8 && c.idx16 && c.stages == 4) SSC_GO(float, 1, 4, 8, uint16_t);
     if (c.nw == 8 && c.idx16) SSC_GO(float, 1, 3, 8, uint16_t);

@@ -10,8 +10,10 @@ bool gather_mfma_supported(ssconv_dtype dt, int ca, int cb, int K);
 
 // out[order ? order[p] : p][:] = sum_s Bt[s] (cb x ca) . src[nbr[s][p]] for p < n_pos.
 // src [*, ca], Bt [K][cb][ca] and out [*, cb] in dt; nbr [K][n_pos] (-1 = absent).
+// Offset splits (fp32 partials added in split order) take their partials from sc (nullptr: the
+// device memory cache); with a fixed scratch region the split count is lowered until they fit.
 int gather_mfma(const void* src, int64_t n_src, ssconv_dtype dt, int ca, const void* Bt, int cb, const int32_t* nbr,
-                const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st);
+                const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st, CallScratch* sc = nullptr);
 
 // bf16 kernel with 256-row tiles and packed kappa (gather_bf16.hip).
 bool gather_bf16_supported(int64_t n_src, int ca, int cb, int K);
