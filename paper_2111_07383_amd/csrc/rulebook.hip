@@ -60,13 +60,17 @@ __global__ void fill_slots(uint64_t* __restrict__ p, int64_t n, uint64_t v, int*
 // Inserts every site; a site outside the grid, with b < 0 or with b > bmax (the largest batch
 // index whose keys fit 32 bits) is not inserted and raises kFlagBounds (one atomic per
 // wavefront that holds such a site).
+// copy (optional): every coordinate row is also written there (the output sites of a submanifold
+// layer are its input sites).
 __global__ void hash_insert_kernel(const int32_t* __restrict__ c, int64_t n, int g0, int g1, int g2, int bmax,
-                                   uint64_t* __restrict__ slots, uint64_t mask, int* __restrict__ flags) {
+                                   uint64_t* __restrict__ slots, uint64_t mask, int* __restrict__ flags,
+                                   int32_t* __restrict__ copy) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   int4 v = make_int4(0, 0, 0, 0);
   bool bad = false;
   if (i < n) {
     v = reinterpret_cast<const int4*>(c)[i];
+    if (copy) reinterpret_cast<int4*>(copy)[i] = v;
     bad = (v.x < 0) | (v.x > bmax) | (v.y < 0) | (v.y >= g0) | (v.z < 0) | (v.z >= g1) | (v.w < 0) | (v.w >= g2);
   }
   const uint64_t any_bad = __ballot(bad);
@@ -208,7 +212,7 @@ __global__ __launch_bounds__(256) void pair_list_kernel(int64_t n_out, int nblk,
 // up.  If site x has neighbour y at offset s (y = x - d(s)), then y has neighbour x at the
 // mirrored offset K-1-s (d(K-1-s) = -d(s)), so that entry is written from here; distinct x
 // give distinct y, so every entry is written at most once.  Rows c..K-1 are set beforehand by
-// mirror_init (c: the identity, above c: -1).  1-D XCD-ordered launch of nblk * c workgroups.
+// rb_init_kernel (c: the identity, above c: -1).  1-D XCD-ordered launch of nblk * c workgroups.
 __global__ __launch_bounds__(256) void mirror_lookup_kernel(const int32_t* __restrict__ c_in, int64_t n, int ksize,
                                                             int g0, int g1, int g2,
                                                             const uint64_t* __restrict__ slots, uint64_t mask,
@@ -224,12 +228,133 @@ __global__ __launch_bounds__(256) void mirror_lookup_kernel(const int32_t* __res
   if (nb >= 0) nbr[(int64_t)(K - 1 - s) * n + nb] = (int32_t)p;
 }
 
-__global__ void mirror_init(int32_t* __restrict__ nbr, int64_t n, int K) {
-  const int c = (K - 1) / 2;
+// One launch that prepares a build (thread i handles entry i of every region it reaches):
+//   slots[0, cap)            <- empty                         (the hash table)
+//   map[0, rows * n)         <- -1, except map[i] = i for i < n when first_identity
+//                               (submanifold: rows c..K-1 of the neighbour map, c = centre;
+//                               generated sets: the whole map)
+//   flags[0] = 0, flags[1] = -1                               (when flags is given)
+__global__ void rb_init_kernel(uint64_t* __restrict__ slots, int64_t cap, int32_t* __restrict__ map, int64_t rows,
+                               int64_t n, int first_identity, int* __restrict__ flags) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= (int64_t)(K - c) * n) return;
-  const int64_t p = i % n;
-  nbr[(int64_t)c * n + i] = i < n ? (int32_t)p : -1;
+  if (i < cap) slots[i] = kEmpty;
+  if (i < rows * n) map[i] = (first_identity && i < n) ? (int32_t)i : -1;
+  if (flags && i == 0) {
+    flags[0] = 0;
+    flags[1] = -1;
+  }
+}
+
+// Compaction of the neighbour map into the pair lists.  The map nbr[K][n] is read as one array in
+// its own (offset-major) order, so the pairs come out grouped by offset with output rows
+// ascending: pairs[pos] = (row, nbr[s][row]) for every entry >= 0, pos = the number of such
+// entries before it; pair_off[s] = the count before offset s's first entry, pair_off[K] = all.
+// The array is cut into tiles of kCompactTile entries, one workgroup each; step j of thread t of a
+// tile is its entry j * kCompactNT + t (coalesced loads, and the valid lanes of one wavefront
+// step write consecutive pairs).  Two launches: pair_count_kernel writes every tile's count,
+// pair_write_kernel adds the counts of the tiles before its own (at most a few thousand values,
+// read from L2) and writes its pairs.  No workgroup waits on another.
+constexpr int kCompactNT = 256, kCompactPer = 32, kCompactTile = kCompactNT * kCompactPer;
+
+// Loads a tile's entries (-1 past the end) and the ballot of valid lanes per step.
+__device__ __forceinline__ void compact_load(const int32_t* __restrict__ nbr, int64_t f0, int64_t total, int tid,
+                                             int (&v)[kCompactPer], uint64_t (&bal)[kCompactPer]) {
+#pragma unroll
+  for (int j = 0; j < kCompactPer; ++j) {
+    const int64_t f = f0 + (int64_t)j * kCompactNT + tid;
+    v[j] = f < total ? nbr[f] : -1;
+  }
+#pragma unroll
+  for (int j = 0; j < kCompactPer; ++j) bal[j] = __ballot(v[j] >= 0);
+}
+
+__global__ __launch_bounds__(kCompactNT) void pair_count_kernel(const int32_t* __restrict__ nbr, int64_t total,
+                                                                int64_t* __restrict__ tile_count) {
+  __shared__ int s_w[kCompactNT / 64];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int v[kCompactPer];
+  uint64_t bal[kCompactPer];
+  compact_load(nbr, (int64_t)blockIdx.x * kCompactTile, total, tid, v, bal);
+  int c = 0;
+#pragma unroll
+  for (int j = 0; j < kCompactPer; ++j) c += __popcll(bal[j]);
+  if (lane == 0) s_w[w] = c;
+  __syncthreads();
+  if (tid == 0) {
+    int64_t t = 0;
+    for (int i = 0; i < kCompactNT / 64; ++i) t += s_w[i];
+    tile_count[blockIdx.x] = t;
+  }
+}
+
+__global__ __launch_bounds__(kCompactNT) void pair_write_kernel(const int32_t* __restrict__ nbr, int64_t n, int K,
+                                                                const int64_t* __restrict__ tile_count,
+                                                                int32_t* __restrict__ pairs,
+                                                                int64_t* __restrict__ pair_off) {
+  constexpr int NW = kCompactNT / 64;
+  __shared__ int s_cnt[kCompactPer][NW];  // valid entries per (step, wavefront)
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int64_t tile = blockIdx.x;
+  const int64_t total = (int64_t)K * n;
+  const int64_t f0 = tile * kCompactTile;
+  int v[kCompactPer];
+  uint64_t bal[kCompactPer];
+  compact_load(nbr, f0, total, tid, v, bal);
+  if (lane == 0) {
+#pragma unroll
+    for (int j = 0; j < kCompactPer; ++j) s_cnt[j][w] = __popcll(bal[j]);
+  }
+  int64_t part = 0;
+  for (int64_t i = tid; i < tile; i += kCompactNT) part += tile_count[i];
+  int64_t before = 0;
+  block_excl_scan<kCompactNT, int64_t>(part, &before);  // also orders the s_cnt writes before the reads
+  // this wavefront's position at step 0: every (step, wavefront) count before it in entry order
+  int64_t pos = before;
+  for (int i = 0; i < w; ++i) pos += s_cnt[0][i];
+  const uint64_t below = (1ull << lane) - 1ull;
+  int64_t f = f0 + tid;
+  int64_t s = f / n, p = f - s * n;
+#pragma unroll
+  for (int j = 0; j < kCompactPer; ++j) {
+    if (f < total) {
+      const int64_t at = pos + __popcll(bal[j] & below);
+      if (p == 0) pair_off[s] = at;
+      if (v[j] >= 0) reinterpret_cast<int2*>(pairs)[at] = make_int2((int)p, v[j]);
+    }
+    // to step j + 1: the rest of this step (wavefronts from w on) and the next step's wavefronts before w
+    if (j + 1 < kCompactPer) {
+#pragma unroll
+      for (int i = 0; i < NW; ++i) pos += (i >= w ? s_cnt[j][i] : 0) + (i < w ? s_cnt[j + 1][i] : 0);
+      f += kCompactNT;
+      if (f < total) {
+        if (n < kCompactNT) {
+          s = f / n, p = f - s * n;
+        } else if ((p += kCompactNT) >= n) {  // p + kCompactNT < 2n
+          p -= n, ++s;
+        }
+      }
+    }
+  }
+  if (tile == gridDim.x - 1 && tid == 0) {
+    int64_t all = before;
+    for (int i = 0; i < kCompactPer * NW; ++i) all += s_cnt[i / NW][i % NW];
+    pair_off[K] = all;
+  }
+}
+
+// The two launches of the compaction; tile_count holds compact_tiles(K, n) values.
+int compact_pairs(const int32_t* nbr, int64_t n, int K, int64_t* tile_count, int32_t* pairs, int64_t* pair_off,
+                  hipStream_t st);
+
+int64_t compact_tiles(int64_t K, int64_t n) { return (K * n + kCompactTile - 1) / kCompactTile; }
+
+int compact_pairs(const int32_t* nbr, int64_t n, int K, int64_t* tile_count, int32_t* pairs, int64_t* pair_off,
+                  hipStream_t st) {
+  const int64_t tiles = compact_tiles(K, n);
+  pair_count_kernel<<<(unsigned)tiles, kCompactNT, 0, st>>>(nbr, (int64_t)K * n, tile_count);
+  pair_write_kernel<<<(unsigned)tiles, kCompactNT, 0, st>>>(nbr, n, K, tile_count, pairs, pair_off);
+  SSC_HIP(hipGetLastError());
+  return SSCONV_OK;
 }
 
 int64_t next_pow2(int64_t v) {
@@ -315,8 +440,23 @@ static int build_hash(const int32_t* coords, int64_t n, const int* g, hipStream_
   if (validate && n > 0) validate_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, g[0], g[1], g[2], flags, flags + 1);
   if (n > 0)
     hash_insert_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, g[0], g[1], g[2], max_batch(g), slots,
-                                                     (uint64_t)(cap - 1), flags);
+                                                     (uint64_t)(cap - 1), flags, nullptr);
   SSC_HIP(hipGetLastError());
+  return SSCONV_OK;
+}
+
+// Pair offsets and flags in one copy: the one synchronisation of a submanifold build (the last of
+// a generated one); device-detected errors surface here.
+static int finish_build(ssconv_rulebook* rb, int64_t* host, hipStream_t st) {
+  const int K = rb->K;
+  SSC_HIP(hipMemcpyAsync(host, rb->pair_off_dev, (size_t)(K + 2) * 8, hipMemcpyDeviceToHost, st));
+  SSC_HIP(hipStreamSynchronize(st));
+  for (int s = 0; s <= K; ++s) rb->pair_off[s] = host[s];
+  rb->n_pairs = host[K];
+  const int fl = (int)(host[K + 1] & 0xffffffff);
+  if (fl & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid, has b < 0, or (max b + 1) * grid volume exceeds the 32-bit key space");
+  if (fl & kFlagDup) return fail(SSCONV_E_DUPLICATE, "duplicate input site");
+  if (fl & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
   return SSCONV_OK;
 }
 
@@ -343,14 +483,17 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
   const size_t pairs_bound = (size_t)K * (size_t)n * 8;  // submanifold: every output has <= K pairs
   const bool pairs_in_block = submanifold && pairs_bound <= ((size_t)1 << 30);
   int* dflags = nullptr;  // [0] flags, [1] max b
+  int64_t* tile_cnt = nullptr;  // per-tile counts of the pair compaction (submanifold builds)
+  const int64_t sub_tiles = submanifold ? compact_tiles(K, n) : 0;
   {
     Carve c;
     const size_t o_hash = c.take((size_t)rb->cap_in * 8), o_off = c.take((size_t)(K + 2) * 8);
-    size_t o_oc = 0, o_nbr = 0, o_pairs = 0;
+    size_t o_oc = 0, o_nbr = 0, o_pairs = 0, o_lb = 0;
     if (submanifold) {
       o_oc = c.take((size_t)n * 16);
       o_nbr = c.take((size_t)K * n * 4);
       if (pairs_in_block) o_pairs = c.take(pairs_bound);
+      o_lb = c.take((size_t)sub_tiles * 8);
     }
     char* b0 = nullptr;
     SSC_TRY(dev_alloc((void**)&b0, c.at, st));
@@ -362,12 +505,41 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
       rb->out_coords = (int32_t*)(b0 + o_oc);
       rb->nbr = (int32_t*)(b0 + o_nbr);
       if (pairs_in_block) rb->pairs = (int32_t*)(b0 + o_pairs);
+      tile_cnt = (int64_t*)(b0 + o_lb);
     }
+  }
+
+  if (submanifold && n > 0) {
+    // Five launches and one read-back: (1) the table, the mirrored rows of the neighbour map, the
+    // look-back state and the flags are set by one kernel; (2) the inserts, which also copy the
+    // sites (the output set); (3) lookups of the offsets before the centre, mirrored entries
+    // written from them; (4) the single-pass compaction into the pair lists.
+    const int c = (K - 1) / 2;
+    const int64_t init_n = std::max<int64_t>(rb->cap_in, (int64_t)(K - c) * n);
+    rb->n_out = n;
+    rb->hash_out = rb->hash_in;
+    rb->cap_out = rb->cap_in;
+    rb_init_kernel<<<cdiv(init_n, 256), 256, 0, st>>>(rb->hash_in, rb->cap_in, rb->nbr + (int64_t)c * n, K - c, n, 1,
+                                                      dflags);
+    hash_insert_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, grid[0], grid[1], grid[2], max_batch(rb->grid),
+                                                     rb->hash_in, (uint64_t)(rb->cap_in - 1), dflags, rb->out_coords);
+    const int nblk = (int)cdiv(n, 256);
+    if (c > 0)
+      mirror_lookup_kernel<<<(unsigned)((int64_t)nblk * c), 256, 0, st>>>(rb->out_coords, n, ksize, grid[0], grid[1],
+                                                                          grid[2], rb->hash_in,
+                                                                          (uint64_t)(rb->cap_in - 1), nblk, rb->nbr);
+    SSC_HIP(hipGetLastError());
+    if (rb->pairs) {
+      SSC_TRY(compact_pairs(rb->nbr, n, K, tile_cnt, rb->pairs, rb->pair_off_dev, st));
+      return finish_build(rb, host, st);
+    }
+    // past 1 GB of pairs at the upper bound: counted, scanned and sized exactly below
   }
 
   // the input table's fill also clears the build flags; its inserts do not depend on the output
   // set, so for generated sets they are queued before the synchronisation that sizes the bitmap
-  SSC_TRY(build_hash(coords, n, rb->grid, st, rb->hash_in, rb->cap_in, dflags, true, !submanifold));
+  if (!(submanifold && n > 0))
+    SSC_TRY(build_hash(coords, n, rb->grid, st, rb->hash_in, rb->cap_in, dflags, true, !submanifold));
   if (!submanifold) {
     // the output bitmap spans the batch: its extent is needed on the host before the next launch
     SSC_HIP(hipMemcpyAsync(host, dflags, 8, hipMemcpyDeviceToHost, st));
@@ -383,8 +555,7 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
   uint32_t* obits = nullptr;  // generated sets: output bitmap and its word offsets (ranks)
   int64_t* owoff = nullptr;
   if (submanifold) {
-    rb->n_out = n;
-    if (n) SSC_HIP(hipMemcpyAsync(rb->out_coords, coords, (size_t)n * 16, hipMemcpyDeviceToDevice, st));
+    rb->n_out = n;  // sites copied and the map's mirrored rows set above
     rb->hash_out = rb->hash_in;
     rb->cap_out = rb->cap_in;
   } else {
@@ -441,7 +612,8 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     const int64_t ncnt = (int64_t)K * nblk;
     Carve c;
     const size_t o_cnt = c.take((size_t)ncnt * 4), o_offs = c.take((size_t)ncnt * 8),
-                 o_stmp = c.take((size_t)scan_tmp_elems(ncnt) * 8 + 8);
+                 o_stmp = c.take((size_t)scan_tmp_elems(ncnt) * 8 + 8),
+                 o_lb = c.take((size_t)compact_tiles(K, n_out) * 8);
     char* t1 = nullptr;
     SSC_TRY(tmp.alloc((void**)&t1, c.at));
     int32_t* counts = (int32_t*)(t1 + o_cnt);
@@ -449,20 +621,18 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     int64_t* stmp = (int64_t*)(t1 + o_stmp);
     int64_t* dtotal = stmp + scan_tmp_elems(ncnt);
     dim3 gp(nblk, K);
-    const uint64_t mask_in = (uint64_t)(rb->cap_in - 1);
     if (submanifold) {
-      const int c = (K - 1) / 2;
-      mirror_init<<<cdiv((int64_t)(K - c) * n_out, 256), 256, 0, st>>>(rb->nbr, n_out, K);
-      if (c > 0)
-        mirror_lookup_kernel<<<(unsigned)((int64_t)nblk * c), 256, 0, st>>>(rb->out_coords, n_out, ksize, grid[0],
-                                                                             grid[1], grid[2], rb->hash_in, mask_in,
-                                                                             nblk, rb->nbr);
+      // the map is complete (set above); only its pair lists are still to be sized and written
       pair_list_kernel<kCount><<<gp, 256, 0, st>>>(n_out, nblk, rb->nbr, counts, nullptr, nullptr);
     } else {
-      SSC_HIP(hipMemsetAsync(rb->nbr, 0xFF, (size_t)K * n_out * 4, st));
+      rb_init_kernel<<<cdiv((int64_t)K * n_out, 256), 256, 0, st>>>(nullptr, 0, rb->nbr, K, n_out, 0, nullptr);
       const int* go = rb->grid_out;
       scatter_neighbours<<<dim3(cdiv(n, 256), K), 256, 0, st>>>(coords, n, ksize, stride, go[0], go[1], go[2], obits,
                                                               owoff, n_out, rb->nbr);
+      if (rb->pairs) {
+        SSC_TRY(compact_pairs(rb->nbr, n_out, K, (int64_t*)(t1 + o_lb), rb->pairs, rb->pair_off_dev, st));
+        return finish_build(rb, host, st);
+      }
       pair_list_kernel<kCount><<<gp, 256, 0, st>>>(n_out, nblk, rb->nbr, counts, nullptr, nullptr);
     }
     SSC_HIP(hipGetLastError());
@@ -485,16 +655,7 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
       rb->pairs = (int32_t*)rb->mem[2];
     }
   }
-  // pair offsets and flags in one copy: the single synchronisation of a submanifold build
-  SSC_HIP(hipMemcpyAsync(host, rb->pair_off_dev, (size_t)(K + 2) * 8, hipMemcpyDeviceToHost, st));
-  SSC_HIP(hipStreamSynchronize(st));
-  for (int s = 0; s <= K; ++s) rb->pair_off[s] = host[s];
-  rb->n_pairs = host[K];
-  const int fl = (int)(host[K + 1] & 0xffffffff);
-  if (fl & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid, has b < 0, or (max b + 1) * grid volume exceeds the 32-bit key space");
-  if (fl & kFlagDup) return fail(SSCONV_E_DUPLICATE, "duplicate input site");
-  if (fl & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
-  return SSCONV_OK;
+  return finish_build(rb, host, st);
 }
 
 }  // namespace ssconv

@@ -55,8 +55,10 @@ def test_error_codes():
         assert _code(lambda: P.Rulebook(c, 8, 3)) == E_HASH_FULL
     finally:
         P.debug_set(1, 0)
-    P.debug_set(2, 2)                                   # second allocation fails
+    P.debug_set(2, 1)                                   # a submanifold build's one allocation fails
     assert _code(lambda: P.Rulebook(c, 8, 3)) == E_NOMEM
+    P.debug_set(2, 2)                                   # a stride-2 build's second allocation fails
+    assert _code(lambda: P.Rulebook(c, 8, 3, stride=2, submanifold=False)) == E_NOMEM
     P.debug_set(2, 0)
     rb = P.Rulebook(c, 8, 3)                            # library still healthy
     assert rb.n_out == len(c)
