@@ -116,7 +116,7 @@ def write_traffic_summary(args):
     ff, fw = kib / float(np.mean(cf)), kib / float(np.mean(cw))
     fk, wk = float(np.mean(fetch)), float(np.mean(write))
     traffic = (fk * ff + wk * fw) * 1024.0
-    run = (f"python3 bench.py --config {spec.index} --steps 3 --warmup 1 --no-cpu-baseline")
+    run = (f"python3 bench.py --config {spec.index} --steps 3 --warmup 1 --no-cpu-baseline --secondary 0")
     cmds = [f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {d}/fetch -o p -- {run}",
             f"rocprofv3 --pmc WRITE_SIZE --output-format csv -d {d}/write -o p -- {run}",
             f"rocprofv3 --pmc FETCH_SIZE --output-format csv -d {dc}/copy_fetch -o p -- "
@@ -315,12 +315,63 @@ class StackBench:
         self.pairs = [L.rb.n_pairs for L in self.st.layers]
         self.grad = torch.from_numpy(make_grad(spec, self.n_outs[-1], spec.layers[-1].cout)).to(dev)
 
-    def step(self):
-        self.st.forward(self.coords, self.feats)
+    def step(self, overlap=True):
+        self.st.forward(self.coords, self.feats, overlap=overlap)
         self.st.backward(self.grad, need_input_grad=False)
 
     def sites(self):
         return sum(self.n_outs)
+
+    def roofline_ms(self):
+        """The stack's roofline time: per layer, synthesis and rule book at HBM bandwidth on their
+        algorithmic bytes, each GEMM phase (forward, input-feature gradient for layers 2..5,
+        kernel gradient) at the fp32 MFMA peak on its useful FLOPs, gates at HBM bandwidth."""
+        P = self.P
+        hbm, peak = HBM_PEAK_GBS * 1e9, PEAK["f32"] * 1e12
+        t = 0.0
+        n_in = int(self.coords.shape[0])
+        for i, (L, p, n_out, lay) in enumerate(zip(self.spec.layers, self.pairs, self.n_outs, self.st.layers)):
+            K = L.ksize ** 3
+            cap = 64
+            while cap < 2 * n_in:
+                cap *= 2
+            rb_bytes = 16 * n_in + 8 * cap + 8 * n_in + 12 * n_out * K + 8 * p
+            synth_bytes = K * L.cin * L.cout * 4 + 4 * int(lay.basis.numel())
+            f = 2.0 * p * L.cin * L.cout
+            gemms = f * (3 if i > 0 else 2)
+            gate = 0
+            if L.gated:
+                c = P.n_channels(L.fields_out[:-1])
+                gate = 2 * (n_out * L.cout * 4 + n_out * c * 4)      # forward and backward
+            t += (rb_bytes + synth_bytes + gate) / hbm + gemms / peak
+            n_in = n_out
+        return t * 1e3
+
+    def serial_report(self, steps=10):
+        """Extra steps with the side stream and the backward fork off, so that no kernel overlaps
+        another: the stack's time against its roofline, and the gather-GEMM launches timed alone."""
+        torch, P = self.torch, self.P
+        P.debug_set(3, 11)
+        try:
+            self.step(overlap=False)
+            torch.cuda.synchronize()
+            P.debug_set(4, 1)
+            t0 = time.perf_counter()
+            for _ in range(steps):
+                self.step(overlap=False)
+            torch.cuda.synchronize()
+            ms = (time.perf_counter() - t0) / steps * 1e3
+            n_timed, kern_ms = P.debug_kernel_ms()
+            P.debug_set(4, 0)
+        finally:
+            P.debug_set(3, 0)
+        flops, launches = self.gather_flops(False)
+        achieved = flops * steps / (kern_ms / 1e3) / 1e12
+        roof = self.roofline_ms()
+        return {"what": "serialised steps (no side stream, no backward fork): stack forward + backward",
+                "stack": {"ms": ms, "roofline_ms": roof, "frac": roof / ms, "M_sites_per_s": self.sites() / ms / 1e3},
+                "gather_gemm": {"launches": n_timed, "avg_launch_ms": kern_ms / max(n_timed, 1),
+                                "achieved_tflops": achieved, "frac": achieved / PEAK["f32"]}}
 
     def gather_flops(self, forward_only):
         """Forward gather-GEMM of every layer plus the input-feature gradient of layers 2..5
@@ -806,7 +857,7 @@ def write_stats_summary(args):
         return re.sub(r"\(.*", "", n)[:70]
 
     steps, warmup = (bench["steps"], bench["warmup"]) if bench else (args.steps, args.warmup)
-    run = f"python3 bench.py --config {spec.index} --steps {steps} --warmup {warmup} --no-cpu-baseline"
+    run = f"python3 bench.py --config {spec.index} --steps {steps} --warmup {warmup} --no-cpu-baseline --secondary 0"
     out = [f"# rocprofv3 kernel statistics: {spec.name} ({spec.dtype}), one step = {step_text(spec)}",
            f"command: rocprofv3 --kernel-trace --stats --output-format csv -d {d} -o p -- {run} > {args.stats_log}",
            f"summary: python3 bench.py --config {spec.index} --stats-summary {d} --stats-log {args.stats_log}", "",
@@ -870,7 +921,7 @@ def write_counter_summary(args):
     cf = _per_dispatch(_counter_rows(os.path.join(dc, "copy_fetch")), COPY_KERNEL, "FETCH_SIZE")
     cw = _per_dispatch(_counter_rows(os.path.join(dc, "copy_write")), COPY_KERNEL, "WRITE_SIZE")
     ff, fw = mb * 1024.0 / float(np.mean(cf)), mb * 1024.0 / float(np.mean(cw))
-    run = f"python3 bench.py --config {spec.index} --steps 3 --warmup 1 --no-cpu-baseline"
+    run = f"python3 bench.py --config {spec.index} --steps 3 --warmup 1 --no-cpu-baseline --secondary 0"
     lines = [f"# rocprofv3 counters per kernel: {spec.name} ({spec.dtype}), one step = {step_text(spec)}",
              "commands (from the repository root, TMPDIR=/tmp, each under timeout -s KILL 120):",
              f"  rocprofv3 --pmc FETCH_SIZE --output-format csv -d {d}/fetch -o p -- {run}",
@@ -988,6 +1039,11 @@ def measure(args, i, steps, warmup, dev):
         for _ in range(10):
             b.phase_step()
         torch.cuda.synchronize()
+    if isinstance(b, StackBench) and args.only == "step":
+        out["phases"] = b.serial_report()
+        ph = out["phases"]
+        log(f"stack serialised: {ph['stack']['ms']:.3f} ms, roofline fraction {ph['stack']['frac']:.3f}; gather "
+            f"alone {ph['gather_gemm']['avg_launch_ms']:.4f} ms avg, {ph['gather_gemm']['frac']:.3f} of peak")
     if isinstance(b, (SingleLayer, BlockBench)) and b.events:
         out["phases"] = b.phase_report()
         ph = out["phases"]

@@ -125,6 +125,30 @@ def test_backward_matches_oracle(i):
     rb.close()
 
 
+def test_bf16_diagnostic_against_unrounded_inputs():
+    """Diagnostic second reference of the bf16 workload: the fp64 oracle on the fp32 features and
+    kernel before their rounding to bfloat16.  The gate stays the reference on the rounded inputs
+    (what the GPU is given); this one also contains the input quantisation.  Each rounded operand
+    is within 2^-9 of its value (relative), so a product is within about 2^-8, and the sum of
+    ~20 * 208 such products with random signs stays within a few 2^-8 of the L_inf norm."""
+    from workloads.gen import make_features
+    i = 4
+    L, dt, desc, basis, rb, W, feats = _layer_io(i)
+    out = P.forward(feats, rb, W).float().cpu().numpy()
+    rb.close()
+    want_rounded, *_ = single_layer_reference(i)
+    f32 = make_features(CONFIGS[i], len(L.coords_in), L.spec.cin, rounded=False).astype(np.float64)
+    kap = L.lay.kappa(L.coeffs, bf16=False)
+    from oracle import conv as oc
+    want_unrounded = oc.forward(f32, L.R, kap, len(L.coords_out))
+    e_gate, e_diag = rel_err(out, want_rounded), rel_err(out, want_unrounded)
+    e_inputs = rel_err(want_rounded, want_unrounded)
+    print(f"config 4 forward: vs rounded inputs {e_gate:.3e}, vs unrounded inputs {e_diag:.3e} "
+          f"(oracle rounded vs unrounded {e_inputs:.3e})", flush=True)
+    assert e_gate < TOL["bf16"]
+    assert e_diag < 4 * 2.0 ** -8
+
+
 def test_forward_backward_deterministic():
     L, dt, desc, basis, rb, W, feats = _layer_io(2)
     g = torch.randn(rb.n_out, L.spec.cout, device=DEV, generator=torch.Generator(DEV).manual_seed(0))

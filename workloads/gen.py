@@ -222,10 +222,11 @@ def round_bf16(x: np.ndarray) -> np.ndarray:
     return r.astype(np.uint32).view(np.float32).reshape(np.shape(x))
 
 
-def make_features(spec: WorkloadSpec, n: int, cin: int) -> np.ndarray:
+def make_features(spec: WorkloadSpec, n: int, cin: int, rounded: bool = True) -> np.ndarray:
+    """N(0, 1) features in fp32; rounded to bfloat16 for a bf16 workload unless rounded=False."""
     rng = np.random.default_rng(_streams(spec)["features"])
     f = rng.standard_normal((n, cin)).astype(np.float32)
-    return round_bf16(f) if spec.dtype == "bf16" else f
+    return round_bf16(f) if spec.dtype == "bf16" and rounded else f
 
 
 def make_coeffs(spec: WorkloadSpec, counts: List[int]) -> List[np.ndarray]:
