@@ -1,8 +1,15 @@
-// Ascending sort of many small buckets of int32 (the per-site entry lists of the voxelisation and
-// interpolation adjoints): one wavefront per bucket, a 64-lane bitonic network on cross-lane
-// shuffles for buckets of up to 64 entries (padding sorts last), an in-place insertion sort by
-// lane 0 beyond that.  The order of a bucket on exit is independent of the order it was filled in,
-// which makes the sums over buckets deterministic.
+// Ascending sort of many buckets of int32 (the per-site entry lists of the voxelisation and
+// interpolation adjoints).  The order of a bucket on exit is independent of the order it was
+// filled in, which makes the sums over buckets deterministic.
+//
+// Buckets of up to 64 entries: one wavefront each, a 64-lane bitonic network on cross-lane
+// shuffles (padding sorts last).  Larger buckets are appended to a list on the device and sorted
+// by a second kernel, one workgroup per bucket: the bitonic network in its all-ascending form
+// (each merge starts by comparing i with its mirror i ^ (k - 1) in the block of k, then halves
+// with i ^ j; every comparator puts the smaller value at the lower index).  In that form entries
+// past the bucket's end behave as +infinity and their comparators never swap, so they are simply
+// skipped: up to kBigLds entries the network runs in LDS, beyond that in place in global memory
+// (O(m log^2 m) either way).
 #pragma once
 
 #include "common.hpp"
@@ -10,11 +17,15 @@
 namespace ssconv {
 namespace {  // one copy per translation unit that includes this header
 
+constexpr int kBigLds = 8192;  // largest bucket sorted in LDS (32 KB)
+
 // Bucket r = a[start[r] .. start[r] + cnt[r]) for r < *n_rows (n_rows read on the device, or
-// n_rows_host when n_rows is null); four buckets per 256-thread workgroup.
+// n_rows_host when n_rows is null); four buckets per 256-thread workgroup.  A bucket of more than
+// 64 entries is appended to big[1 ..] (big[0] counts them; zero at launch).
 __global__ __launch_bounds__(256) void bucket_sort_kernel(const int64_t* __restrict__ n_rows, int64_t n_rows_host,
                                                           const int64_t* __restrict__ start,
-                                                          const int32_t* __restrict__ cnt, int32_t* __restrict__ a) {
+                                                          const int32_t* __restrict__ cnt, int32_t* __restrict__ a,
+                                                          int32_t* __restrict__ big) {
   const int lane = threadIdx.x & 63;
   const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int64_t nr = n_rows ? *n_rows : n_rows_host;
@@ -22,31 +33,90 @@ __global__ __launch_bounds__(256) void bucket_sort_kernel(const int64_t* __restr
   int32_t* b = a + start[r];
   const int m = cnt[r];
   if (m <= 1) return;
-  if (m <= 64) {
-    int32_t v = lane < m ? b[lane] : 0x7fffffff;
-#pragma unroll
-    for (int k = 2; k <= 64; k <<= 1) {
-#pragma unroll
-      for (int j = k >> 1; j > 0; j >>= 1) {
-        const int32_t p = __shfl_xor(v, j, 64);
-        const bool asc = (lane & k) == 0, lower = (lane & j) == 0;
-        v = (lower == asc) ? min(v, p) : max(v, p);
-      }
-    }
-    if (lane < m) b[lane] = v;
+  if (m > 64) {
+    if (lane == 0) big[1 + atomicAdd(big, 1)] = (int32_t)r;
     return;
   }
-  if (lane == 0) {
-    for (int j = 1; j < m; ++j) {
-      const int32_t v = b[j];
-      int k = j - 1;
-      while (k >= 0 && b[k] > v) {
-        b[k + 1] = b[k];
-        --k;
-      }
-      b[k + 1] = v;
+  int32_t v = lane < m ? b[lane] : 0x7fffffff;
+#pragma unroll
+  for (int k = 2; k <= 64; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const int32_t p = __shfl_xor(v, j, 64);
+      const bool asc = (lane & k) == 0, lower = (lane & j) == 0;
+      v = (lower == asc) ? min(v, p) : max(v, p);
     }
   }
+  if (lane < m) b[lane] = v;
+}
+
+// Comparator t (0 <= t < p2 / 2) of the stage (k, j) of the all-ascending network over p2
+// entries: j == k / 2 is the mirror stage, smaller j the half-cleaners.  Returns the pair (lo, hi).
+__device__ __forceinline__ void bitonic_pair(int64_t t, int64_t k, int64_t j, int64_t* lo, int64_t* hi) {
+  if (j == k / 2) {
+    const int64_t base = (t / j) * k, o = t % j;
+    *lo = base + o;
+    *hi = base + k - 1 - o;
+  } else {
+    *lo = (t / j) * 2 * j + t % j;
+    *hi = *lo + j;
+  }
+}
+
+// The listed large buckets, one workgroup each (the grid strides over the list).
+__global__ __launch_bounds__(256) void bucket_sort_big_kernel(const int32_t* __restrict__ big,
+                                                              const int64_t* __restrict__ start,
+                                                              const int32_t* __restrict__ cnt, int32_t* __restrict__ a) {
+  __shared__ int32_t s[kBigLds];
+  const int tid = threadIdx.x;
+  const int nbig = big[0];
+  for (int q = blockIdx.x; q < nbig; q += gridDim.x) {
+    const int64_t r = big[1 + q];
+    int32_t* b = a + start[r];
+    const int64_t m = cnt[r];
+    int64_t p2 = 128;
+    while (p2 < m) p2 <<= 1;
+    if (m <= kBigLds) {
+      for (int64_t i = tid; i < p2; i += 256) s[i] = i < m ? b[i] : 0x7fffffff;
+      __syncthreads();
+      for (int64_t k = 2; k <= p2; k <<= 1)
+        for (int64_t j = k >> 1; j > 0; j >>= 1) {
+          for (int64_t t = tid; t < p2 / 2; t += 256) {
+            int64_t lo, hi;
+            bitonic_pair(t, k, j, &lo, &hi);
+            const int32_t x = s[lo], y = s[hi];
+            if (y < x) s[lo] = y, s[hi] = x;
+          }
+          __syncthreads();
+        }
+      for (int64_t i = tid; i < m; i += 256) b[i] = s[i];
+    } else {
+      for (int64_t k = 2; k <= p2; k <<= 1)
+        for (int64_t j = k >> 1; j > 0; j >>= 1) {
+          for (int64_t t = tid; t < p2 / 2; t += 256) {
+            int64_t lo, hi;
+            bitonic_pair(t, k, j, &lo, &hi);
+            if (hi < m) {  // a comparator with an entry past the end never swaps
+              const int32_t x = b[lo], y = b[hi];
+              if (y < x) b[lo] = y, b[hi] = x;
+            }
+          }
+          __syncthreads();  // also orders this workgroup's global writes before the next stage
+        }
+    }
+    __syncthreads();  // LDS reuse by the next bucket
+  }
+}
+
+// Sorts every bucket: big must hold n_max + 1 int32 (n_max = the largest number of buckets).
+inline int sort_buckets(const int64_t* n_rows, int64_t n_rows_host, int64_t n_max, const int64_t* start,
+                        const int32_t* cnt, int32_t* a, int32_t* big, hipStream_t st) {
+  if (n_max <= 0) return SSCONV_OK;
+  SSC_HIP(hipMemsetAsync(big, 0, 4, st));
+  bucket_sort_kernel<<<cdiv(n_max, 4), 256, 0, st>>>(n_rows, n_rows_host, start, cnt, a, big);
+  bucket_sort_big_kernel<<<256, 256, 0, st>>>(big, start, cnt, a);
+  SSC_HIP(hipGetLastError());
+  return SSCONV_OK;
 }
 
 }  // namespace

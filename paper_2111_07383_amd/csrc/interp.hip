@@ -206,7 +206,7 @@ extern "C" int ssconv_interpolate_backward(ssconv_rulebook_t rb, const float* gr
   auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
   const size_t o_w = up(ne * 4), o_cnt = o_w + up(ne * 4), o_fill = o_cnt + up(n * 4), o_start = o_fill + up(n * 4);
   const size_t o_ent = o_start + up(n * 8), o_tmp = o_ent + up(ne * 4);
-  const size_t total = o_tmp + up((size_t)(scan_tmp_elems(n) + 1) * 8);
+  const size_t o_big = o_tmp + up((size_t)(scan_tmp_elems(n) + 1) * 8), total = o_big + up((n + 1) * 4);
   char* ws = nullptr;
   SSC_TRY(dev_alloc((void**)&ws, total, stream));
   int32_t* rows = (int32_t*)ws;
@@ -216,6 +216,7 @@ extern "C" int ssconv_interpolate_backward(ssconv_rulebook_t rb, const float* gr
   int64_t* start = (int64_t*)(ws + o_start);
   int32_t* ent = (int32_t*)(ws + o_ent);
   int64_t* tmp = (int64_t*)(ws + o_tmp);
+  int32_t* big = (int32_t*)(ws + o_big);
   auto run = [&]() -> int {
     SSC_HIP(hipMemsetAsync(cnt, 0, (size_t)n * 4, stream));
     SSC_HIP(hipMemsetAsync(fillc, 0, (size_t)n * 4, stream));
@@ -223,7 +224,7 @@ extern "C" int ssconv_interpolate_backward(ssconv_rulebook_t rb, const float* gr
     interp_count_kernel<<<cdiv(ne, 256), 256, 0, stream>>>(rows, ne, cnt);
     SSC_TRY(exclusive_scan(cnt, n, start, tmp + scan_tmp_elems(n), tmp, stream));
     interp_fill_kernel<<<cdiv(ne, 256), 256, 0, stream>>>(rows, ne, start, fillc, ent);
-    bucket_sort_kernel<<<cdiv(n, 4), 256, 0, stream>>>(nullptr, n, start, cnt, ent);
+    SSC_TRY(sort_buckets(nullptr, n, n, start, cnt, ent, big, stream));
     if (channels % 4 == 0 && aligned16(grad) && aligned16(grad_feats))
       interp_bwd_kernel<4><<<cdiv(n * channels / 4, 256), 256, 0, stream>>>(grad, channels, wts, start, cnt, ent, n,
                                                                             grad_feats);

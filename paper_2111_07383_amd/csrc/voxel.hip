@@ -137,7 +137,7 @@ extern "C" int ssconv_voxelize(const float* points, const int32_t* batch, const 
   const size_t o_key = o_stmp + up((size_t)(scan_tmp_elems(std::max<int64_t>(nw, n)) + 2) * 8);
   const size_t o_row = o_key + up(n * 4), o_cnt = o_row + up(n * 4), o_fill = o_cnt + up(n * 4);
   const size_t o_start = o_fill + up(n * 4), o_idx = o_start + up(n * 8), o_flags = o_idx + up(n * 4);
-  const size_t total_b = o_flags + 256;
+  const size_t o_big = o_flags + 256, total_b = o_big + up((n + 1) * 4);
   char* ws = nullptr;
   SSC_TRY(dev_alloc((void**)&ws, total_b, st));
   uint32_t* bits = (uint32_t*)(ws + o_bits);
@@ -152,6 +152,7 @@ extern "C" int ssconv_voxelize(const float* points, const int32_t* batch, const 
   int64_t* start = (int64_t*)(ws + o_start);
   int32_t* idx = (int32_t*)(ws + o_idx);
   int* flags = (int*)(ws + o_flags);
+  int32_t* big = (int32_t*)(ws + o_big);
 
   int rc = SSCONV_OK;
   auto run = [&]() -> int {
@@ -168,7 +169,7 @@ extern "C" int ssconv_voxelize(const float* points, const int32_t* batch, const 
       // rows past the site count have zero counts, so the scan over n rows is exact
       SSC_TRY(exclusive_scan(cnt, n, start, d_pts, stmp, st));
       vox_fill_kernel<<<cdiv(n, 256), 256, 0, st>>>(prow, n, start, fillc, idx);
-      bucket_sort_kernel<<<cdiv(n, 4), 256, 0, st>>>(d_sites, 0, start, cnt, idx);
+      SSC_TRY(sort_buckets(d_sites, 0, n, start, cnt, idx, big, st));
       vox_mean_kernel<<<cdiv(n * channels, 256), 256, 0, st>>>(feats, channels, d_sites, start, cnt, idx, feats_out);
     }
     SSC_HIP(hipGetLastError());

@@ -70,3 +70,15 @@ def test_interp_empty_and_deterministic():
     a = [P.interpolate_backward(rb, g, pts) for _ in range(2)]
     assert torch.equal(a[0], a[1])
     rb.close()
+
+
+def test_interp_crowded_sites():
+    """A few sites, each touched by thousands of (point, corner) entries: the adjoint's bucket sort
+    beyond one wavefront (in LDS and, above 8192 entries, in global memory)."""
+    coords = np.array([[0, 4, 4, 4], [0, 4, 4, 5], [0, 4, 5, 4], [0, 5, 4, 4], [0, 5, 5, 5]], np.int32)
+    rng = np.random.default_rng(3)
+    for m in (3000, 20000):
+        pts = rng.uniform(4.2, 5.8, (m, 3)).astype(np.float32)
+        feats = rng.standard_normal((len(coords), 4)).astype(np.float32)
+        grad = rng.standard_normal((m, 4)).astype(np.float32)
+        _check(coords, 8, feats, pts, None, grad)

@@ -54,7 +54,9 @@ def test_object_clouds_rgb1():
     (5000, 4, 16, 0.37, (-0.3, 0.1, -2.0), 3),             # voxel not a power of two
     (20000, 0, 32, 1.0, (0.0, 0.0, 0.0), 4),               # coordinates only
     (3000, 2, 4, 8.0, (0.0, 0.0, 0.0), 1),                 # many points per cell
-    (2000, 3, 2, 16.0, (0.0, 0.0, 0.0), 1),                # hundreds per cell: the in-memory sort
+    (2000, 3, 2, 16.0, (0.0, 0.0, 0.0), 1),                # hundreds per cell: the workgroup sort in LDS
+    (20000, 2, 2, 16.0, (0.0, 0.0, 0.0), 1),               # ~2500 per cell: LDS sort of up to 8192 entries
+    (60000, 1, 1, 40.0, (0.0, 0.0, 0.0), 1),               # ~60 000 in one cell: the sort in global memory
 ])
 def test_random_clouds(n, C, grid, voxel, origin, nbatch):
     rng = np.random.default_rng(n + C)
