@@ -140,6 +140,15 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
   const __amdgpu_buffer_rsrc_t x_rsrc = isF ? f_rsrc : g_rsrc;
   const uint32_t x_rowb = (uint32_t)(isF ? cin : cout) * 2u;
   const uint32_t x_stat = (uint32_t)(isF ? n0 : m0) * 2u + 16u * (uint32_t)(jb + C::H * (lane >> 5));
+  // DMA q of this lane fetches channels (isF ? n0 : m0) + 8 (jb + q + H (lane / 32)) .. + 7; a granule
+  // past the operand's channels (the tile is padded to 32 W) is not fetched (offset past the end:
+  // zeros; the products it feeds are never stored)
+  uint32_t gvalid = 0;
+  {
+    const int ch = isF ? cin : cout, c0 = (isF ? n0 : m0) + 8 * (jb + C::H * (lane >> 5));
+#pragma unroll
+    for (int q = 0; q < C::PW; ++q) gvalid |= (c0 + 8 * q < ch ? 1u : 0u) << q;
+  }
   const uint32_t m0_base = stage0 + (isF ? C::OPB : 0) + jb * C::BLK;  // + stage * STAGE + q * BLK
   const uint32_t p_ent = (uint32_t)prow * 8u + (isF ? 4u : 0u);        // this lane's index in a chunk's pairs
 
@@ -165,7 +174,8 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
 
   // DMA q of this wavefront (block jb + q) into stage k_, from row offset ro_.  The MUBUF
   // immediate offset 16 q is added to the LDS address as well, so M0 is set 16 q bytes lower.
-#define SSK_DMA(q_, ro_, k_) dma16_buf_q(q_, x_rsrc, ro_, m0_base + (k_) * C::STAGE + (q_) * (C::BLK - 16))
+#define SSK_DMA(q_, ro_, k_)                                                                        \
+  dma16_buf_q(q_, x_rsrc, ((gvalid >> (q_)) & 1u) ? (ro_) : kAbsent, m0_base + (k_) * C::STAGE + (q_) * (C::BLK - 16))
 
   // operands of the chunk in stage k_ via transpose reads: rows 8g + 4h + L/4, channel
   // (wm * W + i) * 16 + 4 (L % 4) -> granule column 2 (wm * W + i) + (L % 4) / 2, i.e. block
