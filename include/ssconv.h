@@ -245,6 +245,25 @@ int ssconv_norm_forward(const ssconv_fields* fields /*host*/, const void* x, ssc
 int ssconv_norm_backward(const ssconv_fields* fields /*host*/, const void* x, const void* dy, ssconv_dtype dtype,
                          int64_t n, double eps, void* dx, hipStream_t stream);
 
+/* ---- convolution followed by the steerable normalisation (Sec. 3.2.3, Alg. 1
+ * feature update, then Sec. 3.3, Eq. 11) ----------------------------------------
+ * y = ssconv_forward(feats, W) and z = the Norm of y over fields_out, as
+ * ssconv_forward followed by ssconv_norm_forward(fields_out, y, eps, z) compute
+ * them: y is the same (bit for bit), z agrees up to the order of the fp64
+ * statistics sums.  The Norm's per-channel sums come out of the kernel that
+ * writes y (per row tile of the output-stationary kernels, per row block of the
+ * pair-list and offset-split reduces), so y is not read back before the
+ * elementwise Norm step; the generic fallback kernel leaves none, and a
+ * separate statistics pass then runs.  cout = channels of fields_out (1..1024);
+ * feats [n_in, cin], W [ksize^3, cout, cin], y and z [n_out, cout], all in
+ * `dtype`, 16-byte aligned.  z may alias y (y is then overwritten by z); y
+ * stays the input of ssconv_norm_backward.  n_out = 0 is a no-op.  Temporary
+ * sums come from the library's device memory cache.
+ * Errors: as ssconv_forward and ssconv_norm_forward. */
+int ssconv_forward_norm(const void* feats, ssconv_dtype dtype, int cin, ssconv_rulebook_t rb, const void* W,
+                        const ssconv_fields* fields_out /*host*/, double eps, void* y, void* z,
+                        hipStream_t stream);
+
 /* ---- sparse average pooling (Sec. 3.1, footnote: downsampling is a stride-1
  * convolution followed by average pooling) -----------------------------------
  * rb must be built with ksize = 2, stride = 2, submanifold = 0: its offsets

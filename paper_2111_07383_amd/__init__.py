@@ -18,6 +18,7 @@ from .binding import (  # noqa: F401
     empty_cache,
     forward,
     forward_noalloc,
+    forward_norm,
     NOALLOC_SCRATCH_BYTES,
     gate_backward,
     gate_forward,

@@ -52,6 +52,8 @@ SIGNATURES = {
     "ssconv_gate_forward": (c_int, [POINTER(Fields), c_void_p, c_int, c_int64, c_void_p, c_void_p]),
     "ssconv_gate_backward": (c_int, [POINTER(Fields), c_void_p, c_void_p, c_int, c_int64, c_void_p, c_void_p]),
     "ssconv_norm_forward": (c_int, [POINTER(Fields), c_void_p, c_int, c_int64, c_double, c_void_p, c_void_p]),
+    "ssconv_forward_norm": (c_int, [c_void_p, c_int, c_int, c_void_p, c_void_p, POINTER(Fields), c_double, c_void_p,
+                                    c_void_p, c_void_p]),
     "ssconv_norm_backward": (c_int, [POINTER(Fields), c_void_p, c_void_p, c_int, c_int64, c_double, c_void_p,
                                      c_void_p]),
     "ssconv_pool_forward": (c_int, [c_void_p, c_int, c_int, c_void_p, c_void_p, c_void_p]),

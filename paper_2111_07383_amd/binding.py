@@ -280,6 +280,29 @@ def norm_forward(fields: FieldList, x: torch.Tensor, eps: float = NORM_EPS, out:
     return out
 
 
+def forward_norm(feats: torch.Tensor, rb: Rulebook, W: torch.Tensor, fields_out: FieldList, eps: float = NORM_EPS,
+                 y: Optional[torch.Tensor] = None, z: Optional[torch.Tensor] = None, stream=None):
+    """ssconv_forward_norm: (y, z) = (forward(feats), norm_forward(fields_out, y)), the Norm's
+    statistics taken by the kernel that writes y.  z may be y (then y is overwritten)."""
+    _need(feats, "feats")
+    _need(W, "W", feats.dtype)
+    K, cout, cin = W.shape
+    if feats.shape != (rb.n_in, cin):
+        raise ValueError(f"feats must be [{rb.n_in}, {cin}]")
+    if cout != n_channels(fields_out):
+        raise ValueError(f"W has {cout} output channels; fields_out has {n_channels(fields_out)}")
+    if y is None:
+        y = torch.empty((rb.n_out, cout), dtype=feats.dtype, device=feats.device)
+    if z is None:
+        z = torch.empty_like(y)
+    _need(y, "y", feats.dtype, (rb.n_out, cout))
+    _need(z, "z", feats.dtype, (rb.n_out, cout))
+    f = make_fields(fields_out)
+    check(lib().ssconv_forward_norm(_ptr(feats), _dtype(feats), cin, rb.handle, _ptr(W), byref(f), float(eps), _ptr(y),
+                                    _ptr(z), _stream(stream)), "ssconv_forward_norm")
+    return y, z
+
+
 def norm_backward(fields: FieldList, x: torch.Tensor, dy: torch.Tensor, eps: float = NORM_EPS,
                   stream=None) -> torch.Tensor:
     _need(x, "x")

@@ -3,6 +3,7 @@
 #include <mutex>
 
 #include "conv.hpp"
+#include "norm.hpp"
 #include "synth.hpp"
 
 using namespace ssconv;
@@ -32,6 +33,19 @@ extern "C" int ssconv_forward(const void* feats, ssconv_dtype dtype, int cin, ss
     return SSCONV_OK;
   }
   return conv_forward(feats, dtype, cin, rb, W, cout, out, stream);
+}
+
+extern "C" int ssconv_forward_norm(const void* feats, ssconv_dtype dtype, int cin, ssconv_rulebook_t rb,
+                                   const void* W, const ssconv_fields* fields_out, double eps, void* y, void* z,
+                                   hipStream_t stream) {
+  if (!fields_out) return fail(SSCONV_E_INVALID, "NULL field table");
+  FieldTab f;
+  SSC_TRY(norm_check_fields(fields_out, dtype, rb ? rb->n_out : 0, eps, &f));
+  const int cout = f.ch0[f.n];
+  SSC_TRY(check_conv_args(feats, y, dtype, cin, cout, rb, W));
+  if (z && !aligned16(z)) return fail(SSCONV_E_INVALID, "device buffers must be 16-byte aligned");
+  if ((rb->n_in > 0 && !feats) || (rb->n_out > 0 && (!y || !z))) return fail(SSCONV_E_INVALID, "NULL feature buffer");
+  return conv_forward_norm(feats, dtype, cin, rb, W, cout, f, eps, y, z, stream);
 }
 
 // ---------------------------------------------------------------------------

@@ -22,6 +22,7 @@
 #include <algorithm>
 
 #include "conv.hpp"
+#include "norm.hpp"
 #include "gather_mfma.hpp"
 #include "kgrad_mfma.hpp"
 
@@ -289,10 +290,10 @@ int pick_wnb(int cb) {
 
 template <typename T>
 int dispatch_gg(const void* src, int64_t n_src, int ca, const void* Bt, int cb, const int32_t* nbr, int64_t n_rows, int K,
-                void* out, hipStream_t st, CallScratch* sc = nullptr) {
+                void* out, hipStream_t st, CallScratch* sc = nullptr, NormSink* sink = nullptr) {
   const ssconv_dtype dt = sizeof(T) == 4 ? SSCONV_F32 : SSCONV_BF16;
   if (gather_mfma_supported(dt, ca, cb, K))
-    return gather_mfma(src, n_src, dt, ca, Bt, cb, nbr, nullptr, n_rows, K, out, st, sc);
+    return gather_mfma(src, n_src, dt, ca, Bt, cb, nbr, nullptr, n_rows, K, out, st, sc, sink);
   switch (pick_wnb(cb)) {
     case 1: launch_gg<T, 1>(src, ca, Bt, cb, nbr, n_rows, K, out, st); break;
     case 2: launch_gg<T, 2>(src, ca, Bt, cb, nbr, n_rows, K, out, st); break;
@@ -352,7 +353,7 @@ struct KernelTimer {
 };
 
 int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_rulebook* rb, const void* W, int cout,
-                 void* out, hipStream_t st, CallScratch* sc) {
+                 void* out, hipStream_t st, CallScratch* sc, NormSink* sink) {
   if (rb->n_out == 0) return SSCONV_OK;
   // the pair-list path needs its Y buffer; with a fixed scratch region too small for it the
   // output-stationary kernel runs instead (same sums, another order of the fp32 additions)
@@ -363,14 +364,14 @@ int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_ruleb
     int rc;
     {
       KernelTimer timer(st);
-      rc = pair_gemm(feats, cin, W, cout, rb, 1, out, rb->n_out, ws, st);
+      rc = pair_gemm(feats, cin, W, cout, rb, 1, out, rb->n_out, ws, st, sink);
     }
     scratch_give(sc, ws, st);
     return rc;
   }
   if (dt == SSCONV_F32) {
     KernelTimer timer(st);
-    return dispatch_gg<float>(feats, rb->n_in, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st, sc);
+    return dispatch_gg<float>(feats, rb->n_in, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st, sc, sink);
   }
   if (use_bf16_kernel(dt, rb->n_in, cin, cout, rb->K)) {
     // kappa packed for the bf16 kernel in a stream-ordered scratch buffer
@@ -379,13 +380,42 @@ int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_ruleb
     int rc = pack_b_bf16(W, rb->K, cin, cout, false, false, Bp, st);
     if (rc == SSCONV_OK) {
       KernelTimer timer(st);
-      rc = gather_bf16(feats, rb->n_in, cin, Bp, cout, rb->nbr, nullptr, rb->n_out, rb->K, out, st);
+      rc = gather_bf16(feats, rb->n_in, cin, Bp, cout, rb->nbr, nullptr, rb->n_out, rb->K, out, st, sink);
     }
     scratch_give(sc, Bp, st);
     return rc;
   }
   KernelTimer timer(st);
-  return dispatch_gg<uint16_t>(feats, rb->n_in, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st, sc);
+  return dispatch_gg<uint16_t>(feats, rb->n_in, cin, W, cout, rb->nbr, rb->n_out, rb->K, out, st, sc, sink);
+}
+
+// The convolution with the Norm of its output (Sec. 3.3, Eq. 11).  The kernel that writes y also
+// leaves its per-channel sums (the output-stationary kernels per row tile, the pair-list and
+// offset-split reduces per row block), so the Norm needs no pass of its own over y before the
+// elementwise one; the other paths (the generic fallback kernel, an input set without rows) leave
+// none and the separate statistics pass runs instead.
+int conv_forward_norm(const void* feats, ssconv_dtype dt, int cin, const ssconv_rulebook* rb, const void* W, int cout,
+                      const FieldTab& f, double eps, void* y, void* z, hipStream_t st) {
+  const int64_t n = rb->n_out;
+  if (n == 0) return SSCONV_OK;
+  NormSink sink;
+  sink.C = cout;
+  int rc;
+  if (rb->n_in == 0) {
+    rc = hipMemsetAsync(y, 0, (size_t)n * cout * dtype_bytes(dt), st) == hipSuccess
+             ? SSCONV_OK
+             : fail(SSCONV_E_HIP, "clearing the output failed");
+  } else {
+    rc = conv_forward(feats, dt, cin, rb, W, cout, y, st, nullptr, &sink);
+  }
+  if (rc == SSCONV_OK && sink.nblk == 0) {
+    const NormStatsPlan p = norm_stats_plan(n, cout);
+    rc = norm_sink_take(&sink, p.nblk, st);
+    if (rc == SSCONV_OK) rc = norm_forward_sums(dt, y, n, p, sink.ws, st);
+  }
+  if (rc == SSCONV_OK) rc = norm_forward_finish(f, dt, y, n, eps, sink.nblk, sink.ws, z, st);
+  if (sink.ws) dev_free(sink.ws, st);
+  return rc;
 }
 
 int dw_nsplit(const ssconv_rulebook* rb) {

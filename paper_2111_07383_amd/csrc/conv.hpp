@@ -5,6 +5,8 @@
 
 namespace ssconv {
 
+struct NormSink;
+
 struct BwdLayout {
   size_t nbrT = 0, Wt = 0, part = 0, dW = 0, pair = 0, total = 0;  // byte offsets in the workspace
   int nsplit = 1;
@@ -15,12 +17,17 @@ struct BwdLayout {
 bool pair_path_supported(const ssconv_rulebook* rb, ssconv_dtype dt, int ca, int cb);
 bool pair_path_wins(const ssconv_rulebook* rb, ssconv_dtype dt, int ca, int cb, int64_t n_dst);
 size_t pair_path_bytes(const ssconv_rulebook* rb, int ca, int cb, int64_t n_dst);
+// sink (optional): the reduce pass also leaves the Norm statistics of dst there (norm.hpp).
 int pair_gemm(const void* src, int ca, const void* Bt, int cb, const ssconv_rulebook* rb, int sel_in, void* dst,
-              int64_t n_dst, void* ws, hipStream_t st);
+              int64_t n_dst, void* ws, hipStream_t st, NormSink* sink = nullptr);
 
-// sc: where the call's scratch comes from (nullptr: the device memory cache).
+// sc: where the call's scratch comes from (nullptr: the device memory cache).  sink (optional):
+// the kernel that writes out also leaves the Norm statistics of out there where it can.
 int conv_forward(const void* feats, ssconv_dtype dt, int cin, const ssconv_rulebook* rb, const void* W, int cout,
-                 void* out, hipStream_t st, CallScratch* sc = nullptr);
+                 void* out, hipStream_t st, CallScratch* sc = nullptr, NormSink* sink = nullptr);
+// y = the convolution, z = Norm(y) over the fields f of the output channels (z may alias y).
+int conv_forward_norm(const void* feats, ssconv_dtype dt, int cin, const ssconv_rulebook* rb, const void* W, int cout,
+                      const FieldTab& f, double eps, void* y, void* z, hipStream_t st);
 BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout);
 int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout, const ssconv_rulebook* rb,
                         const void* W, void* grad_feats, char* ws, const BwdLayout& L, hipStream_t st);

@@ -28,6 +28,7 @@
 //   * the epilogue stages each wavefront's rows in LDS and writes 16-byte pieces of rows.
 #include "gather_mfma.hpp"
 #include "lds_dma.hpp"
+#include "norm.hpp"
 
 namespace ssconv {
 namespace {
@@ -78,12 +79,12 @@ __device__ __forceinline__ void dma16_buf(__amdgpu_buffer_rsrc_t rsrc, uint32_t 
 }
 #pragma clang diagnostic pop
 
-template <int NB>
+template <int NB, bool kStats>
 __global__ __launch_bounds__(kNT) void gather_bf16_kernel(const uint16_t* __restrict__ src, int64_t src_bytes, int ca,
                                                           const uint16_t* __restrict__ Bp, int cb,
                                                           const int32_t* __restrict__ nbr,
                                                           const int32_t* __restrict__ order, int64_t n_pos, int K,
-                                                          uint16_t* __restrict__ out) {
+                                                          uint16_t* __restrict__ out, double* __restrict__ stats) {
   using G = GB<NB>;
   constexpr int WN0 = G::WN0, WN1 = G::WN1, L = G::L;
   extern __shared__ __attribute__((aligned(16))) char smem[];
@@ -384,6 +385,53 @@ __global__ __launch_bounds__(kNT) void gather_bf16_kernel(const uint16_t* __rest
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
+  if constexpr (kStats) {
+    // Norm statistics of the stored (bf16) values, per column of the tile: each lane adds its 16
+    // rows in row order, the four lane groups are added pairwise (the same sum in every lane),
+    // then the four row groups in order; stats[(col * row tiles + row tile) * 2 + q] in fp64
+    static_assert(4 * NB * 16 * 16 <= kD * G::STAGE, "the statistics exchange must fit the stage area");
+    __syncthreads();  // every wavefront is done with its staged rows
+    double* red = reinterpret_cast<double*>(stages);  // [4 row groups][NB * 16 columns][2]
+#pragma unroll
+    for (int nb = 0; nb < WN0; ++nb) {
+      if (nb >= nbc) break;
+      double s1 = 0.0, s2 = 0.0;
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t p = p0 + 64 * wm + 16 * mb + 4 * g + i;
+          if (p < n_pos) {
+            const double v = bf16_to_f32(f32_to_bf16_rne(acc[mb][nb][i]));
+            s1 += v;
+            s2 = fma(v, v, s2);
+          }
+        }
+      s1 += __shfl_xor(s1, 16, 64);
+      s2 += __shfl_xor(s2, 16, 64);
+      s1 += __shfl_xor(s1, 32, 64);
+      s2 += __shfl_xor(s2, 32, 64);
+      if (g == 0) {
+        const int c = 16 * WN0 * wn + 16 * nb + r16;
+        red[(wm * NB * 16 + c) * 2] = s1;
+        red[(wm * NB * 16 + c) * 2 + 1] = s2;
+      }
+    }
+    __syncthreads();
+    const int64_t mt = t / gridDim.y;
+    for (int c = tid; c < NB * 16; c += kNT) {
+      const int col = n0 + c;
+      if (col >= cb) continue;
+      double a = 0.0, b = 0.0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        a += red[(j * NB * 16 + c) * 2];
+        b += red[(j * NB * 16 + c) * 2 + 1];
+      }
+      stats[((int64_t)col * gridDim.x + mt) * 2] = a;
+      stats[((int64_t)col * gridDim.x + mt) * 2 + 1] = b;
+    }
+  }
 }
 
 // Bp[s][k/8][n][k%8] from kappa given as Bt[s'][n][k] (transposed = 0) or as W[s'][k][n]
@@ -411,13 +459,18 @@ __global__ void pack_b_kernel(const uint16_t* __restrict__ W, int K, int ca, int
 
 template <int NB>
 int launch_bf16(const void* src, int64_t src_bytes, int ca, const void* Bp, int cb, const int32_t* nbr, const int32_t* order,
-                int64_t n_pos, int K, void* out, hipStream_t st) {
+                int64_t n_pos, int K, void* out, hipStream_t st, NormSink* sink) {
   const size_t smem = bf16_smem<NB>(K);
-  auto kern = gather_bf16_kernel<NB>;
+  auto kern = sink ? gather_bf16_kernel<NB, true> : gather_bf16_kernel<NB, false>;
   SSC_HIP(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem));
   dim3 grid(cdiv(n_pos, kBM), cdiv(cb, NB * 16));
+  double* stats = nullptr;
+  if (sink) {
+    SSC_TRY(norm_sink_take(sink, grid.x, st));
+    stats = (double*)sink->ws;
+  }
   kern<<<grid, kNT, smem, st>>>((const uint16_t*)src, src_bytes, ca, (const uint16_t*)Bp, cb, nbr, order, n_pos, K,
-                                (uint16_t*)out);
+                                (uint16_t*)out, stats);
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;
 }
@@ -458,16 +511,16 @@ int pack_b_bf16(const void* W, int K, int ca, int cb, bool transposed, bool mirr
 }
 
 int gather_bf16(const void* src, int64_t n_src, int ca, const void* Bp, int cb, const int32_t* nbr,
-                const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st) {
+                const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st, NormSink* sink) {
   if (n_pos == 0) return SSCONV_OK;
   if (!gather_bf16_supported(n_src, ca, cb, K))
     return fail(SSCONV_E_INVALID, "bf16 gather kernel does not support this shape (K=%d)", K);
   const int64_t sb = n_src * ca * 2;
   switch (bf16_nb(cb)) {
-    case 4: return launch_bf16<4>(src, sb, ca, Bp, cb, nbr, order, n_pos, K, out, st);
-    case 8: return launch_bf16<8>(src, sb, ca, Bp, cb, nbr, order, n_pos, K, out, st);
-    case 13: return launch_bf16<13>(src, sb, ca, Bp, cb, nbr, order, n_pos, K, out, st);
-    default: return launch_bf16<14>(src, sb, ca, Bp, cb, nbr, order, n_pos, K, out, st);
+    case 4: return launch_bf16<4>(src, sb, ca, Bp, cb, nbr, order, n_pos, K, out, st, sink);
+    case 8: return launch_bf16<8>(src, sb, ca, Bp, cb, nbr, order, n_pos, K, out, st, sink);
+    case 13: return launch_bf16<13>(src, sb, ca, Bp, cb, nbr, order, n_pos, K, out, st, sink);
+    default: return launch_bf16<14>(src, sb, ca, Bp, cb, nbr, order, n_pos, K, out, st, sink);
   }
 }
 

@@ -29,6 +29,7 @@
 // takes channels 8g..8g+7, one per step), bf16 v_mfma_f32_16x16x32_bf16 (one
 // step; lane group g supplies channels 8g..8g+7).
 #include "gather_mfma.hpp"
+#include "norm.hpp"
 #include "lds_dma.hpp"
 
 namespace ssconv {
@@ -84,12 +85,13 @@ __device__ __forceinline__ int ix_get(IX v) {
   return (int)v;
 }
 
-template <typename T, int WMB, int WNB, int S, int NW, typename IX>
+template <typename T, int WMB, int WNB, int S, int NW, typename IX, bool kStats>
 __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restrict__ src, int ca,
                                                           const T* __restrict__ Bt, int cb,
                                                           const int32_t* __restrict__ nbr,
                                                           const int32_t* __restrict__ order, int64_t n_pos, int K,
-                                                          T* __restrict__ out, float* __restrict__ part) {
+                                                          T* __restrict__ out, float* __restrict__ part,
+                                                          double* __restrict__ stats) {
   using SH = Shape<T, WMB, WNB, S, NW>;
   constexpr int BM = SH::BM, RV = SH::RV, VE = SH::VE, BJ = SH::BJ, L = SH::L;
   // dynamic LDS only (base at LDS address 0): stages | junk | bmask | act | count | index table
@@ -312,6 +314,49 @@ __global__ __launch_bounds__(64 * NW) void gather_mfma_kernel(const T* __restric
       }
     }
   }
+  if constexpr (kStats) {
+    // Norm statistics of the stored values, per column of the tile: each lane adds its rows in
+    // row order, the four lane groups are added pairwise (the same sum in every lane), then the
+    // wavefronts in wavefront order; stats[(col * row tiles + row tile) * 2 + q] in fp64
+    static_assert(NW * SH::BN * 16 <= S * SH::STAGE, "the statistics exchange must fit the stage area");
+    __syncthreads();  // every wavefront is past its last read of the stage area
+    double* red = reinterpret_cast<double*>(stages);  // [NW][BN][2]
+#pragma unroll
+    for (int nb = 0; nb < WNB; ++nb) {
+      double s1 = 0.0, s2 = 0.0;
+#pragma unroll
+      for (int mb = 0; mb < WMB; ++mb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t p = p0 + 16 * (w * WMB + mb) + 4 * g + i;
+          if (p < n_pos) {
+            const double v = DT<T>::to_f(DT<T>::from_f(acc[mb][nb][i]));
+            s1 += v;
+            s2 = fma(v, v, s2);
+          }
+        }
+      s1 += __shfl_xor(s1, 16, 64);
+      s2 += __shfl_xor(s2, 16, 64);
+      s1 += __shfl_xor(s1, 32, 64);
+      s2 += __shfl_xor(s2, 32, 64);
+      if (g == 0) {
+        red[(w * SH::BN + 16 * nb + r16) * 2] = s1;
+        red[(w * SH::BN + 16 * nb + r16) * 2 + 1] = s2;
+      }
+    }
+    __syncthreads();
+    for (int c = tid; c < SH::BN; c += SH::NT) {
+      const int col = n0 + c;
+      if (col >= cb) continue;
+      double a = 0.0, b = 0.0;
+      for (int j = 0; j < NW; ++j) {
+        a += red[(j * SH::BN + c) * 2];
+        b += red[(j * SH::BN + c) * 2 + 1];
+      }
+      stats[((int64_t)col * gridDim.x + blockIdx.x) * 2] = a;
+      stats[((int64_t)col * gridDim.x + blockIdx.x) * 2 + 1] = b;
+    }
+  }
 }
 
 // out[order ? order[p] : p][col] = sum over the splits, in split order, of part[z][p][col].
@@ -326,6 +371,31 @@ __global__ __launch_bounds__(256) void split_reduce_kernel(const float* __restri
   for (int z = 1; z < nsplit; ++z) acc += part[(int64_t)z * n + e];
   const int64_t p = e / cb, col = e - p * cb;
   out[(order ? order[p] : p) * cb + col] = DT<T>::from_f(acc);
+}
+
+// The same sums in row blocks (the layout of stats_rows), with the Norm statistics of what it writes.
+template <typename T, int VEC>
+__global__ __launch_bounds__(kStatsThreads) void split_reduce_stats_kernel(const float* __restrict__ part, int nsplit,
+                                                                           int64_t n_pos, int cb,
+                                                                           const int32_t* __restrict__ order, int G,
+                                                                           int64_t rpb, T* __restrict__ out,
+                                                                           double* __restrict__ stats) {
+  const int64_t n = n_pos * cb;
+  stats_rows<VEC>(
+      cb, n_pos, G, rpb,
+      [&](int64_t p, int v, float* val) {
+        const int64_t e = p * cb + v * VEC;
+        T* o = out + (order ? order[p] : p) * cb + v * VEC;
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+          float acc = part[e + k];
+          for (int z = 1; z < nsplit; ++z) acc += part[(int64_t)z * n + e + k];
+          const T q = DT<T>::from_f(acc);
+          o[k] = q;
+          val[k] = DT<T>::to_f(q);
+        }
+      },
+      stats);
 }
 
 template <typename T, int WMB, int WNB, int S, int NW, typename IX>
@@ -351,31 +421,56 @@ int pick_nsplit(int64_t tiles, int K) {
 
 template <typename T, int WMB, int WNB, int S, int NW, typename IX>
 int launch(const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, const int32_t* order, int64_t n_pos,
-           int K, void* out, hipStream_t st, CallScratch* sc) {
+           int K, void* out, hipStream_t st, CallScratch* sc, NormSink* sink) {
   using SH = Shape<T, WMB, WNB, S, NW>;
   const size_t smem = smem_bytes<T, WMB, WNB, S, NW, IX>(K);
-  auto kern = gather_mfma_kernel<T, WMB, WNB, S, NW, IX>;
-  SSC_HIP(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem));
   const int64_t mt = cdiv(n_pos, SH::BM), nt = cdiv(cb, SH::BN);
   int nsplit = debug_gather_variant() == 8 ? std::min(K, 3) : pick_nsplit(mt * nt, K);
   if (sc && sc->fixed())
     while (nsplit > 1 && (size_t)nsplit * n_pos * cb * 4 > sc->left()) --nsplit;
+  if (nsplit == 1 && sink) {  // the tiles also sum the Norm statistics of what they write
+    auto kern = gather_mfma_kernel<T, WMB, WNB, S, NW, IX, true>;
+    SSC_HIP(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem));
+    SSC_TRY(norm_sink_take(sink, mt, st));
+    kern<<<dim3(mt, nt, 1), SH::NT, smem, st>>>((const T*)src, ca, (const T*)Bt, cb, nbr, order, n_pos, K, (T*)out,
+                                                 nullptr, (double*)sink->ws);
+    SSC_HIP(hipGetLastError());
+    return SSCONV_OK;
+  }
+  auto kern = gather_mfma_kernel<T, WMB, WNB, S, NW, IX, false>;
+  SSC_HIP(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)smem));
   if (nsplit == 1) {
     kern<<<dim3(mt, nt, 1), SH::NT, smem, st>>>((const T*)src, ca, (const T*)Bt, cb, nbr, order, n_pos, K, (T*)out,
-                                                 nullptr);
+                                                 nullptr, nullptr);
     SSC_HIP(hipGetLastError());
     return SSCONV_OK;
   }
   float* part = nullptr;
   SSC_TRY(scratch_take(sc, (void**)&part, (size_t)nsplit * n_pos * cb * 4, st));
   kern<<<dim3(mt, nt, nsplit), SH::NT, smem, st>>>((const T*)src, ca, (const T*)Bt, cb, nbr, order, n_pos, K,
-                                                    (T*)out, part);
+                                                    (T*)out, part, nullptr);
   hipError_t e = hipGetLastError();
-  if (e == hipSuccess) {
+  int rc = SSCONV_OK;
+  StatsRows sr;
+  const int vec = cb % 4 == 0 ? 4 : 1;
+  if (e == hipSuccess && sink && stats_rows_plan(n_pos, cb, vec, &sr)) {
+    rc = norm_sink_take(sink, sr.nblk, st);
+    if (rc == SSCONV_OK) {
+      double* stats = (double*)sink->ws;
+      if (vec == 4)
+        split_reduce_stats_kernel<T, 4><<<sr.nblk, kStatsThreads, 0, st>>>(part, nsplit, n_pos, cb, order, sr.G,
+                                                                            sr.rpb, (T*)out, stats);
+      else
+        split_reduce_stats_kernel<T, 1><<<sr.nblk, kStatsThreads, 0, st>>>(part, nsplit, n_pos, cb, order, sr.G,
+                                                                            sr.rpb, (T*)out, stats);
+      e = hipGetLastError();
+    }
+  } else if (e == hipSuccess) {
     split_reduce_kernel<T><<<cdiv(n_pos * cb, 256), 256, 0, st>>>(part, nsplit, n_pos, cb, order, (T*)out);
     e = hipGetLastError();
   }
   scratch_give(sc, part, st);
+  if (rc != SSCONV_OK) return rc;
   if (e != hipSuccess) return fail(SSCONV_E_HIP, "gather launch: %s", hipGetErrorString(e));
   return SSCONV_OK;
 }
@@ -424,17 +519,17 @@ bool pick_cfg(ssconv_dtype dt, int cb, int K, int64_t n_src, Cfg* out) {
 
 template <typename T, int WMB, int S, int NW, typename IX>
 int launch_wnb(int wnb, const void* src, int ca, const void* Bt, int cb, const int32_t* nbr, const int32_t* order,
-               int64_t n_pos, int K, void* out, hipStream_t st, CallScratch* sc) {
+               int64_t n_pos, int K, void* out, hipStream_t st, CallScratch* sc, NormSink* sink) {
   switch (wnb) {
-    case 1: return launch<T, WMB, 1, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
-    case 2: return launch<T, WMB, 2, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
-    case 3: return launch<T, WMB, 3, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
-    case 4: return launch<T, WMB, 4, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
-    case 5: return launch<T, WMB, 5, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
-    case 6: return launch<T, WMB, 6, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
-    case 7: return launch<T, WMB, 7, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
-    case 8: return launch<T, WMB, 8, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
-    default: return launch<T, WMB, 13, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc);
+    case 1: return launch<T, WMB, 1, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc, sink);
+    case 2: return launch<T, WMB, 2, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc, sink);
+    case 3: return launch<T, WMB, 3, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc, sink);
+    case 4: return launch<T, WMB, 4, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc, sink);
+    case 5: return launch<T, WMB, 5, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc, sink);
+    case 6: return launch<T, WMB, 6, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc, sink);
+    case 7: return launch<T, WMB, 7, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc, sink);
+    case 8: return launch<T, WMB, 8, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc, sink);
+    default: return launch<T, WMB, 13, S, NW, IX>(src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc, sink);
   }
 }
 
@@ -446,7 +541,8 @@ bool gather_mfma_supported(ssconv_dtype dt, int ca, int cb, int K) {
 }
 
 int gather_mfma(const void* src, int64_t n_src, ssconv_dtype dt, int ca, const void* Bt, int cb, const int32_t* nbr,
-                const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st, CallScratch* sc) {
+                const int32_t* order, int64_t n_pos, int K, void* out, hipStream_t st, CallScratch* sc,
+                NormSink* sink) {
   if (n_pos == 0) return SSCONV_OK;
   // tuning overrides (same results): 1 = four wavefronts of 32 rows, 2 = four of 16 rows,
   // 3 = no 16-bit index table, 8 = three offset splits (in launch)
@@ -456,7 +552,8 @@ int gather_mfma(const void* src, int64_t n_src, ssconv_dtype dt, int ca, const v
     return fail(SSCONV_E_INVALID, "no gather tile fits the LDS for K=%d", K);
   if (variant == 1 && cfg_smem<float>({2, c.wnb, 3, 4, false}, K) <= (size_t)kLdsLimit) c = {2, c.wnb, 3, 4, false};
   if (variant == 2) c = {1, c.wnb, 3, 4, false};
-#define SSC_GO(T, WMB, S, NW, IX) return launch_wnb<T, WMB, S, NW, IX>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc)
+#define SSC_GO(T, WMB, S, NW, IX) \
+  return launch_wnb<T, WMB, S, NW, IX>(c.wnb, src, ca, Bt, cb, nbr, order, n_pos, K, out, st, sc, sink)
   if (dt == SSCONV_F32) {
     if (c.nw == 8 && c.idx16 && c.stages == 4) SSC_GO(float, 1, 4, 8, uint16_t);
     if (c.nw == 8 && c.idx16) SSC_GO(float, 1, 3, 8, uint16_t);

@@ -18,15 +18,15 @@
 // window's gradient / 8.
 #include <algorithm>
 
-#include "common.hpp"
+#include "norm.hpp"
 
 namespace ssconv {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = kNormThreads;
 constexpr int kMaxBlocks = 512;   // two workgroups per compute unit for the sums
-constexpr int kMaxChunks = 4;     // channels per row <= 4 * 256
-constexpr int kMaxChannels = kMaxChunks * kThreads;
+constexpr int kMaxChunks = kNormMaxChunks;
+constexpr int kMaxChannels = kNormMaxChannels;
 
 // Vector of VEC elements moved as one 16-byte access (VEC = 1: scalar).
 template <typename T, int VEC>
@@ -296,6 +296,56 @@ int norm_run(const FieldTab& f, const void* x, const void* g, int64_t n, double 
   return rc;
 }
 
+}  // namespace
+
+NormStatsPlan norm_stats_plan(int64_t n, int C) {
+  const NormPlan q = norm_plan(n, C);
+  NormStatsPlan p;
+  p.C = q.C, p.G = q.G, p.NC = q.NC, p.nblk = q.nblk, p.rpb = q.rpb;
+  return p;
+}
+
+static size_t up256(size_t b) { return (b + 255) & ~(size_t)255; }
+
+size_t norm_ws_bytes(int C, int64_t nblk) {
+  return up256((size_t)C * nblk * 2 * 8) + up256((size_t)C * 2 * 8) + (size_t)C * 16;
+}
+
+int norm_sink_take(NormSink* s, int64_t nblk, hipStream_t st) {
+  void* p = nullptr;
+  SSC_TRY(scratch_take(s->sc, &p, norm_ws_bytes(s->C, nblk), st));
+  s->ws = (char*)p;
+  s->nblk = nblk;
+  return SSCONV_OK;
+}
+
+int norm_forward_sums(ssconv_dtype dt, const void* y, int64_t n, const NormStatsPlan& p, char* ws, hipStream_t st) {
+  double* part = (double*)ws;
+  if (dt == SSCONV_F32)
+    norm_sums_kernel<float, 2><<<p.nblk, kThreads, 0, st>>>((const float*)y, nullptr, n, p.C, p.G, p.NC, p.rpb, part);
+  else
+    norm_sums_kernel<uint16_t, 2><<<p.nblk, kThreads, 0, st>>>((const uint16_t*)y, nullptr, n, p.C, p.G, p.NC, p.rpb,
+                                                               part);
+  SSC_HIP(hipGetLastError());
+  return SSCONV_OK;
+}
+
+int norm_forward_finish(const FieldTab& f, ssconv_dtype dt, const void* y, int64_t n, double eps, int64_t nblk,
+                        char* ws, void* z, hipStream_t st) {
+  const int C = f.ch0[f.n];
+  const size_t part_b = up256((size_t)C * nblk * 2 * 8), sums_b = up256((size_t)C * 2 * 8);
+  double* part = (double*)ws;
+  double* sums = (double*)(ws + part_b);
+  float4* coef = (float4*)(ws + part_b + sums_b);
+  norm_reduce_kernel<2><<<C, kThreads, 0, st>>>(part, (int)nblk, sums);
+  norm_coef_kernel<2><<<cdiv(f.f0[f.n], 64), 64, 0, st>>>(f, sums, n, eps, coef);
+  SSC_HIP(hipGetLastError());
+  return dt == SSCONV_F32 ? launch_apply<float, false>(y, nullptr, n, C, coef, z, st)
+                          : launch_apply<uint16_t, false>(y, nullptr, n, C, coef, z, st);
+}
+
+namespace {
+
 // ---------------------------------------------------------------------------------------------
 // Pooling
 // ---------------------------------------------------------------------------------------------
@@ -396,6 +446,11 @@ int check_norm(const ssconv_fields* fields, ssconv_dtype dt, int64_t n, double e
 }
 
 }  // namespace
+
+int norm_check_fields(const ssconv_fields* fields, ssconv_dtype dt, int64_t n, double eps, FieldTab* f) {
+  return check_norm(fields, dt, n, eps, f);
+}
+
 }  // namespace ssconv
 
 using namespace ssconv;

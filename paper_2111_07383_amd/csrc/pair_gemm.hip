@@ -17,6 +17,7 @@
 #include <algorithm>
 
 #include "conv.hpp"
+#include "norm.hpp"
 
 namespace ssconv {
 namespace {
@@ -161,18 +162,11 @@ __global__ void pair_map_scatter(const int2* __restrict__ pairs, const int64_t* 
   }
 }
 
-// dst[r][VEC columns] = sum over s of Y[map[s][r]]; eight offsets' map entries and rows are
-// fetched together, then added in offset order.
+// acc = sum over s of Y[map[s][r]][VEC columns from v * VEC]; eight offsets' map entries and rows
+// are fetched together, then added in offset order (absent pairs add 0).
 template <int VEC>
-__global__ __launch_bounds__(kThreads) void pair_reduce_kernel(const float* __restrict__ Y, int cb,
-                                                               const int32_t* __restrict__ map, int K, int64_t n_dst,
-                                                               float* __restrict__ dst) {
-  const int nv = cb / VEC;
-  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-  if (i >= n_dst * nv) return;
-  const int64_t r = i / nv;
-  const int v = (int)(i - r * nv);
-  float acc[VEC];
+__device__ __forceinline__ void pair_row(const float* __restrict__ Y, int cb, const int32_t* __restrict__ map, int K,
+                                         int64_t n_dst, int64_t r, int v, float* acc) {
 #pragma unroll
   for (int k = 0; k < VEC; ++k) acc[k] = 0.f;
   for (int s0 = 0; s0 < K; s0 += 8) {
@@ -200,12 +194,48 @@ __global__ __launch_bounds__(kThreads) void pair_reduce_kernel(const float* __re
 #pragma unroll
       for (int k = 0; k < VEC; ++k) acc[k] += y[j][k];
   }
+}
+
+template <int VEC>
+__device__ __forceinline__ void store_row(float* __restrict__ dst, int cb, int64_t r, int v, const float* acc) {
   if constexpr (VEC == 4) {
     *reinterpret_cast<float4*>(dst + r * cb + v * 4) = make_float4(acc[0], acc[1], acc[2], acc[3]);
   } else {
 #pragma unroll
     for (int k = 0; k < VEC; ++k) dst[r * cb + v * VEC + k] = acc[k];
   }
+}
+
+// dst[r][VEC columns] = pair_row, one thread per (row, vector).
+template <int VEC>
+__global__ __launch_bounds__(kThreads) void pair_reduce_kernel(const float* __restrict__ Y, int cb,
+                                                               const int32_t* __restrict__ map, int K, int64_t n_dst,
+                                                               float* __restrict__ dst) {
+  const int nv = cb / VEC;
+  const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  if (i >= n_dst * nv) return;
+  const int64_t r = i / nv;
+  const int v = (int)(i - r * nv);
+  float acc[VEC];
+  pair_row<VEC>(Y, cb, map, K, n_dst, r, v, acc);
+  store_row<VEC>(dst, cb, r, v, acc);
+}
+
+// The same rows (same values, same order of addition) in row blocks, with the Norm statistics of
+// what it writes (part, in the row-block layout of stats_rows).
+template <int VEC>
+__global__ __launch_bounds__(kStatsThreads) void pair_reduce_stats_kernel(const float* __restrict__ Y, int cb,
+                                                                          const int32_t* __restrict__ map, int K,
+                                                                          int64_t n_dst, int G, int64_t rpb,
+                                                                          float* __restrict__ dst,
+                                                                          double* __restrict__ part) {
+  stats_rows<VEC>(
+      cb, n_dst, G, rpb,
+      [&](int64_t r, int v, float* acc) {
+        pair_row<VEC>(Y, cb, map, K, n_dst, r, v, acc);
+        store_row<VEC>(dst, cb, r, v, acc);
+      },
+      part);
 }
 
 template <int NB>
@@ -253,7 +283,7 @@ size_t pair_path_bytes(const ssconv_rulebook* rb, int ca, int cb, int64_t n_dst)
 // sel_in = 1: rows of src are the pairs' input rows (forward); 0: their output rows (gradient).
 // ws: pair_path_bytes(rb, ca, cb, n_dst) bytes, 256-byte aligned.
 int pair_gemm(const void* src, int ca, const void* Bt, int cb, const ssconv_rulebook* rb, int sel_in, void* dst,
-              int64_t n_dst, void* ws, hipStream_t st) {
+              int64_t n_dst, void* ws, hipStream_t st, NormSink* sink) {
   const int K = rb->K;
   float* Y = (float*)ws;
   float* Bp = (float*)((char*)ws + y_bytes(rb, cb));
@@ -296,6 +326,19 @@ int pair_gemm(const void* src, int ca, const void* Bt, int cb, const ssconv_rule
     default: launch_pair_gemm<8>(grid, S, ca, B, cb, rb, tt, sel_in, Y, st); break;
   }
   const bool vec = cb % 4 == 0 && aligned16(dst);
+  StatsRows sr;
+  if (sink && stats_rows_plan(n_dst, cb, vec ? 4 : 1, &sr)) {
+    SSC_TRY(norm_sink_take(sink, sr.nblk, st));
+    double* part = (double*)sink->ws;
+    if (vec)
+      pair_reduce_stats_kernel<4><<<sr.nblk, kStatsThreads, 0, st>>>(Y, cb, map, K, n_dst, sr.G, sr.rpb, (float*)dst,
+                                                                      part);
+    else
+      pair_reduce_stats_kernel<1><<<sr.nblk, kStatsThreads, 0, st>>>(Y, cb, map, K, n_dst, sr.G, sr.rpb, (float*)dst,
+                                                                      part);
+    SSC_HIP(hipGetLastError());
+    return SSCONV_OK;
+  }
   const int64_t items = n_dst * (vec ? cb / 4 : cb);
   if (vec)
     pair_reduce_kernel<4><<<cdiv(items, kThreads), kThreads, 0, st>>>(Y, cb, map, K, n_dst, (float*)dst);

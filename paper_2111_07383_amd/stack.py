@@ -130,7 +130,9 @@ class Stack:
 class DownBlock:
     """The paper's downsampling block: a stride-1 submanifold SS-Conv, steerable Norm (Eq. 11)
     over every output field (gate channels included), the gated nonlinearity (Eq. 12), then
-    2x2x2 average pooling (the footnote of Sec. 3.1).  Rule books are rebuilt every call."""
+    2x2x2 average pooling (the footnote of Sec. 3.1).  The convolution and its Norm are one call
+    (``forward_norm``: the kernel that writes the convolution output also sums its statistics).
+    Rule books are rebuilt every call."""
     state: LayerState
     dtype: torch.dtype = torch.float32
     norm_eps: float = B.NORM_EPS
@@ -158,8 +160,7 @@ class DownBlock:
         L.W = B.synth_kernel(L.desc, L.basis, L.coeffs, self.dtype)
         L.rb = B.Rulebook(coords, L.grid, s.ksize, 1, True)
         L.x = feats
-        L.y = B.forward(feats, L.rb, L.W)
-        self.z = B.norm_forward(s.fields_out, L.y, self.norm_eps)
+        L.y, self.z = B.forward_norm(feats, L.rb, L.W, s.fields_out, self.norm_eps)
         h = B.gate_forward(regular_fields(s), self.z) if s.gated else self.z
         with torch.cuda.stream(side):
             self.pool_rb = B.Rulebook(coords, L.grid, 2, 2, False)
