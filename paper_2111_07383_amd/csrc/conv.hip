@@ -409,7 +409,7 @@ int conv_forward_norm(const void* feats, ssconv_dtype dt, int cin, const ssconv_
     rc = conv_forward(feats, dt, cin, rb, W, cout, y, st, nullptr, &sink);
   }
   if (rc == SSCONV_OK && sink.nblk == 0) {
-    const NormStatsPlan p = norm_stats_plan(n, cout);
+    const NormStatsPlan p = norm_stats_plan(dt, y, n, cout);
     rc = norm_sink_take(&sink, p.nblk, st);
     if (rc == SSCONV_OK) rc = norm_forward_sums(dt, y, n, p, sink.ws, st);
   }
@@ -429,8 +429,9 @@ int dw_nsplit(const ssconv_rulebook* rb) {
 
 static size_t align256(size_t b) { return (b + 255) & ~(size_t)255; }
 
-// The bf16 kernel gradient cuts the pair lists into work units (about two per compute unit).
-constexpr int kKgradUnits = 512;
+// The bf16 kernel gradient cuts the pair lists into work units, one per compute unit (measured on
+// the 128^3 208-channel layer: 512 units ran the gradient no faster and doubled the partials to add).
+constexpr int kKgradUnits = 256;
 
 static bool use_kgrad_units(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout) {
   if (dt == SSCONV_F32) return kgrad_f32_units_ok(rb, cin, cout);
@@ -438,7 +439,7 @@ static bool use_kgrad_units(const ssconv_rulebook* rb, ssconv_dtype dt, int cin,
          (int64_t)rb->n_in * cin * 2 < ((int64_t)1 << 31) && (int64_t)rb->n_out * cout * 2 < ((int64_t)1 << 31);
 }
 
-// Work units of the kernel gradient: bf16 ~512 (one workgroup each, launched in row order), fp32
+// Work units of the kernel gradient: bf16 ~256 (one workgroup each, launched in row order), fp32
 // enough wavefront tasks for one round of the wavefront slots.
 static KgradUnits plan_units(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int cout) {
   if (dt == SSCONV_F32) return kgrad_units(rb, kgrad_f32_units_want(rb, cin, cout), false);

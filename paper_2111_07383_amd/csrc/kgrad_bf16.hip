@@ -293,17 +293,45 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
 }
 
 // dW[s] (field-pair-blocked, dw_block_pos) = sum of offset s's unit partials ([cout][cin]) in unit
-// order.
-__global__ void reduce_units_kernel(const float* __restrict__ part, KgradUnits units, int cin, int cout,
-                                    FieldTab fout, FieldTab fin, float* __restrict__ dW) {
-  const int e = blockIdx.x * blockDim.x + threadIdx.x;
+// order.  A thread takes VEC consecutive elements of one row (cin % VEC == 0) and loads eight
+// units' values before adding them in order, so the partials stream instead of one round trip
+// per unit.
+template <int VEC>
+__global__ __launch_bounds__(256) void reduce_units_kernel(const float* __restrict__ part, KgradUnits units, int cin,
+                                                           int cout, FieldTab fout, FieldTab fin,
+                                                           float* __restrict__ dW) {
+  const int e = (blockIdx.x * blockDim.x + threadIdx.x) * VEC;
   const int s = blockIdx.y;
   const int64_t n = (int64_t)cin * cout;
   if (e >= n) return;
-  float acc = 0.f;
-  for (int u = units.uoff[s]; u < units.uoff[s + 1]; ++u) acc += part[(int64_t)u * n + e];
+  float acc[VEC];
+#pragma unroll
+  for (int k = 0; k < VEC; ++k) acc[k] = 0.f;
+  const int u1 = units.uoff[s + 1];
+  int u = units.uoff[s];
+  for (; u + 8 <= u1; u += 8) {
+    float v[8][VEC];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float* p = part + (int64_t)(u + j) * n + e;
+      if constexpr (VEC == 4) {
+        const float4 t = *reinterpret_cast<const float4*>(p);
+        v[j][0] = t.x, v[j][1] = t.y, v[j][2] = t.z, v[j][3] = t.w;
+      } else {
+        v[j][0] = *p;
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+#pragma unroll
+      for (int k = 0; k < VEC; ++k) acc[k] += v[j][k];
+  }
+  for (; u < u1; ++u)
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) acc[k] += part[(int64_t)u * n + e + k];
   const int o = e / cin;
-  dW[dw_block_pos(fout, fin, units.K, cin, s, o, e - o * cin)] = acc;
+#pragma unroll
+  for (int k = 0; k < VEC; ++k) dW[dw_block_pos(fout, fin, units.K, cin, s, o, e + k - o * cin)] = acc[k];
 }
 
 }  // namespace
@@ -357,8 +385,10 @@ int reduce_units(const float* part, const KgradUnits& units, int cin, int cout, 
                  const FieldTab& fin, float* dW, hipStream_t st) {
   const int64_t n = (int64_t)cin * cout;
   if (n == 0 || units.K == 0) return SSCONV_OK;
-  dim3 grid(cdiv(n, 256), units.K);
-  reduce_units_kernel<<<grid, 256, 0, st>>>(part, units, cin, cout, fout, fin, dW);
+  if (cin % 4 == 0)
+    reduce_units_kernel<4><<<dim3(cdiv(n / 4, 256), units.K), 256, 0, st>>>(part, units, cin, cout, fout, fin, dW);
+  else
+    reduce_units_kernel<1><<<dim3(cdiv(n, 256), units.K), 256, 0, st>>>(part, units, cin, cout, fout, fin, dW);
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;
 }

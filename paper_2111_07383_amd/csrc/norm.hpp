@@ -15,15 +15,17 @@ constexpr int kNormThreads = 256;
 constexpr int kNormMaxChunks = 4;                       // channels per row <= 4 * 256
 constexpr int kNormMaxChannels = kNormMaxChunks * kNormThreads;
 
-// Row blocks of the separate statistics pass over y [n, C]: blocks of rpb rows.  For C <= 256,
-// G = 256 / C row groups of C threads (thread t: channel t % C, rows r0 + t / C + k G, added in
-// row order, the G groups then added in group order); for C > 256 one group, thread t holding
-// channels t + 256 j.
+// Row blocks of the separate statistics pass over y [n, C]: blocks of rpb rows.  vec: thread t
+// holds the 16 bytes of channels (t % nv) * VEC .. of rows r0 + t / nv + k G (nv = C / VEC vectors
+// per row, G = 256 / nv row groups); else, for C <= 256, G = 256 / C row groups of C threads
+// (thread t: channel t % C, rows r0 + t / C + k G), for C > 256 one group, thread t holding
+// channels t + 256 j.  Rows are added in row order, the G groups then in group order.
 struct NormStatsPlan {
   int C, G, NC, nblk;
   int64_t rpb;
+  bool vec;
 };
-NormStatsPlan norm_stats_plan(int64_t n, int C);
+NormStatsPlan norm_stats_plan(ssconv_dtype dt, const void* y, int64_t n, int C);
 
 // Device bytes of the statistics workspace of C channels over nblk row blocks: the partial sums
 // (at its start), the channel sums and the per-channel coefficients.
@@ -57,7 +59,7 @@ int norm_check_fields(const ssconv_fields* fields, ssconv_dtype dt, int64_t n, d
 // then added in group order.
 // ---------------------------------------------------------------------------------------------
 constexpr int kStatsThreads = 512;
-constexpr int kStatsRowsPerThread = 2;  // rows per thread: keeps the row loads of the whole grid in flight
+constexpr int kStatsRowsPerThread = 2;  // rows per thread (measured: 1 row gave more partials and no gain)
 
 struct StatsRows {
   int G;

@@ -241,10 +241,170 @@ __global__ __launch_bounds__(kThreads) void norm_apply_kernel(const T* x, const 
   }
 }
 
+// Channel-stationary vector layout (C % VEC == 0, nv = C / VEC <= 256): thread t < G * nv
+// (G = 256 / nv row groups) owns the VEC channels v * VEC .. of vector v = t % nv in rows
+// r0 + t / nv + k G, so its coefficients and sums stay in registers and every access is 16 bytes.
+template <typename T, int VEC>
+struct VecIO {
+  static __device__ __forceinline__ void load(const T* p, float* f) {
+    const Vec<T, VEC> a = vload<T, VEC>(p);
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) f[k] = DT<T>::to_f(a.e[k]);
+  }
+  static __device__ __forceinline__ void store(T* p, const float* f) {
+    Vec<T, VEC> a;
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) a.e[k] = DT<T>::from_f(f[k]);
+    vstore<T, VEC>(p, a);
+  }
+};
+
+// Channel sums as norm_sums_kernel, in the vector layout: rows added in row order per thread,
+// four rows' loads issued together; the G groups then added in group order.
+template <typename T, int VEC, int NQ>
+__global__ __launch_bounds__(kThreads) void norm_sums_vec_kernel(const T* __restrict__ x, const T* __restrict__ g,
+                                                                 int64_t n, int C, int G, int64_t rpb,
+                                                                 double* __restrict__ part) {
+  __shared__ double red[VEC][kThreads];
+  const int nv = C / VEC, t = threadIdx.x, v = t % nv, grp = t / nv, nblk = gridDim.x;
+  const int64_t r0 = (int64_t)blockIdx.x * rpb;
+  const int64_t r1 = min(n, r0 + rpb);
+  double acc[NQ][VEC];
+#pragma unroll
+  for (int q = 0; q < NQ; ++q)
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) acc[q][k] = 0.0;
+  if (grp < G) {
+    const int64_t c0 = (int64_t)v * VEC;
+    int64_t r = r0 + grp;
+    for (; r + 3 * (int64_t)G < r1; r += 4 * (int64_t)G) {
+      float xv[4][VEC], gv[4][VEC];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        VecIO<T, VEC>::load(x + (r + i * (int64_t)G) * C + c0, xv[i]);
+        if (NQ == 4) VecIO<T, VEC>::load(g + (r + i * (int64_t)G) * C + c0, gv[i]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int k = 0; k < VEC; ++k) {
+          const double dv = xv[i][k];
+          acc[0][k] += dv;
+          acc[1][k] = fma(dv, dv, acc[1][k]);
+          if (NQ == 4) {
+            const double dw = gv[i][k];
+            acc[2][k] += dw;
+            acc[3][k] = fma(dw, dv, acc[3][k]);
+          }
+        }
+    }
+    for (; r < r1; r += G) {
+      float xv[VEC], gv[VEC];
+      VecIO<T, VEC>::load(x + r * C + c0, xv);
+      if (NQ == 4) VecIO<T, VEC>::load(g + r * C + c0, gv);
+#pragma unroll
+      for (int k = 0; k < VEC; ++k) {
+        const double dv = xv[k];
+        acc[0][k] += dv;
+        acc[1][k] = fma(dv, dv, acc[1][k]);
+        if (NQ == 4) {
+          const double dw = gv[k];
+          acc[2][k] += dw;
+          acc[3][k] = fma(dw, dv, acc[3][k]);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < NQ; ++q) {
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) red[k][t] = acc[q][k];
+    __syncthreads();
+    for (int e = t; e < C; e += kThreads) {
+      const int vv = e / VEC, k = e % VEC;
+      double sum = 0.0;
+      for (int j = 0; j < G; ++j) sum += red[k][j * nv + vv];
+      part[((int64_t)e * nblk + blockIdx.x) * NQ + q] = sum;
+    }
+    __syncthreads();
+  }
+}
+
+// The elementwise pass in the vector layout, each thread's coefficients loaded once.  The output
+// may alias x (and g) element for element.
+template <typename T, int VEC, bool kBwd>
+__global__ __launch_bounds__(kThreads) void norm_apply_vec_kernel(const T* x, const T* g, int64_t n, int C, int G,
+                                                                  int64_t rpb, const float4* __restrict__ coef,
+                                                                  T* y) {
+  const int nv = C / VEC, t = threadIdx.x, v = t % nv, grp = t / nv;
+  if (grp >= G) return;
+  const int64_t c0 = (int64_t)v * VEC;
+  float4 q[VEC];
+#pragma unroll
+  for (int k = 0; k < VEC; ++k) q[k] = coef[c0 + k];
+  const int64_t r0 = (int64_t)blockIdx.x * rpb;
+  const int64_t r1 = min(n, r0 + rpb);
+  int64_t r = r0 + grp;
+  for (; r + 3 * (int64_t)G < r1; r += 4 * (int64_t)G) {
+    float xv[4][VEC], gv[4][VEC];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      VecIO<T, VEC>::load(x + (r + i * (int64_t)G) * C + c0, xv[i]);
+      if (kBwd) VecIO<T, VEC>::load(g + (r + i * (int64_t)G) * C + c0, gv[i]);
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float o[VEC];
+#pragma unroll
+      for (int k = 0; k < VEC; ++k) {
+        const float xm = xv[i][k] - q[k].z;
+        o[k] = kBwd ? fmaf(q[k].x, gv[i][k], fmaf(q[k].y, xm, q[k].w)) : q[k].x * xm;
+      }
+      VecIO<T, VEC>::store(y + (r + i * (int64_t)G) * C + c0, o);
+    }
+  }
+  for (; r < r1; r += G) {
+    float xv[VEC], gv[VEC], o[VEC];
+    VecIO<T, VEC>::load(x + r * C + c0, xv);
+    if (kBwd) VecIO<T, VEC>::load(g + r * C + c0, gv);
+#pragma unroll
+    for (int k = 0; k < VEC; ++k) {
+      const float xm = xv[k] - q[k].z;
+      o[k] = kBwd ? fmaf(q[k].x, gv[k], fmaf(q[k].y, xm, q[k].w)) : q[k].x * xm;
+    }
+    VecIO<T, VEC>::store(y + r * C + c0, o);
+  }
+}
+
 struct NormPlan {
   int C, G, NC, nblk;
   int64_t rpb;
 };
+
+// The vector layout where it applies: VEC elements of 16 bytes, nv = C / VEC <= 256 (else the
+// scalar layout of norm_sums_kernel / norm_apply_kernel).
+template <typename T>
+bool vec_layout(int C, const void* a, const void* b, const void* c) {
+  constexpr int V = 16 / sizeof(T);
+  return C % V == 0 && C / V <= kThreads && aligned16(a) && (!b || aligned16(b)) && (!c || aligned16(c));
+}
+
+// Row blocks of the vector-layout sums: at least four row steps of each thread, at most
+// kMaxVecBlocks blocks.
+constexpr int kMaxVecBlocks = 1024;
+template <typename T>
+NormPlan norm_vec_plan(int64_t n, int C) {
+  constexpr int V = 16 / sizeof(T);
+  NormPlan p;
+  p.C = C;
+  p.NC = 1;
+  p.G = kThreads / (C / V);
+  const int64_t want = (n + 4 * (int64_t)p.G - 1) / (4 * (int64_t)p.G);
+  p.nblk = (int)std::max<int64_t>(1, std::min<int64_t>(kMaxVecBlocks, want));
+  p.rpb = (n + p.nblk - 1) / p.nblk;
+  p.nblk = (int)((n + p.rpb - 1) / p.rpb);
+  return p;
+}
 
 NormPlan norm_plan(int64_t n, int C) {
   NormPlan p;
@@ -261,10 +421,19 @@ NormPlan norm_plan(int64_t n, int C) {
 
 template <typename T, bool kBwd>
 int launch_apply(const void* x, const void* g, int64_t n, int C, const float4* coef, void* y, hipStream_t st) {
+  constexpr int V = 16 / sizeof(T);
+  if (vec_layout<T>(C, x, kBwd ? g : nullptr, y)) {
+    // four row steps of each thread per block
+    const int G = kThreads / (C / V);
+    const int64_t rpb = 4 * (int64_t)G;
+    norm_apply_vec_kernel<T, V, kBwd><<<cdiv(n, rpb), kThreads, 0, st>>>((const T*)x, (const T*)g, n, C, G, rpb, coef,
+                                                                          (T*)y);
+    SSC_HIP(hipGetLastError());
+    return SSCONV_OK;
+  }
   // rows per block: about 4096 elements per workgroup
   const int64_t rpb = std::max<int64_t>(1, 4096 / C);
   const unsigned nb = cdiv(n, rpb);
-  constexpr int V = 16 / sizeof(T);
   const bool vec = C % V == 0 && aligned16(x) && aligned16(y) && (!kBwd || aligned16(g));
   if (vec)
     norm_apply_kernel<T, V, kBwd><<<nb, kThreads, 0, st>>>((const T*)x, (const T*)g, n, C, rpb, coef, (T*)y);
@@ -277,7 +446,8 @@ int launch_apply(const void* x, const void* g, int64_t n, int C, const float4* c
 template <typename T, int NQ>
 int norm_run(const FieldTab& f, const void* x, const void* g, int64_t n, double eps, void* y, hipStream_t st) {
   const int C = f.ch0[f.n];
-  const NormPlan p = norm_plan(n, C);
+  const bool vec = vec_layout<T>(C, x, NQ == 4 ? g : nullptr, nullptr);
+  const NormPlan p = vec ? norm_vec_plan<T>(n, C) : norm_plan(n, C);
   const size_t part_b = ((size_t)C * p.nblk * NQ * 8 + 255) & ~(size_t)255;
   const size_t sums_b = ((size_t)C * NQ * 8 + 255) & ~(size_t)255;
   char* ws = nullptr;
@@ -285,7 +455,11 @@ int norm_run(const FieldTab& f, const void* x, const void* g, int64_t n, double 
   double* part = (double*)ws;
   double* sums = (double*)(ws + part_b);
   float4* coef = (float4*)(ws + part_b + sums_b);
-  norm_sums_kernel<T, NQ><<<p.nblk, kThreads, 0, st>>>((const T*)x, (const T*)g, n, C, p.G, p.NC, p.rpb, part);
+  if (vec)
+    norm_sums_vec_kernel<T, 16 / sizeof(T), NQ><<<p.nblk, kThreads, 0, st>>>((const T*)x, (const T*)g, n, C, p.G,
+                                                                             p.rpb, part);
+  else
+    norm_sums_kernel<T, NQ><<<p.nblk, kThreads, 0, st>>>((const T*)x, (const T*)g, n, C, p.G, p.NC, p.rpb, part);
   norm_reduce_kernel<NQ><<<C, kThreads, 0, st>>>(part, p.nblk, sums);
   const int n_fields = f.f0[f.n];
   norm_coef_kernel<NQ><<<cdiv(n_fields, 64), 64, 0, st>>>(f, sums, n, eps, coef);
@@ -298,10 +472,13 @@ int norm_run(const FieldTab& f, const void* x, const void* g, int64_t n, double 
 
 }  // namespace
 
-NormStatsPlan norm_stats_plan(int64_t n, int C) {
-  const NormPlan q = norm_plan(n, C);
+NormStatsPlan norm_stats_plan(ssconv_dtype dt, const void* y, int64_t n, int C) {
+  const bool vec = dt == SSCONV_F32 ? vec_layout<float>(C, y, nullptr, nullptr)
+                                    : vec_layout<uint16_t>(C, y, nullptr, nullptr);
+  const NormPlan q = !vec ? norm_plan(n, C) : dt == SSCONV_F32 ? norm_vec_plan<float>(n, C)
+                                                               : norm_vec_plan<uint16_t>(n, C);
   NormStatsPlan p;
-  p.C = q.C, p.G = q.G, p.NC = q.NC, p.nblk = q.nblk, p.rpb = q.rpb;
+  p.C = q.C, p.G = q.G, p.NC = q.NC, p.nblk = q.nblk, p.rpb = q.rpb, p.vec = vec;
   return p;
 }
 
@@ -321,7 +498,12 @@ int norm_sink_take(NormSink* s, int64_t nblk, hipStream_t st) {
 
 int norm_forward_sums(ssconv_dtype dt, const void* y, int64_t n, const NormStatsPlan& p, char* ws, hipStream_t st) {
   double* part = (double*)ws;
-  if (dt == SSCONV_F32)
+  if (p.vec && dt == SSCONV_F32)
+    norm_sums_vec_kernel<float, 4, 2><<<p.nblk, kThreads, 0, st>>>((const float*)y, nullptr, n, p.C, p.G, p.rpb, part);
+  else if (p.vec)
+    norm_sums_vec_kernel<uint16_t, 8, 2><<<p.nblk, kThreads, 0, st>>>((const uint16_t*)y, nullptr, n, p.C, p.G, p.rpb,
+                                                                     part);
+  else if (dt == SSCONV_F32)
     norm_sums_kernel<float, 2><<<p.nblk, kThreads, 0, st>>>((const float*)y, nullptr, n, p.C, p.G, p.NC, p.rpb, part);
   else
     norm_sums_kernel<uint16_t, 2><<<p.nblk, kThreads, 0, st>>>((const uint16_t*)y, nullptr, n, p.C, p.G, p.NC, p.rpb,

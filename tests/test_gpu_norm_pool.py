@@ -119,6 +119,8 @@ NORM_CASES = {
     "wide": (((0, 64), (1, 64), (2, 32)), 1500),                   # C = 416 > 256: two channel chunks
     "vectors_only": (((1, 3), (3, 2)), 999),                       # C = 23, no scalar field
     "single_row": (((0, 3), (1, 2)), 1),                           # var = 0: scalars become 0
+    "max_channels": (((0, 64), (1, 64), (2, 64), (3, 32), (4, 16), (0, 80)), 777),  # C = 1024
+    "fp32_vectors": (((0, 4), (1, 1), (2, 1)), 4097),             # C = 12: 16-byte vectors in fp32 only
 }
 
 
