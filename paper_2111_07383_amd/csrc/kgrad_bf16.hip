@@ -44,12 +44,20 @@ constexpr int kBufferWord3 = 0x00020000;   // buffer descriptor word 3 for gfx9-
 constexpr int kS = 4;                      // LDS stages
 constexpr int kPBLK = 1024;                // pair indices per staged block
 
-template <int W>
+// Operand staging in LDS.  Quad layout (kQuad, the default): granule quad j (channels 32j .. 32j
+// + 31 of the tile) of the chunk's 32 rows is 2 KB, row r at 64 r, the granule of position p at
+// 16 (p ^ 2 ((r / 8) % 2)) (the swizzle keeps the 32 lanes served together by a transpose read on
+// distinct banks); one DMA fills a quad for 16 rows, so a lane fetches 16 bytes of a 64-byte piece
+// of one row.  Column layout: granule column j (16 bytes of 32 rows, 512 B) in block j % H, half
+// j / H, blocks padded to 1088 bytes; one DMA fills a block with two 16-byte pieces of 32 rows.
+// Measured on gathered 416-byte rows (1 KB DMAs, 80 MB table): 64-byte pieces moved 24-27 B/ns
+// per CU, 16-byte pieces 11-15.
+template <int W, bool kQuad = true>
 struct KB {
   static constexpr int TW = 32 * W;                 // tile width in channels (each side)
   static constexpr int H = 2 * W;                   // DMA blocks per operand (two granule columns each)
-  static constexpr int BLK = 1024 + 64;             // bytes per DMA block (padded)
-  static constexpr int OPB = H * BLK;               // bytes per operand per stage
+  static constexpr int BLK = 1024 + 64;             // bytes per DMA block (padded), column layout
+  static constexpr int OPB = kQuad ? 2 * W * 1024 : H * BLK;  // bytes per operand per stage
   static constexpr int STAGE = 2 * OPB;
   static constexpr int PW = W;                      // DMAs per wavefront per chunk
   static_assert(W <= 7, "DMA immediate offsets are instantiated for up to 7 blocks per wavefront");
@@ -69,6 +77,19 @@ __device__ __forceinline__ void dma16_buf(__amdgpu_buffer_rsrc_t rsrc, uint32_t 
                : "memory", "m0");
 }
 #pragma clang diagnostic pop
+
+// dma16_buf with immediate offset 64 q; q is a constant once the callers' loops are unrolled
+__device__ __forceinline__ void dma16_buf_q64(int q, __amdgpu_buffer_rsrc_t rsrc, uint32_t off, uint32_t lds) {
+  switch (q) {
+    case 0: dma16_buf<0>(rsrc, off, lds); break;
+    case 1: dma16_buf<64>(rsrc, off, lds); break;
+    case 2: dma16_buf<128>(rsrc, off, lds); break;
+    case 3: dma16_buf<192>(rsrc, off, lds); break;
+    case 4: dma16_buf<256>(rsrc, off, lds); break;
+    case 5: dma16_buf<320>(rsrc, off, lds); break;
+    default: dma16_buf<384>(rsrc, off, lds); break;
+  }
+}
 
 // dma16_buf with immediate offset 16 q; q is a constant once the callers' loops are unrolled
 __device__ __forceinline__ void dma16_buf_q(int q, __amdgpu_buffer_rsrc_t rsrc, uint32_t off, uint32_t lds) {
@@ -94,13 +115,13 @@ __device__ __forceinline__ s4 tr_read(uint32_t lds) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4*)(uintptr_t)lds);
 }
 
-template <int W>
+template <int W, bool kQuad>
 __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restrict__ G, int64_t g_rows, int cout,
                                                          const uint16_t* __restrict__ F, int64_t f_rows, int cin,
                                                          const int2* __restrict__ pairs,
                                                          const int64_t* __restrict__ pair_off, KgradUnits units,
                                                          int mtiles, int ntiles, float* __restrict__ part) {
-  using C = KB<W>;
+  using C = KB<W, kQuad>;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   char* stages = smem;
   char* pblk = smem + kS * C::STAGE;  // [2][kPBLK] int2
@@ -131,25 +152,30 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
       const_cast<int2*>(pairs + beg), (short)0, npairs * 8, kBufferWord3);
   const uint32_t stage0 = lds_addr(stages), pblk_a = lds_addr(pblk);
 
-  // DMA duty: wavefronts 0-1 fetch grad_out (operand 0), 2-3 feats (operand 1); wavefront w
-  // issues blocks jb .. jb + W - 1 of its operand, jb = W * (w % 2).  Lane l fetches pair row
-  // l % 32, granule column (block + H * (l / 32)).
+  // DMA duty: wavefronts 0-1 fetch grad_out (operand 0), 2-3 feats (operand 1).  Quad layout:
+  // wavefront w fills quads 0 .. W - 1 of rows 16 (w % 2) .. + 15, lane l: row 16 (w % 2) + l / 4,
+  // granule gq = (l % 4) ^ swizzle of the quad.  Column layout: blocks jb .. jb + W - 1,
+  // jb = W * (w % 2), lane l: row l % 32, granule column (block + H * (l / 32)).
   const bool isF = w >= 2;
   const int jb = W * (w & 1);
-  const int prow = lane & 31;
+  const int prow = kQuad ? 16 * (w & 1) + (lane >> 2) : lane & 31;
+  const int gq = (lane & 3) ^ (((prow >> 3) & 1) << 1);
   const __amdgpu_buffer_rsrc_t x_rsrc = isF ? f_rsrc : g_rsrc;
   const uint32_t x_rowb = (uint32_t)(isF ? cin : cout) * 2u;
-  const uint32_t x_stat = (uint32_t)(isF ? n0 : m0) * 2u + 16u * (uint32_t)(jb + C::H * (lane >> 5));
-  // DMA q of this lane fetches channels (isF ? n0 : m0) + 8 (jb + q + H (lane / 32)) .. + 7; a granule
-  // past the operand's channels (the tile is padded to 32 W) is not fetched (offset past the end:
-  // zeros; the products it feeds are never stored)
+  const uint32_t x_stat = (uint32_t)(isF ? n0 : m0) * 2u +
+                          16u * (uint32_t)(kQuad ? gq : jb + C::H * (lane >> 5));
+  // DMA q of this lane fetches channels (isF ? n0 : m0) + 8 (4q + gq) .. + 7 (column layout: + 8 (jb
+  // + q + H (lane / 32))); a granule past the operand's channels (the tile is padded to 32 W) is
+  // not fetched (offset past the end: zeros; the products it feeds are never stored)
   uint32_t gvalid = 0;
   {
-    const int ch = isF ? cin : cout, c0 = (isF ? n0 : m0) + 8 * (jb + C::H * (lane >> 5));
+    const int ch = isF ? cin : cout;
+    const int c0 = (isF ? n0 : m0) + 8 * (kQuad ? gq : jb + C::H * (lane >> 5));
 #pragma unroll
-    for (int q = 0; q < C::PW; ++q) gvalid |= (c0 + 8 * q < ch ? 1u : 0u) << q;
+    for (int q = 0; q < C::PW; ++q) gvalid |= (c0 + 8 * (kQuad ? 4 * q : q) < ch ? 1u : 0u) << q;
   }
-  const uint32_t m0_base = stage0 + (isF ? C::OPB : 0) + jb * C::BLK;  // + stage * STAGE + q * BLK
+  // + stage * STAGE + q * (quad: 2048, column: BLK)
+  const uint32_t m0_base = stage0 + (isF ? C::OPB : 0) + (kQuad ? (w & 1) * 1024 : jb * C::BLK);
   const uint32_t p_ent = (uint32_t)prow * 8u + (isF ? 4u : 0u);        // this lane's index in a chunk's pairs
 
   // pair block b (slice pairs [b*kPBLK, (b+1)*kPBLK)) into buffer b % 2: 8 KB per block, two
@@ -172,24 +198,40 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
     dst_ = (prow < npairs - (c_) * 32) ? (uint32_t)v_ * x_rowb + x_stat : kAbsent;                  \
   } while (0)
 
-  // DMA q of this wavefront (block jb + q) into stage k_, from row offset ro_.  The MUBUF
-  // immediate offset 16 q is added to the LDS address as well, so M0 is set 16 q bytes lower.
+  // DMA q of this wavefront (quad q; column layout: block jb + q) into stage k_, from row offset
+  // ro_.  The MUBUF immediate offset (64 q; column layout: 16 q) is added to the LDS address as
+  // well, so M0 is set that much lower.
 #define SSK_DMA(q_, ro_, k_)                                                                        \
-  dma16_buf_q(q_, x_rsrc, ((gvalid >> (q_)) & 1u) ? (ro_) : kAbsent, m0_base + (k_) * C::STAGE + (q_) * (C::BLK - 16))
+  do {                                                                                              \
+    const uint32_t src_ = ((gvalid >> (q_)) & 1u) ? (ro_) : kAbsent;                                \
+    if constexpr (kQuad)                                                                            \
+      dma16_buf_q64(q_, x_rsrc, src_, m0_base + (k_) * C::STAGE + (q_) * (2048 - 64));              \
+    else                                                                                            \
+      dma16_buf_q(q_, x_rsrc, src_, m0_base + (k_) * C::STAGE + (q_) * (C::BLK - 16));              \
+  } while (0)
 
-  // operands of the chunk in stage k_ via transpose reads: rows 8g + 4h + L/4, channel
-  // (wm * W + i) * 16 + 4 (L % 4) -> granule column 2 (wm * W + i) + (L % 4) / 2, i.e. block
-  // 2i + (L % 4) / 2 and half wm (grad_out; feats: wn), byte 8 ((L % 4) % 2)
+  // operands of the chunk in stage k_ via transpose reads: rows R = 8g + 4h + L/4, channel
+  // 16 bi + 4 (L % 4) for MFMA block bi = wm * W + i (grad_out; feats: wn * W + i), i.e. granule
+  // J = 2 bi + (L % 4) / 2, byte 8 ((L % 4) % 2).  Quad layout: quad bi / 2, row R, position
+  // 2 ((bi % 2) ^ (g % 2)) + (L % 4) / 2 (R / 8 = g).  Column layout: block 2i + (L % 4) / 2, half
+  // wm (wn), row R.
   const uint32_t rd_lane =
-      (uint32_t)((((r16 & 3) >> 1) * C::BLK) + (8 * g + (r16 >> 2)) * 16 + ((r16 & 1) * 8));
-  const uint32_t rd_a = stage0 + wm * 512 + rd_lane, rd_b = stage0 + C::OPB + wn * 512 + rd_lane;
+      kQuad ? (uint32_t)((8 * g + (r16 >> 2)) * 64 + ((r16 & 3) >> 1) * 16 + (r16 & 1) * 8)
+            : (uint32_t)((((r16 & 3) >> 1) * C::BLK) + (8 * g + (r16 >> 2)) * 16 + ((r16 & 1) * 8));
+  const uint32_t gx = (uint32_t)(g & 1) * 32u;  // quad layout: the swizzle bit of this lane's rows
+  const uint32_t rd_a = stage0 + (kQuad ? 0u : wm * 512u) + rd_lane;
+  const uint32_t rd_b = stage0 + C::OPB + (kQuad ? 0u : wn * 512u) + rd_lane;
+  // byte offset of MFMA block bi_ (wave-uniform) in the quad layout; h = 1 adds 4 rows (256 B)
+#define SSK_QOFF(bi_) ((uint32_t)((bi_) >> 1) * 2048u + ((((uint32_t)(bi_) & 1u) * 32u) ^ gx))
 #define SSK_READ(da_, db_, i_, k_)                                                                  \
   do {                                                                                              \
-    const uint32_t o_ = (k_) * C::STAGE + 2 * (i_) * C::BLK;                                        \
-    const s4 a0_ = tr_read(rd_a + o_);                                                              \
-    const s4 a1_ = tr_read(rd_a + o_ + 64);                                                         \
-    const s4 b0_ = tr_read(rd_b + o_);                                                              \
-    const s4 b1_ = tr_read(rd_b + o_ + 64);                                                         \
+    const uint32_t oa_ = (k_) * C::STAGE + (kQuad ? SSK_QOFF(wm * W + (i_)) : 2 * (i_) * C::BLK);   \
+    const uint32_t ob_ = (k_) * C::STAGE + (kQuad ? SSK_QOFF(wn * W + (i_)) : 2 * (i_) * C::BLK);   \
+    const uint32_t hs_ = kQuad ? 256u : 64u;                                                        \
+    const s4 a0_ = tr_read(rd_a + oa_);                                                             \
+    const s4 a1_ = tr_read(rd_a + oa_ + hs_);                                                       \
+    const s4 b0_ = tr_read(rd_b + ob_);                                                             \
+    const s4 b1_ = tr_read(rd_b + ob_ + hs_);                                                       \
     da_[i_] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(a0_, a1_, 0, 1, 2, 3, 4, 5, 6, 7)); \
     db_[i_] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(b0_, b1_, 0, 1, 2, 3, 4, 5, 6, 7)); \
   } while (0)
@@ -272,6 +314,7 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
     SSK_BODY(3, a1, b1, a0, b0)
   }
 #undef SSK_BODY
+#undef SSK_QOFF
 #undef SSK_READ
 #undef SSK_DMA
 #undef SSK_ROW
@@ -405,12 +448,15 @@ int kgrad_bf16(const void* grad_out, int64_t n_out, const void* feats, int64_t n
   const int mtiles = (cout + 32 * W - 1) / (32 * W), ntiles = (cin + 32 * W - 1) / (32 * W);
   dim3 grid((unsigned)(units.nunits * mtiles * ntiles));
   const int2* pairs = reinterpret_cast<const int2*>(rb->pairs);
+  // override 12: the column layout (same operands in the MFMAs, same results bit for bit)
+  const bool quad = debug_gather_variant() != 12;
 #define SSK_LAUNCH(Wv)                                                                              \
   do {                                                                                              \
-    auto kern = kgrad_bf16_kernel<Wv>;                                                              \
-    SSC_HIP(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, KB<Wv>::SMEM)); \
-    kern<<<grid, 256, KB<Wv>::SMEM, st>>>((const uint16_t*)grad_out, n_out, cout, (const uint16_t*)feats, n_in, \
-                                          cin, pairs, rb->pair_off_dev, units, mtiles, ntiles, part);  \
+    auto kern = quad ? kgrad_bf16_kernel<Wv, true> : kgrad_bf16_kernel<Wv, false>;                  \
+    const int smem = quad ? KB<Wv, true>::SMEM : KB<Wv, false>::SMEM;                               \
+    SSC_HIP(hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, smem)); \
+    kern<<<grid, 256, smem, st>>>((const uint16_t*)grad_out, n_out, cout, (const uint16_t*)feats, n_in, cin, \
+                                  pairs, rb->pair_off_dev, units, mtiles, ntiles, part);            \
   } while (0)
   if (W == 2) SSK_LAUNCH(2);
   else if (W == 4) SSK_LAUNCH(4);

@@ -261,7 +261,7 @@ bool pair_path_wins(const ssconv_rulebook* rb, ssconv_dtype dt, int ca, int cb, 
   if (!pair_path_supported(rb, dt, ca, cb) || n_dst <= 0) return false;
   const int64_t v = debug_gather_variant();
   if (v == 9) return true;
-  if (v != 0 && v != 11) return false;  // 10 and the other overrides forbid it (11 only concerns the fork)
+  if (v != 0 && v != 11 && v != 12) return false;  // 10 and the others forbid it (11, 12 concern other kernels)
   const double P = (double)rb->n_pairs;
   const double density = std::min(1.0, P / ((double)n_dst * rb->K));
   const double flops = 2.0 * P * ca * cb;

@@ -149,6 +149,48 @@ def test_bf16_diagnostic_against_unrounded_inputs():
     assert e_diag < 4 * 2.0 ** -8
 
 
+_KGRAD_LAYERS = {
+    "c4": None,                                                     # the 128^3 scene layer, tile 224
+    "w2": (((0, 16), (1, 8)), ((0, 16), (1, 8), (2, 4))),           # 40 -> 60: tile 64
+    "w4": (((0, 16), (1, 8), (2, 4), (1, 8), (0, 16)), ((0, 32), (1, 16), (2, 8))),  # 100 -> 120: tile 128
+    "w7x2": (((0, 32), (1, 32), (2, 16)), ((0, 32), (1, 32), (2, 16), (1, 12), (0, 56))),  # 208 -> 300: 2 tiles
+}
+
+
+@pytest.mark.parametrize("name", list(_KGRAD_LAYERS))
+def test_bf16_kernel_gradient_staging_layouts_bit_identical(name):
+    """The bf16 kernel gradient with its operands staged in 64-byte quads (default) against the
+    16-byte column layout (override 12): the MFMAs read the same operands, so the coefficient
+    gradient agrees bit for bit.  Tiles of 64, 128 and 224 channels, one layer with two output
+    tiles, ragged channel counts inside the tiles."""
+    from workloads.configs import LayerSpec
+    print(f"bf16 kernel gradient staging, {name}", flush=True)
+    if name == "c4":
+        L, dt, desc, basis, rb, W, feats = _layer_io(4)
+        spec = L.spec
+    else:
+        fin, fout = _KGRAD_LAYERS[name]
+        spec = LayerSpec(3, 1, True, fin, fout, shells=(0.0, 1.0))
+        L6 = layers_of(6)[0]
+        rb = P.Rulebook(_tensor(L6.coords_in), L6.grid, 3, 1, True)
+        desc = P.layer_desc(spec)
+        basis = _tensor(P.basis_build(desc))
+        gen = torch.Generator(DEV).manual_seed(len(name))
+        coeffs = torch.randn(P.basis_info(desc)[1], device=DEV, generator=gen)
+        W = P.synth_kernel(desc, basis, coeffs, torch.bfloat16)
+        feats = torch.randn(rb.n_in, spec.cin, device=DEV, generator=gen).to(torch.bfloat16)
+    g = torch.randn(rb.n_out, spec.cout, device=DEV, generator=torch.Generator(DEV).manual_seed(7)).to(torch.bfloat16)
+    got = []
+    for variant in (0, 12):
+        P.debug_set(3, variant)
+        try:
+            got.append(P.backward(feats, g, rb, W, desc, basis, need_feats=False)[1])
+        finally:
+            P.debug_set(3, 0)
+    assert torch.equal(got[0], got[1])
+    rb.close()
+
+
 def test_forward_backward_deterministic():
     L, dt, desc, basis, rb, W, feats = _layer_io(2)
     g = torch.randn(rb.n_out, L.spec.cout, device=DEV, generator=torch.Generator(DEV).manual_seed(0))
