@@ -336,7 +336,7 @@ __global__ __launch_bounds__(256) void kgrad_bf16_kernel(const uint16_t* __restr
 }
 
 // dW[s] (field-pair-blocked, dw_block_pos) = sum of offset s's unit partials ([cout][cin]) in unit
-// order.  A thread takes VEC consecutive elements of one row (cin % VEC == 0) and loads eight
+// order.  A thread takes VEC consecutive elements of one row (cin % VEC == 0) and loads sixteen
 // units' values before adding them in order, so the partials stream instead of one round trip
 // per unit.
 template <int VEC>
@@ -350,13 +350,15 @@ __global__ __launch_bounds__(256) void reduce_units_kernel(const float* __restri
   float acc[VEC];
 #pragma unroll
   for (int k = 0; k < VEC; ++k) acc[k] = 0.f;
-  const int u1 = units.uoff[s + 1];
-  int u = units.uoff[s];
-  for (; u + 8 <= u1; u += 8) {
-    float v[8][VEC];
+  // batches of 16 units: every load issued (a unit past the offset's last reads that last unit
+  // again and contributes +0, which leaves the sum unchanged: it never holds -0), then the adds in
+  // unit order
+  const int u0 = units.uoff[s], u1 = units.uoff[s + 1];
+  for (int u = u0; u < u1; u += 16) {
+    float v[16][VEC];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float* p = part + (int64_t)(u + j) * n + e;
+    for (int j = 0; j < 16; ++j) {
+      const float* p = part + (int64_t)min(u + j, u1 - 1) * n + e;
       if constexpr (VEC == 4) {
         const float4 t = *reinterpret_cast<const float4*>(p);
         v[j][0] = t.x, v[j][1] = t.y, v[j][2] = t.z, v[j][3] = t.w;
@@ -365,13 +367,10 @@ __global__ __launch_bounds__(256) void reduce_units_kernel(const float* __restri
       }
     }
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
+    for (int j = 0; j < 16; ++j)
 #pragma unroll
-      for (int k = 0; k < VEC; ++k) acc[k] += v[j][k];
+      for (int k = 0; k < VEC; ++k) acc[k] += u + j < u1 ? v[j][k] : 0.f;
   }
-  for (; u < u1; ++u)
-#pragma unroll
-    for (int k = 0; k < VEC; ++k) acc[k] += part[(int64_t)u * n + e + k];
   const int o = e / cin;
 #pragma unroll
   for (int k = 0; k < VEC; ++k) dW[dw_block_pos(fout, fin, units.K, cin, s, o, e + k - o * cin)] = acc[k];

@@ -141,6 +141,7 @@ __global__ __launch_bounds__(256) void synth_adjoint_kernel(SynthArgs a, const f
     }
 #pragma unroll
     for (int j = 0; j < kQB; ++j) {
+      if (q0 + j >= nq) break;  // uniform per workgroup: no butterflies for absent coefficients
       float v = acc[j];
 #pragma unroll
       for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
@@ -201,6 +202,7 @@ __global__ __launch_bounds__(256) void synth_adjoint_wave_kernel(SynthArgs a, co
     float mine = 0.f;  // lane j keeps coefficient j's sum
 #pragma unroll
     for (int j = 0; j < kQB; ++j) {
+      if (q0 + j >= nq) break;  // uniform per wavefront: no butterflies for absent coefficients
       float v = acc[j];
 #pragma unroll
       for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
