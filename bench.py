@@ -231,7 +231,9 @@ class SingleLayer:
         W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt)
         if ev:
             ev[1].record()
-        rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, L.stride, L.submanifold)
+        # asynchronous build: the forward is queued behind it without a host round trip (a bf16
+        # forward needs only the neighbour map; the backward settles the build)
+        rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, L.stride, L.submanifold, asynchronous=True)
         if ev:
             ev[2].record()
         out = P.forward(self.feats, rb, W)
@@ -450,7 +452,7 @@ class BlockBench:
                 next(marks).record()
         W = P.synth_kernel(self.desc, self.basis, self.coeffs, torch.float32)
         mark()
-        rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, 1, True)
+        rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, 1, True, asynchronous=True)
         mark()
         y, z = P.forward_norm(self.feats, rb, W, L.fields_out)
         mark()

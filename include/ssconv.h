@@ -24,7 +24,9 @@
  *    handle is returned (the out-handle is set to NULL).
  *  - Work is enqueued on the given stream and is asynchronous, except
  *    ssconv_build_rulebook, which synchronises the stream to size its
- *    outputs and to report device-detected errors.
+ *    outputs and to report device-detected errors (ssconv_build_rulebook_async
+ *    defers that for submanifold layers), and the calls that settle such a
+ *    build.
  *  - Sites are int32 (b, x, y, z) with 0 <= x < grid[0], 0 <= y < grid[1],
  *    0 <= z < grid[2], b >= 0 and (max b + 1) * grid[0]*grid[1]*grid[2] < 2^32.
  *  - Kernel offsets s = (dx, dy, dz) in S = {-h..ksize-1-h}^3, h = ksize/2
@@ -142,6 +144,27 @@ int ssconv_basis_build(const ssconv_basis_desc* desc /*host*/, float* basis /*ho
 int ssconv_build_rulebook(const int32_t* coords, int64_t n, const int32_t* grid /*host [3]*/,
                           int ksize, int stride, int submanifold, hipStream_t stream,
                           ssconv_rulebook_t* out /*host*/);
+/* The same build without its final synchronisation, for submanifold layers
+ * (generated output sets synchronise as ssconv_build_rulebook does, since the
+ * output count sizes their buffers): the handle is returned as soon as the
+ * build's kernels and the read-back of its pair counts are queued on `stream`.
+ * The pair counts, and the errors the device detects (E_BOUNDS, E_DUPLICATE,
+ * E_HASH_FULL), reach the host when the build is settled: by
+ * ssconv_rulebook_wait, or by the first call that needs them (rulebook info,
+ * pairs and hash, backward and its workspace size, fp32 forwards, pooling,
+ * interpolation), which then returns that error.  The neighbour map is complete
+ * on `stream`, so a bf16 forward and the map and site copies may be queued
+ * before the build is settled; if the build then reports an error, their
+ * results are undefined (never an access out of bounds: every map entry is a
+ * row of the input or -1).  Argument errors and allocation failures are
+ * returned at once, as by ssconv_build_rulebook. */
+int ssconv_build_rulebook_async(const int32_t* coords, int64_t n, const int32_t* grid /*host [3]*/,
+                                int ksize, int stride, int submanifold, hipStream_t stream,
+                                ssconv_rulebook_t* out /*host*/);
+/* Settles an asynchronous build (blocks the host until its read-back has
+ * arrived) and returns the build's result; a synchronous build returns
+ * SSCONV_OK.  Every later call returns the same result. */
+int ssconv_rulebook_wait(ssconv_rulebook_t rb);
 
 /* n_in, n_out (host) and, if non-NULL, pair_counts (host [ksize^3]) = |R_s|. */
 int ssconv_rulebook_info(ssconv_rulebook_t rb, int64_t* n_in, int64_t* n_out,

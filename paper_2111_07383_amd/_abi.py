@@ -37,6 +37,9 @@ SIGNATURES = {
     "ssconv_basis_build": (c_int, [POINTER(BasisDesc), c_void_p]),
     "ssconv_build_rulebook": (c_int, [c_void_p, c_int64, POINTER(c_int), c_int, c_int, c_int, c_void_p,
                                       POINTER(c_void_p)]),
+    "ssconv_build_rulebook_async": (c_int, [c_void_p, c_int64, POINTER(c_int), c_int, c_int, c_int, c_void_p,
+                                            POINTER(c_void_p)]),
+    "ssconv_rulebook_wait": (c_int, [c_void_p]),
     "ssconv_rulebook_info": (c_int, [c_void_p, POINTER(c_int64), POINTER(c_int64), POINTER(c_int64)]),
     "ssconv_rulebook_out_coords": (c_int, [c_void_p, c_void_p, c_void_p]),
     "ssconv_rulebook_pairs": (c_int, [c_void_p, c_void_p, c_void_p]),

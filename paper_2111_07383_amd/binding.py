@@ -92,10 +92,14 @@ def basis_build(desc: BasisDesc) -> np.ndarray:
 
 
 class Rulebook:
-    """Owner of an ssconv_rulebook_t (hash tables, neighbour map, pair lists)."""
+    """Owner of an ssconv_rulebook_t (hash tables, neighbour map, pair lists).
+
+    ``asynchronous``: ssconv_build_rulebook_async -- a submanifold build returns before its pair
+    counts reach the host; ``pair_counts`` / ``n_pairs`` (and ``wait()``) settle it, and so does
+    every library call that needs them."""
 
     def __init__(self, coords: torch.Tensor, grid, ksize: int, stride: int = 1, submanifold: bool = True,
-                 stream=None):
+                 stream=None, asynchronous: bool = False):
         _need(coords, "coords", torch.int32)
         if coords.dim() != 2 or coords.shape[1] != 4:
             raise ValueError("coords must be [n, 4] (b, x, y, z)")
@@ -103,17 +107,40 @@ class Rulebook:
         h = c_void_p()
         self._h = None
         self.device = coords.device
-        check(lib().ssconv_build_rulebook(_ptr(coords), coords.shape[0], g, int(ksize), int(stride),
-                                          int(bool(submanifold)), _stream(stream), byref(h)),
-              "ssconv_build_rulebook")
+        build = lib().ssconv_build_rulebook_async if asynchronous else lib().ssconv_build_rulebook
+        check(build(_ptr(coords), coords.shape[0], g, int(ksize), int(stride), int(bool(submanifold)),
+                    _stream(stream), byref(h)), "ssconv_build_rulebook")
         self._h = h
         self.ksize, self.K, self.stride, self.submanifold = ksize, ksize ** 3, stride, bool(submanifold)
-        n_in, n_out = c_int64(), c_int64()
-        counts = (c_int64 * self.K)()
-        check(lib().ssconv_rulebook_info(h, byref(n_in), byref(n_out), counts), "ssconv_rulebook_info")
-        self.n_in, self.n_out = n_in.value, n_out.value
-        self.pair_counts = np.array(counts[:], np.int64)
-        self.n_pairs = int(self.pair_counts.sum())
+        self._counts = None
+        self.n_in = int(coords.shape[0])
+        if self.submanifold:
+            self.n_out = self.n_in
+        else:
+            self._settle()
+        if not asynchronous:
+            self._settle()
+
+    def _settle(self):
+        if self._counts is None:
+            n_in, n_out = c_int64(), c_int64()
+            counts = (c_int64 * self.K)()
+            check(lib().ssconv_rulebook_info(self.handle, byref(n_in), byref(n_out), counts), "ssconv_rulebook_info")
+            self.n_in, self.n_out = n_in.value, n_out.value
+            self._counts = np.array(counts[:], np.int64)
+        return self._counts
+
+    def wait(self):
+        """Settles an asynchronous build (raises its error, if any)."""
+        check(lib().ssconv_rulebook_wait(self.handle), "ssconv_rulebook_wait")
+
+    @property
+    def pair_counts(self) -> np.ndarray:
+        return self._settle()
+
+    @property
+    def n_pairs(self) -> int:
+        return int(self._settle().sum())
 
     @property
     def handle(self) -> c_void_p:

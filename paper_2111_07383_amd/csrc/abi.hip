@@ -27,6 +27,9 @@ int check_conv_args(const void* a, const void* b, ssconv_dtype dt, int cin, int 
 extern "C" int ssconv_forward(const void* feats, ssconv_dtype dtype, int cin, ssconv_rulebook_t rb, const void* W,
                               int cout, void* out, hipStream_t stream) {
   SSC_TRY(check_conv_args(feats, out, dtype, cin, cout, rb, W));
+  // fp32 picks its kernel from the pair counts; bf16 needs only the neighbour map, so it may run
+  // on an asynchronous build that has not been settled yet
+  if (dtype != SSCONV_BF16) SSC_TRY(rulebook_settle(rb));
   if ((rb->n_in > 0 && !feats) || (rb->n_out > 0 && !out)) return fail(SSCONV_E_INVALID, "NULL feature buffer");
   if (rb->n_in == 0 && rb->n_out > 0) {
     SSC_HIP(hipMemsetAsync(out, 0, (size_t)rb->n_out * cout * dtype_bytes(dtype), stream));
@@ -43,6 +46,7 @@ extern "C" int ssconv_forward_norm(const void* feats, ssconv_dtype dtype, int ci
   SSC_TRY(norm_check_fields(fields_out, dtype, rb ? rb->n_out : 0, eps, &f));
   const int cout = f.ch0[f.n];
   SSC_TRY(check_conv_args(feats, y, dtype, cin, cout, rb, W));
+  if (dtype != SSCONV_BF16) SSC_TRY(rulebook_settle(rb));
   if (z && !aligned16(z)) return fail(SSCONV_E_INVALID, "device buffers must be 16-byte aligned");
   if ((rb->n_in > 0 && !feats) || (rb->n_out > 0 && (!y || !z))) return fail(SSCONV_E_INVALID, "NULL feature buffer");
   return conv_forward_norm(feats, dtype, cin, rb, W, cout, f, eps, y, z, stream);
@@ -89,6 +93,7 @@ __global__ void zero_halves_kernel(uint16_t* __restrict__ p, int64_t n) {
 extern "C" int ssconv_forward_noalloc(const void* feats, ssconv_dtype dtype, int cin, ssconv_rulebook_t rb,
                                       const void* W, int cout, void* out, hipStream_t stream) {
   SSC_TRY(check_conv_args(feats, out, dtype, cin, cout, rb, W));
+  if (dtype != SSCONV_BF16) SSC_TRY(rulebook_settle(rb));
   if ((rb->n_in > 0 && !feats) || (rb->n_out > 0 && !out)) return fail(SSCONV_E_INVALID, "NULL feature buffer");
   if (rb->n_out == 0) return SSCONV_OK;
   if (rb->n_in == 0) {  // no input rows: every output row is 0 (a fill kernel, no memset node)
@@ -105,6 +110,7 @@ extern "C" int ssconv_forward_noalloc(const void* feats, ssconv_dtype dtype, int
 
 extern "C" size_t ssconv_backward_workspace_size(ssconv_rulebook_t rb, ssconv_dtype dtype, int cin, int cout) {
   if (!rb || cin < 1 || cout < 1) return 0;
+  if (rulebook_settle(rb) != SSCONV_OK) return 0;
   return bwd_layout(rb, dtype, cin, cout).total;
 }
 
@@ -113,6 +119,7 @@ extern "C" int ssconv_backward(const void* feats, const void* grad_out, ssconv_d
                                void* grad_feats, float* grad_coeffs, void* workspace, size_t ws_bytes,
                                hipStream_t stream) {
   SSC_TRY(check_conv_args(feats, grad_out, dtype, cin, cout, rb, W));
+  SSC_TRY(rulebook_settle(rb));
   if (grad_feats && !aligned16(grad_feats)) return fail(SSCONV_E_INVALID, "grad_feats must be 16-byte aligned");
   const BwdLayout L = bwd_layout(rb, dtype, cin, cout);
   if (!workspace || ws_bytes < L.total || (reinterpret_cast<uintptr_t>(workspace) & 255))

@@ -138,4 +138,19 @@ struct ssconv_rulebook {
   void* mem[3] = {nullptr, nullptr, nullptr};  // the allocations every buffer above lives in
   // host copies
   int64_t* pair_off = nullptr;  // [K + 1] (host)
+  // An asynchronous submanifold build returns before its pair counts and flags reach the host:
+  // they arrive in `stage` (pinned, from the library's pool) when `ready` has passed, and
+  // rulebook_settle() reads them on first need; `status` then holds the build's result.
+  bool pending = false;
+  int status = 0;
+  char error[192] = {0};
+  hipEvent_t ready = nullptr;
+  int64_t* stage = nullptr;
 };
+
+namespace ssconv {
+// Completes an asynchronous build (waits for its read-back, fills pair_off / n_pairs, turns the
+// device-detected errors into the build's status); returns that status on every call.  A build
+// made synchronously is settled already.
+int rulebook_settle(ssconv_rulebook* rb);
+}  // namespace ssconv

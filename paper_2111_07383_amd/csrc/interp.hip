@@ -140,6 +140,7 @@ __global__ void interp_bwd_kernel(const float* __restrict__ grad, int C, const f
 
 int interp_args(ssconv_rulebook_t rb, int C, const float* points, int64_t m, const float* origin, float voxel) {
   if (!rb) return fail(SSCONV_E_INVALID, "NULL rule book");
+  SSC_TRY(rulebook_settle(rb));
   if (C < 1) return fail(SSCONV_E_INVALID, "channels must be positive");
   if (m < 0 || m > 0x0fffffffll) return fail(SSCONV_E_INVALID, "m must be in [0, 2^28)");
   if (!origin || !(voxel > 0.f) || !std::isfinite(voxel)) return fail(SSCONV_E_INVALID, "bad origin / voxel");

@@ -607,6 +607,7 @@ int pool_run(const void* src, int C, const ssconv_rulebook* rb, void* dst, hipSt
 int check_pool(ssconv_dtype dt, int C, ssconv_rulebook_t rb, const void* a, const void* b) {
   if (dt != SSCONV_F32 && dt != SSCONV_BF16) return fail(SSCONV_E_DTYPE, "unsupported dtype %d", (int)dt);
   if (!rb) return fail(SSCONV_E_INVALID, "NULL rule book");
+  SSC_TRY(rulebook_settle(rb));
   if (rb->ksize != 2 || rb->stride != 2)
     return fail(SSCONV_E_INVALID, "pooling needs a rule book built with ksize 2, stride 2");
   if (C < 1) return fail(SSCONV_E_INVALID, "channels must be positive");

@@ -16,6 +16,9 @@
 // (input, offset) being the rank of its bit, so no table of the outputs is
 // probed (it is built only if a caller asks for it).
 #include <algorithm>
+#include <cstdio>
+#include <mutex>
+#include <vector>
 
 #include "hash.hpp"
 #include "scan.hpp"
@@ -381,10 +384,80 @@ struct Staging {
 };
 thread_local Staging g_stage;
 
+// Pinned read-back buffers and events of asynchronous builds, reused across builds (a pinned
+// allocation or an event creation per build would cost host time on every call).
+struct StagePool {
+  std::mutex mu;
+  std::vector<std::pair<int64_t*, hipEvent_t>> free_list;
+  int get(int64_t** buf, hipEvent_t* ev) {
+    {
+      std::lock_guard<std::mutex> lk(mu);
+      if (!free_list.empty()) {
+        *buf = free_list.back().first;
+        *ev = free_list.back().second;
+        free_list.pop_back();
+        return SSCONV_OK;
+      }
+    }
+    void* q = nullptr;
+    if (hipHostMalloc(&q, 4096, hipHostMallocDefault) != hipSuccess || !q) {
+      (void)hipGetLastError();
+      return fail(SSCONV_E_NOMEM, "pinned host staging allocation failed");
+    }
+    if (hipEventCreateWithFlags(ev, hipEventDisableTiming) != hipSuccess) {
+      (void)hipGetLastError();
+      (void)hipHostFree(q);
+      return fail(SSCONV_E_HIP, "event creation failed");
+    }
+    *buf = (int64_t*)q;
+    return SSCONV_OK;
+  }
+  void put(int64_t* buf, hipEvent_t ev) {
+    std::lock_guard<std::mutex> lk(mu);
+    free_list.emplace_back(buf, ev);
+  }
+};
+StagePool g_stage_pool;
+
+// Reads the pair counts and the build flags from host memory (the read-back has completed).
+int settle_from(ssconv_rulebook* rb, const int64_t* host) {
+  const int K = rb->K;
+  for (int s = 0; s <= K; ++s) rb->pair_off[s] = host[s];
+  rb->n_pairs = host[K];
+  const int fl = (int)(host[K + 1] & 0xffffffff);
+  if (fl & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid, has b < 0, or (max b + 1) * grid volume exceeds the 32-bit key space");
+  if (fl & kFlagDup) return fail(SSCONV_E_DUPLICATE, "duplicate input site");
+  if (fl & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
+  return SSCONV_OK;
+}
+
 }  // namespace
+
+int rulebook_settle(ssconv_rulebook* rb) {
+  if (rb->pending) {
+    rb->pending = false;
+    int rc;
+    if (hipEventSynchronize(rb->ready) != hipSuccess) {
+      (void)hipGetLastError();
+      rc = fail(SSCONV_E_HIP, "waiting for the rule book build failed");
+    } else {
+      rc = settle_from(rb, rb->stage);
+    }
+    rb->status = rc;
+    if (rc != SSCONV_OK) snprintf(rb->error, sizeof(rb->error), "%s", ssconv_last_error());
+    return rc;
+  }
+  if (rb->status != SSCONV_OK) return fail(rb->status, "%s", rb->error);
+  return SSCONV_OK;
+}
 
 void rulebook_free(ssconv_rulebook* rb) {
   if (!rb) return;
+  if (rb->stage) {
+    if (rb->pending) (void)hipEventSynchronize(rb->ready);  // the read-back still writes the stage
+    (void)hipGetLastError();
+    g_stage_pool.put(rb->stage, rb->ready);
+  }
   for (void* m : rb->mem) dev_free(m, rb->stream);  // every device buffer lives in these blocks
   delete[] rb->pair_off;
   delete rb;
@@ -447,21 +520,24 @@ static int build_hash(const int32_t* coords, int64_t n, const int* g, hipStream_
 
 // Pair offsets and flags in one copy: the one synchronisation of a submanifold build (the last of
 // a generated one); device-detected errors surface here.
-static int finish_build(ssconv_rulebook* rb, int64_t* host, hipStream_t st) {
+// The one read-back of a build: the pair counts and the flags.  async: queued into a pooled
+// pinned buffer with an event behind it, settled later (rulebook_settle).
+static int finish_build(ssconv_rulebook* rb, int64_t* host, hipStream_t st, bool async) {
   const int K = rb->K;
+  if (async) {
+    SSC_TRY(g_stage_pool.get(&rb->stage, &rb->ready));
+    SSC_HIP(hipMemcpyAsync(rb->stage, rb->pair_off_dev, (size_t)(K + 2) * 8, hipMemcpyDeviceToHost, st));
+    SSC_HIP(hipEventRecord(rb->ready, st));
+    rb->pending = true;
+    return SSCONV_OK;
+  }
   SSC_HIP(hipMemcpyAsync(host, rb->pair_off_dev, (size_t)(K + 2) * 8, hipMemcpyDeviceToHost, st));
   SSC_HIP(hipStreamSynchronize(st));
-  for (int s = 0; s <= K; ++s) rb->pair_off[s] = host[s];
-  rb->n_pairs = host[K];
-  const int fl = (int)(host[K + 1] & 0xffffffff);
-  if (fl & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid, has b < 0, or (max b + 1) * grid volume exceeds the 32-bit key space");
-  if (fl & kFlagDup) return fail(SSCONV_E_DUPLICATE, "duplicate input site");
-  if (fl & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
-  return SSCONV_OK;
+  return settle_from(rb, host);
 }
 
 static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int ksize, int stride, int submanifold,
-                      hipStream_t st, ssconv_rulebook* rb) {
+                      hipStream_t st, ssconv_rulebook* rb, bool async) {
   rb->ksize = ksize;
   rb->K = ksize * ksize * ksize;
   rb->stride = stride;
@@ -531,7 +607,7 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     SSC_HIP(hipGetLastError());
     if (rb->pairs) {
       SSC_TRY(compact_pairs(rb->nbr, n, K, tile_cnt, rb->pairs, rb->pair_off_dev, st));
-      return finish_build(rb, host, st);
+      return finish_build(rb, host, st, async);
     }
     // past 1 GB of pairs at the upper bound: counted, scanned and sized exactly below
   }
@@ -631,7 +707,7 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
                                                               owoff, n_out, rb->nbr);
       if (rb->pairs) {
         SSC_TRY(compact_pairs(rb->nbr, n_out, K, (int64_t*)(t1 + o_lb), rb->pairs, rb->pair_off_dev, st));
-        return finish_build(rb, host, st);
+        return finish_build(rb, host, st, false);
       }
       pair_list_kernel<kCount><<<gp, 256, 0, st>>>(n_out, nblk, rb->nbr, counts, nullptr, nullptr);
     }
@@ -655,15 +731,17 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
       rb->pairs = (int32_t*)rb->mem[2];
     }
   }
-  return finish_build(rb, host, st);
+  return finish_build(rb, host, st, false);
 }
 
 }  // namespace ssconv
 
 using namespace ssconv;
 
-extern "C" int ssconv_build_rulebook(const int32_t* coords, int64_t n, const int32_t* grid, int ksize, int stride,
-                                     int submanifold, hipStream_t stream, ssconv_rulebook_t* out) {
+namespace {
+
+int build_entry(const int32_t* coords, int64_t n, const int32_t* grid, int ksize, int stride, int submanifold,
+                hipStream_t stream, ssconv_rulebook_t* out, bool async) {
   if (!out) return fail(SSCONV_E_INVALID, "out handle pointer is NULL");
   *out = nullptr;
   if (!grid) return fail(SSCONV_E_INVALID, "grid is NULL");
@@ -680,7 +758,7 @@ extern "C" int ssconv_build_rulebook(const int32_t* coords, int64_t n, const int
   for (int a = 0; a < 3; ++a)
     if (grid[a] < 1) return fail(SSCONV_E_INVALID, "grid extents must be positive");
   auto* rb = new ssconv_rulebook();
-  int rc = build_impl(coords, n, grid, ksize, stride, submanifold ? 1 : 0, stream, rb);
+  int rc = build_impl(coords, n, grid, ksize, stride, submanifold ? 1 : 0, stream, rb, async);
   if (rc != SSCONV_OK) {
     std::string msg = ssconv_last_error();
     rulebook_free(rb);
@@ -691,8 +769,26 @@ extern "C" int ssconv_build_rulebook(const int32_t* coords, int64_t n, const int
   return SSCONV_OK;
 }
 
+}  // namespace
+
+extern "C" int ssconv_build_rulebook(const int32_t* coords, int64_t n, const int32_t* grid, int ksize, int stride,
+                                     int submanifold, hipStream_t stream, ssconv_rulebook_t* out) {
+  return build_entry(coords, n, grid, ksize, stride, submanifold, stream, out, false);
+}
+
+extern "C" int ssconv_build_rulebook_async(const int32_t* coords, int64_t n, const int32_t* grid, int ksize,
+                                           int stride, int submanifold, hipStream_t stream, ssconv_rulebook_t* out) {
+  return build_entry(coords, n, grid, ksize, stride, submanifold, stream, out, true);
+}
+
+extern "C" int ssconv_rulebook_wait(ssconv_rulebook_t rb) {
+  if (!rb) return fail(SSCONV_E_INVALID, "NULL rule book");
+  return rulebook_settle(rb);
+}
+
 extern "C" int ssconv_rulebook_info(ssconv_rulebook_t rb, int64_t* n_in, int64_t* n_out, int64_t* pair_counts) {
   if (!rb) return fail(SSCONV_E_INVALID, "NULL rule book");
+  SSC_TRY(rulebook_settle(rb));
   if (n_in) *n_in = rb->n_in;
   if (n_out) *n_out = rb->n_out;
   if (pair_counts)
@@ -707,7 +803,9 @@ extern "C" int ssconv_rulebook_out_coords(ssconv_rulebook_t rb, int32_t* dst, hi
 }
 
 extern "C" int ssconv_rulebook_pairs(ssconv_rulebook_t rb, int32_t* dst, hipStream_t stream) {
-  if (!rb || (!dst && rb->n_pairs)) return fail(SSCONV_E_INVALID, "NULL argument");
+  if (!rb) return fail(SSCONV_E_INVALID, "NULL rule book");
+  SSC_TRY(rulebook_settle(rb));
+  if (!dst && rb->n_pairs) return fail(SSCONV_E_INVALID, "NULL argument");
   if (rb->n_pairs) SSC_HIP(hipMemcpyAsync(dst, rb->pairs, (size_t)rb->n_pairs * 8, hipMemcpyDeviceToDevice, stream));
   return SSCONV_OK;
 }
@@ -722,6 +820,7 @@ extern "C" int ssconv_rulebook_neighbours(ssconv_rulebook_t rb, int32_t* dst, hi
 extern "C" int ssconv_rulebook_hash(ssconv_rulebook_t rb, int which, uint64_t* dst, int64_t* capacity,
                                     hipStream_t stream) {
   if (!rb || (which != 0 && which != 1)) return fail(SSCONV_E_INVALID, "bad argument");
+  SSC_TRY(rulebook_settle(rb));
   if (which && rb->hash_out != rb->hash_in && !rb->hash_out_built) {
     // a generated output set's table is filled on first request, on the caller's stream
     int* dflags = (int*)(rb->pair_off_dev + rb->K + 1);

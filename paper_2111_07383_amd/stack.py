@@ -96,11 +96,12 @@ class Stack:
         return self._side_stream
 
     def _prepare(self, i: int, coords: torch.Tensor):
-        """Kernel and rule book of layer i on the current stream (the build synchronises it)."""
+        """Kernel and rule book of layer i on the current stream (a generated output set's build
+        synchronises it; a submanifold build is settled by the first call that needs its counts)."""
         L = self.layers[i]
         s = L.layer
         L.W = B.synth_kernel(L.desc, L.basis, L.coeffs, self.dtype)
-        L.rb = B.Rulebook(coords, L.grid, s.ksize, s.stride, s.submanifold)
+        L.rb = B.Rulebook(coords, L.grid, s.ksize, s.stride, s.submanifold, asynchronous=True)
 
     def backward(self, grad: torch.Tensor, need_input_grad: bool = True):
         """Returns (grad of the stack input or None, [grad_coeffs per layer])."""
@@ -158,7 +159,7 @@ class DownBlock:
             if rb is not None:
                 rb.close()
         L.W = B.synth_kernel(L.desc, L.basis, L.coeffs, self.dtype)
-        L.rb = B.Rulebook(coords, L.grid, s.ksize, 1, True)
+        L.rb = B.Rulebook(coords, L.grid, s.ksize, 1, True, asynchronous=True)
         L.x = feats
         L.y, self.z = B.forward_norm(feats, L.rb, L.W, s.fields_out, self.norm_eps)
         h = B.gate_forward(regular_fields(s), self.z) if s.gated else self.z

@@ -65,6 +65,69 @@ def test_error_codes():
     rb.close()
 
 
+def test_async_rulebook_matches_sync():
+    """ssconv_build_rulebook_async: pairs, neighbour map and hash contents equal the synchronous
+    build's; a
+    bf16 forward queued before the build is settled, the fp32 forward (which settles it) and the
+    backward give the same bits as on the synchronous build."""
+    from cases import coords_of, layers_of
+    L = layers_of(4)[0]
+    c = torch.from_numpy(L.coords_in).to(DEV)
+    gen = torch.Generator(DEV).manual_seed(3)
+    rb_s = P.Rulebook(c, L.grid, 3, 1, True)
+    rb_a = P.Rulebook(c, L.grid, 3, 1, True, asynchronous=True)
+    W = (torch.randn(27, 16, 24, device=DEV, generator=gen) * 0.2).to(torch.bfloat16)
+    f = torch.randn(rb_s.n_in, 24, device=DEV, generator=gen).to(torch.bfloat16)
+    y_a = P.forward(f, rb_a, W)                         # queued on the unsettled build
+    y_s = P.forward(f, rb_s, W)
+    assert torch.equal(y_a, y_s)
+    assert rb_a.n_pairs == rb_s.n_pairs and np.array_equal(rb_a.pair_counts, rb_s.pair_counts)
+    assert torch.equal(rb_a.pairs(), rb_s.pairs()) and torch.equal(rb_a.neighbours(), rb_s.neighbours())
+    # the table's contents as a set (concurrent inserts place keys in race-dependent slots)
+    assert torch.equal(torch.sort(rb_a.hash_slots(0))[0], torch.sort(rb_s.hash_slots(0))[0])
+    g = torch.randn(rb_s.n_out, 16, device=DEV, generator=gen).to(torch.bfloat16)
+    assert torch.equal(P.backward(f, g, rb_a, W, need_coeffs=False)[0], P.backward(f, g, rb_s, W, need_coeffs=False)[0])
+    rb_a.close()
+    rb_a = P.Rulebook(c, L.grid, 3, 1, True, asynchronous=True)
+    W32, f32 = W.float(), f.float()
+    assert torch.equal(P.forward(f32, rb_a, W32), P.forward(f32, rb_s, W32))   # fp32 settles first
+    rb_a.close()
+    rb_s.close()
+    P.Rulebook(c, L.grid, 3, 1, True, asynchronous=True).close()   # destroyed before it is settled
+
+
+def test_async_rulebook_reports_errors_when_settled():
+    """The errors the device detects surface when the asynchronous build is settled: by wait(),
+    the pair counts, an fp32 forward or the backward; a bf16 forward queued before that runs (its
+    result is undefined) without any access outside the buffers."""
+    c = torch.from_numpy(_coords(0, 50, 8)).to(DEV)
+    dup = torch.cat([c, c[:1]])
+    rb = P.Rulebook(dup, 8, 3, asynchronous=True)       # no error yet
+    gen = torch.Generator(DEV).manual_seed(4)
+    W = torch.randn(27, 8, 8, device=DEV, generator=gen).to(torch.bfloat16)
+    f = torch.randn(len(dup), 8, device=DEV, generator=gen).to(torch.bfloat16)
+    P.forward(f, rb, W)
+    torch.cuda.synchronize()
+    assert _code(lambda: rb.wait()) == E_DUPLICATE
+    assert _code(lambda: rb.wait()) == E_DUPLICATE      # the same result on every call
+    assert _code(lambda: rb.n_pairs) == E_DUPLICATE
+    assert _code(lambda: P.forward(f.float(), rb, W.float())) == E_DUPLICATE
+    g = torch.zeros(len(dup), 8, device=DEV, dtype=torch.bfloat16)
+    assert _code(lambda: P.backward(f, g, rb, W, need_coeffs=False)) == E_DUPLICATE
+    rb.close()
+    P.debug_set(1, 16)                                  # 16 slots for 50 sites
+    try:
+        rb = P.Rulebook(c, 8, 3, asynchronous=True)
+        assert _code(lambda: rb.wait()) == E_HASH_FULL
+        rb.close()
+    finally:
+        P.debug_set(1, 0)
+    rb = P.Rulebook(c, 8, 3, asynchronous=True)         # a clean build settles without error
+    rb.wait()
+    assert rb.n_pairs > 0
+    rb.close()
+
+
 def test_empty_input():
     c = torch.zeros((0, 4), dtype=torch.int32, device=DEV)
     for stride, sub in ((1, True), (2, False)):
