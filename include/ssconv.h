@@ -394,8 +394,9 @@ int ssconv_interpolate_backward(ssconv_rulebook_t rb, const float* grad, int cha
  * (one GEMM per offset over R_s, then a per-row sum in offset order) wherever
  * it applies; 10 = never take it, which a cost model otherwise decides;
  * 11 = run the coefficient gradient of ssconv_backward on the caller's
- * stream instead of forking it onto the library's second stream next to a
- * pair-list feature gradient; 12 = the bf16 kernel gradient stages its
+ * stream instead of forking it onto the library's second stream (all of it
+ * next to a pair-list feature gradient, its reduction and synthesis adjoint
+ * next to the fp32 gather kernel); 12 = the bf16 kernel gradient stages its
  * operands as 16-byte granule columns instead of 64-byte quads (the same
  * results, bit for bit); results
  * agree within the dtype's tolerance for every value); option 4 = kernel

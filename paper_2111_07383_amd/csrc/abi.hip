@@ -137,16 +137,28 @@ extern "C" int ssconv_backward(const void* feats, const void* grad_out, ssconv_d
   // depend on the feature gradient.  When the feature gradient takes the pair-list path (a chain
   // of small launches) the coefficient gradient runs on the library's second stream, forked from
   // and joined back to the caller's, so the two overlap (disjoint workspace regions).  Next to
-  // the output-stationary gather kernels it is not forked: measured, the bf16 gather and the
-  // kernel gradient slow each other down (C4 step 1.49 -> 1.56 ms), and the fp32 gain is 1%.
-  // Kernel-selection override 11 switches the fork off.
+  // the fp32 output-stationary gather kernel only its tail is forked: the kernel gradient runs on
+  // the caller's stream, then its reduction and the synthesis adjoint (small, memory-bound) run
+  // on the second stream next to the feature gradient (C2 backward 1.437 -> 1.424 ms).  Next to
+  // the bf16 gather nothing is forked: the tail cost it 0.802 -> 0.809 ms (C4 backward), and the
+  // whole coefficient gradient made the two slow each other down (C4 step 1.49 -> 1.56 ms).
+  // Kernel-selection override 11 switches both forks off.
   hipStream_t dw_stream = stream;
-  const bool fork = grad_feats && grad_coeffs && rb->n_out > 0 && L.pair_feats && debug_gather_variant() != 11;
+  const bool both = grad_feats && grad_coeffs && rb->n_out > 0 && debug_gather_variant() != 11;
+  const bool fork = both && L.pair_feats;
+  const bool fork_tail = both && !L.pair_feats && rb->n_in > 0 && dtype == SSCONV_F32;
+  bool need_join = fork;
   if (fork) SSC_TRY(aux_fork(stream, &dw_stream));
   int rc = SSCONV_OK;
   if (grad_coeffs) {
     float* dW = nullptr;
-    rc = conv_backward_dw(feats, grad_out, dtype, cin, cout, rb, sa.out, sa.in, ws, L, &dW, dw_stream);
+    hipStream_t tail = dw_stream;
+    rc = conv_backward_dw(feats, grad_out, dtype, cin, cout, rb, sa.out, sa.in, ws, L, &dW, dw_stream,
+                          fork_tail ? &tail : nullptr);
+    if (fork_tail && tail != stream) {
+      dw_stream = tail;
+      need_join = true;
+    }
     if (rc == SSCONV_OK) rc = launch_synth_adjoint(sa, basis, dW, grad_coeffs, dw_stream);
   }
   if (rc == SSCONV_OK && grad_feats) {
@@ -157,7 +169,7 @@ extern "C" int ssconv_backward(const void* feats, const void* grad_out, ssconv_d
       rc = conv_backward_feats(grad_out, dtype, cin, cout, rb, W, grad_feats, ws, L, stream);
     }
   }
-  if (fork) {
+  if (need_join) {
     const int jr = aux_join(stream, dw_stream);  // always joined, so nothing stays pending on the side stream
     if (rc == SSCONV_OK) rc = jr;
   }

@@ -523,10 +523,11 @@ int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout
 
 int conv_backward_dw(const void* feats, const void* grad_out, ssconv_dtype dt, int cin, int cout,
                      const ssconv_rulebook* rb, const FieldTab& fout, const FieldTab& fin, char* ws,
-                     const BwdLayout& L, float** dW_out, hipStream_t st) {
+                     const BwdLayout& L, float** dW_out, hipStream_t st, hipStream_t* tail) {
   float* part = (float*)(ws + L.part);
   float* dW = (float*)(ws + L.dW);
   *dW_out = dW;
+  if (tail) *tail = st;
   const int K = rb->K;
   const int64_t n = (int64_t)K * cin * cout;
   if (use_kgrad_units(rb, dt, cin, cout)) {
@@ -535,7 +536,12 @@ int conv_backward_dw(const void* feats, const void* grad_out, ssconv_dtype dt, i
       SSC_TRY(kgrad_f32(grad_out, feats, cin, cout, rb, units, part, st));
     else
       SSC_TRY(kgrad_bf16(grad_out, rb->n_out, feats, rb->n_in, cin, cout, rb, units, part, st));
-    return reduce_units(part, units, cin, cout, fout, fin, dW, st);
+    hipStream_t rst = st;
+    if (tail) {
+      SSC_TRY(aux_fork(st, &rst));
+      *tail = rst;
+    }
+    return reduce_units(part, units, cin, cout, fout, fin, dW, rst);
   }
   if (kgrad_supported(dt, cin, cout))
     SSC_TRY(kgrad_partials(grad_out, feats, dt, cin, cout, rb, kgrad_plan(rb, dt, cin, cout), part, st));

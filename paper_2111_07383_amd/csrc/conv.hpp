@@ -32,8 +32,11 @@ BwdLayout bwd_layout(const ssconv_rulebook* rb, ssconv_dtype dt, int cin, int co
 int conv_backward_feats(const void* grad_out, ssconv_dtype dt, int cin, int cout, const ssconv_rulebook* rb,
                         const void* W, void* grad_feats, char* ws, const BwdLayout& L, hipStream_t st);
 // Kernel gradient dW in the field-pair-blocked layout (dw_block_pos) of the fields fout, fin.
+// With tail given, a balanced-unit kernel gradient forks its reduction onto the library's second
+// stream (aux_fork after the partials are queued on st) and *tail receives the stream dW is
+// complete on (st when nothing was forked); the caller joins it.
 int conv_backward_dw(const void* feats, const void* grad_out, ssconv_dtype dt, int cin, int cout,
                      const ssconv_rulebook* rb, const FieldTab& fout, const FieldTab& fin, char* ws,
-                     const BwdLayout& L, float** dW_out, hipStream_t st);
+                     const BwdLayout& L, float** dW_out, hipStream_t st, hipStream_t* tail = nullptr);
 
 }  // namespace ssconv

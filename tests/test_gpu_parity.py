@@ -236,11 +236,13 @@ def test_pair_path_deterministic():
     rb.close()
 
 
-def test_backward_fork_bit_identical():
-    """The coefficient gradient forked onto the library's second stream (next to a pair-list
-    feature gradient) gives the same bits as on the caller's stream (override 11)."""
-    L, dt, desc, basis, rb, W, feats = _layer_io(3)
-    g = torch.randn(rb.n_out, L.spec.cout, device=DEV, generator=torch.Generator(DEV).manual_seed(2))
+@pytest.mark.parametrize("i", [3, 2])
+def test_backward_fork_bit_identical(i):
+    """The coefficient gradient forked onto the library's second stream gives the same bits as on
+    the caller's stream (override 11): all of it next to a pair-list feature gradient (workload 3),
+    its reduction and synthesis adjoint next to the fp32 gather kernel (workload 2)."""
+    L, dt, desc, basis, rb, W, feats = _layer_io(i)
+    g = torch.randn(rb.n_out, L.spec.cout, device=DEV, generator=torch.Generator(DEV).manual_seed(2)).to(dt)
     a1, b1 = P.backward(feats, g, rb, W, desc, basis)
     P.debug_set(3, 11)
     try:
