@@ -1004,8 +1004,6 @@ def measure(args, i, steps, warmup, dev):
     torch.cuda.synchronize()
     log(f"warmup done ({warmup} steps); timing {steps} steps")
     P.debug_set(4, 1)                 # HIP events around each gather-GEMM launch, on its stream
-    if args.only == "step" and isinstance(b, SingleLayer):
-        b.events = []                 # phase boundaries of every timed step (torch's stream)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
@@ -1041,6 +1039,11 @@ def measure(args, i, steps, warmup, dev):
         b.events = []                 # per-phase times from extra sequential steps, after the timed ones
         for _ in range(10):
             b.phase_step()
+        torch.cuda.synchronize()
+    if isinstance(b, SingleLayer) and args.only == "step":
+        b.events = []                 # phase boundaries (torch's stream) of as many extra steps, after the
+        for _ in range(steps):        # timed ones, so the timed steps carry only the gather-launch events
+            b.step()
         torch.cuda.synchronize()
     if isinstance(b, StackBench) and args.only == "step":
         out["phases"] = b.serial_report()
