@@ -173,7 +173,10 @@ void dev_free(void* p, hipStream_t stream) {
   Block b = it->second;
   g_live_blocks.erase(it);
   b.stream = stream;
-  if (!b.ev && hipEventCreateWithFlags(&b.ev, hipEventDisableTiming) != hipSuccess) b.ev = nullptr;
+  // device-side ordering only (stream waits, and the wait before hipFree in ssconv_empty_cache):
+  // no system-scope fence, so a record does not write back and invalidate the caches
+  if (!b.ev && hipEventCreateWithFlags(&b.ev, hipEventDisableTiming | hipEventDisableSystemFence) != hipSuccess)
+    b.ev = nullptr;
   if (!b.ev || hipEventRecord(b.ev, stream) != hipSuccess) {
     release_block(b);
     return;
@@ -194,7 +197,10 @@ bool debug_timing_events(hipEvent_t* start, hipEvent_t* stop) {
   if (g_debug_timing.load() == 0 || g_timing.used == kMaxTimed) return false;
   if (g_timing.used == g_timing.ev.size()) {
     hipEvent_t a = nullptr, b = nullptr;
-    if (hipEventCreate(&a) != hipSuccess || hipEventCreate(&b) != hipSuccess) {
+    // timestamps only (read after the last stop event completes): no system-scope fence, which
+    // would write back and invalidate the caches around every timed launch
+    if (hipEventCreateWithFlags(&a, hipEventDisableSystemFence) != hipSuccess ||
+        hipEventCreateWithFlags(&b, hipEventDisableSystemFence) != hipSuccess) {
       if (a) (void)hipEventDestroy(a);
       (void)hipGetLastError();
       return false;
@@ -315,8 +321,9 @@ int aux_fork(hipStream_t caller, hipStream_t* side) {
     if (!g_aux[dev]) SSC_HIP(hipStreamCreateWithFlags(&g_aux[dev], hipStreamNonBlocking));
   }
   AuxEvents& e = g_aux_ev[dev];
-  if (!e.fork) SSC_HIP(hipEventCreateWithFlags(&e.fork, hipEventDisableTiming));
-  if (!e.join) SSC_HIP(hipEventCreateWithFlags(&e.join, hipEventDisableTiming));
+  // stream-to-stream ordering on one device: no system-scope fence needed
+  if (!e.fork) SSC_HIP(hipEventCreateWithFlags(&e.fork, hipEventDisableTiming | hipEventDisableSystemFence));
+  if (!e.join) SSC_HIP(hipEventCreateWithFlags(&e.join, hipEventDisableTiming | hipEventDisableSystemFence));
   SSC_HIP(hipEventRecord(e.fork, caller));
   SSC_HIP(hipStreamWaitEvent(g_aux[dev], e.fork, 0));
   *side = g_aux[dev];
