@@ -211,15 +211,38 @@ __global__ __launch_bounds__(256) void pair_list_kernel(int64_t n_out, int nblk,
   }
 }
 
+// Tiles of the pair compaction below: kCompactTile consecutive entries of the flattened map.
+constexpr int kCompactNT = 256, kCompactPer = 32, kCompactTile = kCompactNT * kCompactPer;
+constexpr int kCompactShift = 13;
+static_assert(kCompactTile == 1 << kCompactShift, "tile index by shift");
+
+// Adds this wavefront's present entries to the counts of the compaction tiles that hold them
+// (f: the entry's index in the flattened map): one atomic per distinct tile of the wavefront.
+__device__ __forceinline__ void count_tiles(bool present, int64_t f, int64_t* __restrict__ tile_cnt) {
+  const int lane = threadIdx.x & 63;
+  const int64_t t = f >> kCompactShift;
+  uint64_t left = __ballot(present);
+  while (left) {
+    const int leader = __ffsll((unsigned long long)left) - 1;
+    const int64_t tl = __shfl(t, leader, 64);
+    const uint64_t same = __ballot(present && t == tl);
+    if (lane == leader) atomicAdd((unsigned long long*)&tile_cnt[tl], (unsigned long long)__popcll(same));
+    left &= ~same;
+  }
+}
+
 // Submanifold layers (one site set, rows shared): only the offsets s < c = (K-1)/2 are looked
 // up.  If site x has neighbour y at offset s (y = x - d(s)), then y has neighbour x at the
 // mirrored offset K-1-s (d(K-1-s) = -d(s)), so that entry is written from here; distinct x
 // give distinct y, so every entry is written at most once.  Rows c..K-1 are set beforehand by
-// rb_init_kernel (c: the identity, above c: -1).  1-D XCD-ordered launch of nblk * c workgroups.
+// rb_init_kernel (c: the identity, above c: -1).  Every entry written here is also counted into the
+// compaction tile that holds it (tile_cnt, preset by rb_init_kernel with the centre row's entries),
+// so the compaction needs no counting pass.  1-D XCD-ordered launch of nblk * c workgroups.
 __global__ __launch_bounds__(256) void mirror_lookup_kernel(const int32_t* __restrict__ c_in, int64_t n, int ksize,
                                                             int g0, int g1, int g2,
                                                             const uint64_t* __restrict__ slots, uint64_t mask,
-                                                            int nblk, int32_t* __restrict__ nbr) {
+                                                            int nblk, int32_t* __restrict__ nbr,
+                                                            int64_t* __restrict__ tile_cnt) {
   const int K = ksize * ksize * ksize, c = (K - 1) / 2;
   int64_t rblk;
   int s;
@@ -229,6 +252,8 @@ __global__ __launch_bounds__(256) void mirror_lookup_kernel(const int32_t* __res
   const int nb = lookup(c_in, p, s, ksize, 1, g0, g1, g2, slots, mask);
   nbr[(int64_t)s * n + p] = nb;
   if (nb >= 0) nbr[(int64_t)(K - 1 - s) * n + nb] = (int32_t)p;
+  count_tiles(nb >= 0, (int64_t)s * n + p, tile_cnt);
+  count_tiles(nb >= 0, (int64_t)(K - 1 - s) * n + (nb >= 0 ? nb : 0), tile_cnt);
 }
 
 // One launch that prepares a build (thread i handles entry i of every region it reaches):
@@ -237,14 +262,21 @@ __global__ __launch_bounds__(256) void mirror_lookup_kernel(const int32_t* __res
 //                               (submanifold: rows c..K-1 of the neighbour map, c = centre;
 //                               generated sets: the whole map)
 //   flags[0] = 0, flags[1] = -1                               (when flags is given)
+//   tile_cnt[0, ntiles)      <- the entries [c0, c0 + n) (the centre row) in each compaction tile
+//                               (when tile_cnt is given; the lookups add the rest)
 __global__ void rb_init_kernel(uint64_t* __restrict__ slots, int64_t cap, int32_t* __restrict__ map, int64_t rows,
-                               int64_t n, int first_identity, int* __restrict__ flags) {
+                               int64_t n, int first_identity, int* __restrict__ flags,
+                               int64_t* __restrict__ tile_cnt = nullptr, int64_t ntiles = 0, int64_t c0 = 0) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < cap) slots[i] = kEmpty;
   if (i < rows * n) map[i] = (first_identity && i < n) ? (int32_t)i : -1;
   if (flags && i == 0) {
     flags[0] = 0;
     flags[1] = -1;
+  }
+  if (tile_cnt && i < ntiles) {
+    const int64_t lo = max(i * kCompactTile, c0), hi = min((i + 1) * kCompactTile, c0 + n);
+    tile_cnt[i] = hi > lo ? hi - lo : 0;
   }
 }
 
@@ -256,8 +288,8 @@ __global__ void rb_init_kernel(uint64_t* __restrict__ slots, int64_t cap, int32_
 // tile is its entry j * kCompactNT + t (coalesced loads, and the valid lanes of one wavefront
 // step write consecutive pairs).  Two launches: pair_count_kernel writes every tile's count,
 // pair_write_kernel adds the counts of the tiles before its own (at most a few thousand values,
-// read from L2) and writes its pairs.  No workgroup waits on another.
-constexpr int kCompactNT = 256, kCompactPer = 32, kCompactTile = kCompactNT * kCompactPer;
+// read from L2) and writes its pairs.  No workgroup waits on another.  A submanifold build has its
+// counts from the lookups already (mirror_lookup_kernel) and skips the counting launch.
 
 // Loads a tile's entries (-1 past the end) and the ballot of valid lanes per step.
 __device__ __forceinline__ void compact_load(const int32_t* __restrict__ nbr, int64_t f0, int64_t total, int tid,
@@ -345,16 +377,17 @@ __global__ __launch_bounds__(kCompactNT) void pair_write_kernel(const int32_t* _
   }
 }
 
-// The two launches of the compaction; tile_count holds compact_tiles(K, n) values.
+// The launches of the compaction; tile_count holds compact_tiles(K, n) values, already the counts
+// when counted.
 int compact_pairs(const int32_t* nbr, int64_t n, int K, int64_t* tile_count, int32_t* pairs, int64_t* pair_off,
-                  hipStream_t st);
+                  hipStream_t st, bool counted = false);
 
 int64_t compact_tiles(int64_t K, int64_t n) { return (K * n + kCompactTile - 1) / kCompactTile; }
 
 int compact_pairs(const int32_t* nbr, int64_t n, int K, int64_t* tile_count, int32_t* pairs, int64_t* pair_off,
-                  hipStream_t st) {
+                  hipStream_t st, bool counted) {
   const int64_t tiles = compact_tiles(K, n);
-  pair_count_kernel<<<(unsigned)tiles, kCompactNT, 0, st>>>(nbr, (int64_t)K * n, tile_count);
+  if (!counted) pair_count_kernel<<<(unsigned)tiles, kCompactNT, 0, st>>>(nbr, (int64_t)K * n, tile_count);
   pair_write_kernel<<<(unsigned)tiles, kCompactNT, 0, st>>>(nbr, n, K, tile_count, pairs, pair_off);
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;
@@ -586,27 +619,30 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
   }
 
   if (submanifold && n > 0) {
-    // Five launches and one read-back: (1) the table, the mirrored rows of the neighbour map, the
-    // look-back state and the flags are set by one kernel; (2) the inserts, which also copy the
-    // sites (the output set); (3) lookups of the offsets before the centre, mirrored entries
-    // written from them; (4) the single-pass compaction into the pair lists.
+    // Four launches and one read-back: (1) the table, the mirrored rows of the neighbour map, the
+    // compaction's tile counts (the centre row's share) and the flags are set by one kernel; (2) the
+    // inserts, which also copy the sites (the output set); (3) lookups of the offsets before the
+    // centre, mirrored entries written from them, every entry counted into its compaction tile;
+    // (4) the single-pass compaction into the pair lists.
     const int c = (K - 1) / 2;
-    const int64_t init_n = std::max<int64_t>(rb->cap_in, (int64_t)(K - c) * n);
+    const int64_t init_n0 = std::max<int64_t>(rb->cap_in, (int64_t)(K - c) * n);
     rb->n_out = n;
     rb->hash_out = rb->hash_in;
     rb->cap_out = rb->cap_in;
+    const int64_t init_n = std::max<int64_t>(init_n0, sub_tiles);
     rb_init_kernel<<<cdiv(init_n, 256), 256, 0, st>>>(rb->hash_in, rb->cap_in, rb->nbr + (int64_t)c * n, K - c, n, 1,
-                                                      dflags);
+                                                      dflags, tile_cnt, sub_tiles, (int64_t)c * n);
     hash_insert_kernel<<<cdiv(n, 256), 256, 0, st>>>(coords, n, grid[0], grid[1], grid[2], max_batch(rb->grid),
                                                      rb->hash_in, (uint64_t)(rb->cap_in - 1), dflags, rb->out_coords);
     const int nblk = (int)cdiv(n, 256);
     if (c > 0)
       mirror_lookup_kernel<<<(unsigned)((int64_t)nblk * c), 256, 0, st>>>(rb->out_coords, n, ksize, grid[0], grid[1],
                                                                           grid[2], rb->hash_in,
-                                                                          (uint64_t)(rb->cap_in - 1), nblk, rb->nbr);
+                                                                          (uint64_t)(rb->cap_in - 1), nblk, rb->nbr,
+                                                                          tile_cnt);
     SSC_HIP(hipGetLastError());
     if (rb->pairs) {
-      SSC_TRY(compact_pairs(rb->nbr, n, K, tile_cnt, rb->pairs, rb->pair_off_dev, st));
+      SSC_TRY(compact_pairs(rb->nbr, n, K, tile_cnt, rb->pairs, rb->pair_off_dev, st, true));
       return finish_build(rb, host, st, async);
     }
     // past 1 GB of pairs at the upper bound: counted, scanned and sized exactly below
