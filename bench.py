@@ -208,6 +208,9 @@ class SingleLayer:
         self.hash_cap = int(rb.hash_slots(0).shape[0])
         rb.close()
         self.ws = torch.empty((ws,), dtype=torch.uint8, device=dev)
+        K = self.L.ksize ** 3
+        self.W = torch.empty((K, self.L.cout, self.L.cin), dtype=self.dt, device=dev)
+        self.side = torch.cuda.Stream(device=dev)  # default priority, like every stream here
         self.events = None      # per-step [synth, rulebook, forward, backward] boundaries when set
 
     def forward_only(self):
@@ -226,16 +229,24 @@ class SingleLayer:
             ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
             self.events.append(ev)
             ev[0].record()
-        # synthesis does not depend on the rule book: launched first, it runs while the host
-        # prepares the rule-book launches instead of after the rule book's synchronisation
-        W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt)
-        if ev:
+        # synthesis does not depend on the rule book.  In the timed steps it runs on a second
+        # stream beside the build (both are short, latency-bound launches), joined before the
+        # forward; the side stream first waits for the main one, so the previous step's backward
+        # is done with W.  The phase pass (events set) runs the two in sequence on one stream.
+        main = torch.cuda.current_stream()
+        if ev is None:
+            self.side.wait_stream(main)
+            W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt, out=self.W, stream=self.side)
+        else:
+            W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt, out=self.W)
             ev[1].record()
         # asynchronous build: the forward is queued behind it without a host round trip (a bf16
         # forward needs only the neighbour map; the backward settles the build)
         rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, L.stride, L.submanifold, asynchronous=True)
         if ev:
             ev[2].record()
+        else:
+            main.wait_stream(self.side)
         out = P.forward(self.feats, rb, W)
         if ev:
             ev[3].record()

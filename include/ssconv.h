@@ -101,11 +101,16 @@ const char* ssconv_version(void);
 
 /* Device memory the library allocates (rule book buffers, the packed bf16 kernel
  * of ssconv_forward) comes from a per-process cache: a freed block is kept with
- * an event recorded on the freeing stream and reused, on the same stream at
- * once, on another stream after waiting for that event; up to 8 GB of free
- * blocks are kept.  ssconv_empty_cache waits for and releases every free
- * block (blocks in use are untouched); ssconv_cached_bytes returns the bytes
- * held in free blocks.  Both are safe to call at any time. */
+ * the stream that freed it and reused, on that stream at once (stream order),
+ * on another stream after that stream waits for an event recorded at reuse on
+ * the freeing stream; up to 8 GB of free blocks are kept, beyond that the
+ * oldest are freed stream-ordered on their freeing stream.  A stream that
+ * frees library memory (destroys a rule book, runs a call with temporaries)
+ * must therefore stay valid while the cache holds the block: until
+ * ssconv_empty_cache, or for the life of the process.  ssconv_empty_cache
+ * synchronises each free block's stream and releases every free block (blocks
+ * in use are untouched); ssconv_cached_bytes returns the bytes held in free
+ * blocks.  Both are safe to call at any time. */
 int ssconv_empty_cache(void);
 int64_t ssconv_cached_bytes(void);
 

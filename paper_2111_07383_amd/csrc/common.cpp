@@ -43,9 +43,9 @@ int fail(int code, const char* fmt, ...) {
   return code;
 }
 
-// Device memory cache.  A block the library frees is kept with an event recorded on the freeing
-// stream and handed out again: reuse on the same stream needs nothing (stream order), reuse on
-// another stream first makes that stream wait for the event.  A stream-ordered allocation costs
+// Device memory cache.  A block the library frees is kept with its freeing stream and handed out
+// again: reuse on the same stream needs nothing (stream order), reuse on another stream first
+// records an event on the freeing stream and makes the new stream wait for it.  A stream-ordered allocation costs
 // tens of microseconds of host time after a synchronisation and can block the host while the
 // device is busy; a cache hit costs a lock and a short search.  Blocks come in 64 KB steps; a
 // request takes the smallest free block of at least its size and at most twice it (+ 1 MB).
@@ -95,19 +95,25 @@ int dev_alloc(void** p, size_t bytes, hipStream_t stream) {
         best = i;
     }
     if (best < g_free_blocks.size()) {
-      Block b = g_free_blocks[best];
+      Block& b = g_free_blocks[best];
       if (b.stream != stream) {
-        hipError_t e = hipStreamWaitEvent(stream, b.ev, 0);
+        // ordered after the block's last use: an event recorded now on the freeing stream covers
+        // everything queued there so far, the free included (no system-scope fence: device-side
+        // ordering only)
+        hipError_t e = b.ev ? hipSuccess : hipEventCreateWithFlags(&b.ev, hipEventDisableTiming | hipEventDisableSystemFence);
+        if (e == hipSuccess) e = hipEventRecord(b.ev, b.stream);
+        if (e == hipSuccess) e = hipStreamWaitEvent(stream, b.ev, 0);
         if (e != hipSuccess) {
           (void)hipGetLastError();
-          return fail(SSCONV_E_HIP, "hipStreamWaitEvent: %s", hipGetErrorString(e));
+          return fail(SSCONV_E_HIP, "ordering a cached block after its freeing stream: %s", hipGetErrorString(e));
         }
       }
+      Block got = b;
       g_free_blocks.erase(g_free_blocks.begin() + (std::ptrdiff_t)best);
-      g_free_bytes -= b.bytes;
-      b.stream = stream;
-      g_live_blocks[b.p] = b;
-      *p = b.p;
+      g_free_bytes -= got.bytes;
+      got.stream = stream;
+      g_live_blocks[got.p] = got;
+      *p = got.p;
       return SSCONV_OK;
     }
   }
@@ -172,15 +178,11 @@ void dev_free(void* p, hipStream_t stream) {
   }
   Block b = it->second;
   g_live_blocks.erase(it);
+  // Kept with the freeing stream and nothing recorded: reuse on that stream is ordered by the
+  // stream itself, and reuse on another one records its event then (dev_alloc).  An event
+  // recorded here would sit between two kernels of the stream on every free, and each such
+  // record holds the next kernel's start back by microseconds.
   b.stream = stream;
-  // device-side ordering only (stream waits, and the wait before hipFree in ssconv_empty_cache):
-  // no system-scope fence, so a record does not write back and invalidate the caches
-  if (!b.ev && hipEventCreateWithFlags(&b.ev, hipEventDisableTiming | hipEventDisableSystemFence) != hipSuccess)
-    b.ev = nullptr;
-  if (!b.ev || hipEventRecord(b.ev, stream) != hipSuccess) {
-    release_block(b);
-    return;
-  }
   g_free_blocks.push_back(b);
   g_free_bytes += b.bytes;
   while (g_free_bytes > kCacheLimit && !g_free_blocks.empty()) {
@@ -264,11 +266,15 @@ extern "C" int ssconv_debug_set(int option, int64_t value) {
 extern "C" int ssconv_empty_cache(void) {
   using namespace ssconv;
   std::lock_guard<std::mutex> lk(g_cache_mu);
+  int cur = 0;
+  (void)hipGetDevice(&cur);
   for (Block& b : g_free_blocks) {
-    if (b.ev) (void)hipEventSynchronize(b.ev);
+    (void)hipSetDevice(b.dev);
+    (void)hipStreamSynchronize(b.stream);  // the block's last use is queued there
     (void)hipFree(b.p);
     if (b.ev) (void)hipEventDestroy(b.ev);
   }
+  (void)hipSetDevice(cur);
   (void)hipGetLastError();
   g_free_blocks.clear();
   g_free_bytes = 0;

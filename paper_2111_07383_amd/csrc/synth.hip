@@ -1,9 +1,10 @@
 // Kernel synthesis (Sec. 3.2.1, Eq. 7 with the block matrix of Eq. 9) and its adjoint.
 //
-// W[s][o][i] = sum_q w[off(field(o), field(i)) + q] * B^{k l}_q[s][a][b], one thread per
-// element of W so the dominant cost -- writing W -- is a coalesced stream.
-// The adjoint dw[off + q] = sum_{s,a,b} dW[s][o][i] B_q[s][a][b] uses one
-// workgroup per (out field, in field) pair with a fixed reduction order; dW comes
+// W[s][o][i] = sum_q w[off(field(o), field(i)) + q] * B^{k l}_q[s][a][b], one wavefront per
+// (out field, in field) block of W: the block's coefficients and table entries are the same for
+// every lane (scalar loads), its K(2k+1)(2l+1) elements spread over the lanes.
+// The adjoint dw[off + q] = sum_{s,a,b} dW[s][o][i] B_q[s][a][b] uses one wavefront (or one
+// workgroup) per (out field, in field) pair with a fixed reduction order; dW comes
 // field-pair-blocked (dw_block_pos), so a pair's values are one contiguous run.
 #include "synth.hpp"
 
@@ -35,6 +36,16 @@ int make_synth_args(const ssconv_basis_desc* d, SynthArgs* a) {
     off += (int64_t)a->out.mult[e] * a->rowsz[a->out.l[e]];
   }
   a->n_coeff = off;
+  for (int eo = 0; eo < a->out.n; ++eo) {
+    const int k = a->out.l[eo];
+    int64_t c0 = a->row0[eo];
+    for (int ei = 0; ei < a->in.n; ++ei) {
+      const int l = a->in.l[ei];
+      if (a->rowsz[k] > 0x7fffffffll) return fail(SSCONV_E_INVALID, "coefficient row too long");
+      a->ep[eo][ei] = EntryPair{c0, a->base[k][l], (int)a->rowsz[k], a->nq[k][l], k, l};
+      c0 += (int64_t)a->in.mult[ei] * a->nq[k][l];
+    }
+  }
   a->n_out_fields = a->out.f0[a->out.n];
   a->n_in_fields = a->in.f0[a->in.n];
   return SSCONV_OK;
@@ -42,58 +53,69 @@ int make_synth_args(const ssconv_basis_desc* d, SynthArgs* a) {
 
 namespace {
 
-struct ChanInfo {
-  int entry, field, comp, l;
-};
-
-__device__ __forceinline__ ChanInfo chan_info(const FieldTab& t, int c) {
+// Entry holding field f (f0 ascends, entries past n hold the field count): counted over every
+// table slot, so with f uniform across the wavefront the table is read by scalar loads.
+__device__ __forceinline__ int field_entry(const FieldTab& t, int f) {
   int e = 0;
-  while (e + 1 < t.n && c >= t.ch0[e + 1]) ++e;
-  const int d = 2 * t.l[e] + 1, r = c - t.ch0[e];
-  return ChanInfo{e, r / d, r % d, t.l[e]};
+#pragma unroll
+  for (int j = 1; j < SSCONV_MAX_ENTRIES; ++j) e += f >= t.f0[j];
+  return e;
 }
 
-// Offset of the first coefficient of the (out field (eo, fo), in field (ei, fi)) block.
-__device__ __forceinline__ int64_t coeff_off(const SynthArgs& a, int eo, int fo, int k, int ei, int fi) {
-  int64_t off = a.row0[eo] + (int64_t)fo * a.rowsz[k];
-  for (int e = 0; e < ei; ++e) off += (int64_t)a.in.mult[e] * a.nq[k][a.in.l[e]];
-  return off + (int64_t)fi * a.nq[k][a.in.l[ei]];
-}
-
-// Loads of the coefficients and basis values of one element are issued kQL at a time with no
-// dependence between them, so an element costs one memory round trip per kQL basis functions.
+// Basis values of kSU elements are loaded kQL functions at a time with no dependence between
+// them, so a lane's elements cost one memory round trip per kQL basis functions.
 constexpr int kQL = 8;
+constexpr int kSU = 4;
 
-// grid (ceil(cout * cin / 256), K): the workgroup row is one offset s, so the element index fits
-// in 32 bits and the (out, in) channel split is one 32-bit division.
+// One wavefront per (out field, in field) pair, four per workgroup.  Lane t takes the block's
+// elements e = t, t + 64, ... in (s, a, b) order (e = (s (2k+1) + a)(2l+1) + b, the basis layout)
+// and writes W[s][ro + a][cc + b]; the sum over q runs in q order for every element.
 template <typename T>
 __global__ __launch_bounds__(256) void synth_kernel(SynthArgs a, const float* __restrict__ basis,
                                                     const float* __restrict__ coeffs, T* __restrict__ W) {
-  const int plane = a.cout * a.cin;
-  const int idx = blockIdx.x * 256 + threadIdx.x;
-  if (idx >= plane) return;
-  const int s = blockIdx.y;
-  const int co = idx / a.cin, ci = idx - co * a.cin;
-  const ChanInfo o = chan_info(a.out, co), i = chan_info(a.in, ci);
-  const int k = o.l, l = i.l, dk = 2 * k + 1, dl = 2 * l + 1;
-  const int nq = a.nq[k][l];
-  const float* cp = coeffs + coeff_off(a, o.entry, o.field, k, i.entry, i.field);
-  const float* bp = basis + a.base[k][l] + ((int64_t)s * dk + o.comp) * dl + i.comp;
-  const int64_t qstride = (int64_t)a.K * dk * dl;
-  float acc = 0.f;
-  for (int q0 = 0; q0 < nq; q0 += kQL) {
-    float cv[kQL], bv[kQL];
+  const int lane = threadIdx.x & 63;
+  const int pair = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
+  if (pair >= a.n_in_fields * a.n_out_fields) return;  // uniform per wavefront
+  const int fi_all = pair % a.n_in_fields, fo_all = pair / a.n_in_fields;
+  const int eo = field_entry(a.out, fo_all), ei = field_entry(a.in, fi_all);
+  const EntryPair& ep = a.ep[eo][ei];
+  const int fo = fo_all - a.out.f0[eo], fi = fi_all - a.in.f0[ei];
+  const int k = ep.k, l = ep.l, dk = 2 * k + 1, dl = 2 * l + 1, dkl = dk * dl;
+  const int nq = ep.nq;
+  const int ro = a.out.ch0[eo] + fo * dk, cc = a.in.ch0[ei] + fi * dl;
+  const float* cp = coeffs + ep.coff0 + (int64_t)fo * ep.rowsz + (int64_t)fi * nq;
+  const float* bp = basis + ep.base;
+  const int n = a.K * dkl;
+  const int64_t qstride = n;
+  const int64_t plane = (int64_t)a.cout * a.cin;
+  for (int e0 = lane; e0 < n; e0 += 64 * kSU) {
+    float acc[kSU];
 #pragma unroll
-    for (int j = 0; j < kQL; ++j) {
-      const bool ok = q0 + j < nq;
-      cv[j] = ok ? cp[q0 + j] : 0.f;
-      bv[j] = ok ? bp[(q0 + j) * qstride] : 0.f;
+    for (int u = 0; u < kSU; ++u) acc[u] = 0.f;
+    for (int q0 = 0; q0 < nq; q0 += kQL) {
+      float cv[kQL], bv[kSU][kQL];
+#pragma unroll
+      for (int j = 0; j < kQL; ++j) cv[j] = q0 + j < nq ? cp[q0 + j] : 0.f;
+#pragma unroll
+      for (int u = 0; u < kSU; ++u) {
+        const int e = e0 + u * 64;
+#pragma unroll
+        for (int j = 0; j < kQL; ++j) bv[u][j] = (e < n && q0 + j < nq) ? bp[(q0 + j) * qstride + e] : 0.f;
+      }
+#pragma unroll
+      for (int u = 0; u < kSU; ++u)
+#pragma unroll
+        for (int j = 0; j < kQL; ++j)
+          if (q0 + j < nq) acc[u] = fmaf(cv[j], bv[u][j], acc[u]);
     }
 #pragma unroll
-    for (int j = 0; j < kQL; ++j)
-      if (q0 + j < nq) acc = fmaf(cv[j], bv[j], acc);
+    for (int u = 0; u < kSU; ++u) {
+      const int e = e0 + u * 64;
+      if (e >= n) break;
+      const int s = e / dkl, r = e - s * dkl, ca = r / dl, cb = r - ca * dl;
+      W[(int64_t)s * plane + (int64_t)(ro + ca) * a.cin + cc + cb] = DT<T>::from_f(acc[u]);
+    }
   }
-  W[(int64_t)s * plane + idx] = DT<T>::from_f(acc);
 }
 
 // One workgroup per (in field, out field) pair; its coefficients are done 16 at a time in
@@ -107,18 +129,17 @@ __global__ __launch_bounds__(256) void synth_adjoint_kernel(SynthArgs a, const f
   __shared__ float red[4][kQB];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int fi_all = blockIdx.x, fo_all = blockIdx.y;
-  int eo = 0, ei = 0;
-  while (eo + 1 < a.out.n && fo_all >= a.out.f0[eo + 1]) ++eo;
-  while (ei + 1 < a.in.n && fi_all >= a.in.f0[ei + 1]) ++ei;
+  const int eo = field_entry(a.out, fo_all), ei = field_entry(a.in, fi_all);
+  const EntryPair& ep = a.ep[eo][ei];
   const int fo = fo_all - a.out.f0[eo], fi = fi_all - a.in.f0[ei];
-  const int k = a.out.l[eo], l = a.in.l[ei], dk = 2 * k + 1, dl = 2 * l + 1;
-  const int nq = a.nq[k][l];
+  const int k = ep.k, l = ep.l, dk = 2 * k + 1, dl = 2 * l + 1;
+  const int nq = ep.nq;
   if (nq == 0) return;  // uniform per workgroup
   const int ro = a.out.ch0[eo] + fo * dk, cc = a.in.ch0[ei] + fi * dl;
-  const int64_t off = coeff_off(a, eo, fo, k, ei, fi);
+  const int64_t off = ep.coff0 + (int64_t)fo * ep.rowsz + (int64_t)fi * nq;
   const int n = a.K * dk * dl;
   const int64_t qstride = (int64_t)a.K * dk * dl;
-  const float* bp = basis + a.base[k][l];
+  const float* bp = basis + ep.base;
   const int64_t blk = (int64_t)a.K * ((int64_t)ro * a.cin + (int64_t)dk * cc);  // dW is field-pair-blocked
   for (int q0 = 0; q0 < nq; q0 += kQB) {
     float acc[kQB];
@@ -164,21 +185,20 @@ __global__ __launch_bounds__(256) void synth_adjoint_wave_kernel(SynthArgs a, co
                                                                  const float* __restrict__ dW,
                                                                  float* __restrict__ dcoef) {
   const int lane = threadIdx.x & 63;
-  const int pair = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int pair = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
   if (pair >= a.n_in_fields * a.n_out_fields) return;  // uniform per wavefront
   const int fi_all = pair % a.n_in_fields, fo_all = pair / a.n_in_fields;
-  int eo = 0, ei = 0;
-  while (eo + 1 < a.out.n && fo_all >= a.out.f0[eo + 1]) ++eo;
-  while (ei + 1 < a.in.n && fi_all >= a.in.f0[ei + 1]) ++ei;
+  const int eo = field_entry(a.out, fo_all), ei = field_entry(a.in, fi_all);
+  const EntryPair& ep = a.ep[eo][ei];
   const int fo = fo_all - a.out.f0[eo], fi = fi_all - a.in.f0[ei];
-  const int k = a.out.l[eo], l = a.in.l[ei], dk = 2 * k + 1, dl = 2 * l + 1;
-  const int nq = a.nq[k][l];
+  const int k = ep.k, l = ep.l, dk = 2 * k + 1, dl = 2 * l + 1;
+  const int nq = ep.nq;
   if (nq == 0) return;
   const int ro = a.out.ch0[eo] + fo * dk, cc = a.in.ch0[ei] + fi * dl;
-  const int64_t off = coeff_off(a, eo, fo, k, ei, fi);
+  const int64_t off = ep.coff0 + (int64_t)fo * ep.rowsz + (int64_t)fi * nq;
   const int n = a.K * dk * dl;
   const int64_t qstride = (int64_t)a.K * dk * dl;
-  const float* bp = basis + a.base[k][l];
+  const float* bp = basis + ep.base;
   const int64_t blk = (int64_t)a.K * ((int64_t)ro * a.cin + (int64_t)dk * cc);
   for (int q0 = 0; q0 < nq; q0 += kQB) {
     float acc[kQB];
@@ -219,7 +239,8 @@ int launch_synth(const SynthArgs& a, const float* basis, const float* coeffs, ss
   const int64_t plane = (int64_t)a.cout * a.cin;
   if (plane == 0 || a.K == 0) return SSCONV_OK;
   if (plane > 0x7fffffffll) return fail(SSCONV_E_INVALID, "Cout * Cin must be below 2^31");
-  const dim3 g((unsigned)cdiv(plane, 256), (unsigned)a.K);
+  const int64_t pairs = (int64_t)a.n_in_fields * a.n_out_fields;
+  const unsigned g = (unsigned)cdiv(pairs, 4);
   if (dt == SSCONV_F32)
     synth_kernel<float><<<g, 256, 0, st>>>(a, basis, coeffs, (float*)W);
   else
