@@ -182,6 +182,35 @@ def parse():
 # GPU side
 # ---------------------------------------------------------------------------
 
+class StreamOrder:
+    """Orders a stream after the work queued so far on another one, through a reused HIP event
+    created without timing and without the system-scope fence: device-side ordering needs
+    neither, and a fenced record writes back the caches between two kernels of the stream.
+    Calls the HIP runtime the library itself links (same process-wide instance as torch's)."""
+
+    def __init__(self):
+        import ctypes
+        self.ct = ctypes
+        self.hip = ctypes.CDLL("libamdhip64.so.7")
+        self.events = {}
+
+    def _check(self, rc, what):
+        if rc != 0:
+            raise RuntimeError(f"{what} failed with HIP error {rc}")
+
+    def wait(self, waiter, signaller):
+        ct, hip = self.ct, self.hip
+        key = (waiter.cuda_stream, signaller.cuda_stream)
+        ev = self.events.get(key)
+        if ev is None:
+            ev = ct.c_void_p()
+            self._check(hip.hipEventCreateWithFlags(ct.byref(ev), ct.c_uint(0x2 | 0x20000000)),
+                        "hipEventCreateWithFlags")  # hipEventDisableTiming | hipEventDisableSystemFence
+            self.events[key] = ev
+        self._check(hip.hipEventRecord(ev, ct.c_void_p(signaller.cuda_stream)), "hipEventRecord")
+        self._check(hip.hipStreamWaitEvent(ct.c_void_p(waiter.cuda_stream), ev, ct.c_uint(0)), "hipStreamWaitEvent")
+
+
 class SingleLayer:
     def __init__(self, i, dev):
         import torch
@@ -209,8 +238,10 @@ class SingleLayer:
         rb.close()
         self.ws = torch.empty((ws,), dtype=torch.uint8, device=dev)
         K = self.L.ksize ** 3
-        self.W = torch.empty((K, self.L.cout, self.L.cin), dtype=self.dt, device=dev)
+        self.Wb = [torch.empty((K, self.L.cout, self.L.cin), dtype=self.dt, device=dev) for _ in range(2)]
         self.side = torch.cuda.Stream(device=dev)  # default priority, like every stream here
+        self.pending = None     # (rule book, W) of the next step, queued on the side stream
+        self.order = StreamOrder()
         self.events = None      # per-step [synth, rulebook, forward, backward] boundaries when set
 
     def forward_only(self):
@@ -222,37 +253,68 @@ class SingleLayer:
             self._out = torch.empty((self.n_out, L.cout), dtype=self.dt, device=self.feats.device)
         P.forward(self.feats, self._rb, self._W, out=self._out)
 
+    def _prepare(self, W):
+        """Synthesis into W and the rule-book build of one step, queued on the side stream."""
+        P, L = self.P, self.L
+        P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt, out=W, stream=self.side)
+        rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, L.stride, L.submanifold, stream=self.side,
+                        asynchronous=True)
+        return rb, W
+
     def step(self):
-        P, L, torch = self.P, self.L, self.torch
-        ev = None
+        """One training step of the layer: synthesis, rule book, forward, backward.
+
+        Timed steps are software-pipelined over two streams: a step's synthesis and rule book
+        (short, latency-bound launches that need only the coefficients and the coordinates) are
+        queued on the side stream behind the previous step's forward, so they run beside that
+        step's backward (its kernel gradient), not beside a gather; the main stream waits for
+        them before its forward.  Every step still synthesises one kernel, builds one rule book
+        and runs one forward and one backward.  W alternates between two buffers (the side
+        stream's wait for a forward also orders it after the backward before, the last reader of
+        the buffer it writes); the side stream waits for each backward before the rule book's
+        blocks are freed on it."""
         if self.events is not None:
-            ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
-            self.events.append(ev)
-            ev[0].record()
-        # synthesis does not depend on the rule book.  In the timed steps it runs on a second
-        # stream beside the build (both are short, latency-bound launches), joined before the
-        # forward; the side stream first waits for the main one, so the previous step's backward
-        # is done with W.  The phase pass (events set) runs the two in sequence on one stream.
+            return self.step_in_sequence()
+        P, torch = self.P, self.torch
         main = torch.cuda.current_stream()
-        if ev is None:
-            self.side.wait_stream(main)
-            W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt, out=self.W, stream=self.side)
-        else:
-            W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt, out=self.W)
-            ev[1].record()
+        if self.pending is None:
+            self.order.wait(self.side, main)
+            self.pending = self._prepare(self.Wb[0])
+        rb, W = self.pending
+        self.order.wait(main, self.side)
+        out = P.forward(self.feats, rb, W)
+        self.order.wait(self.side, main)
+        self.pending = self._prepare(self.Wb[1] if W is self.Wb[0] else self.Wb[0])
+        P.backward(self.feats, self.grad, rb, W, self.desc, self.basis, n_coeff=self.n_coeff, workspace=self.ws)
+        self.order.wait(self.side, main)
+        rb.close()   # stream-ordered on the side stream (its build stream), after this backward
+        return out
+
+    def drain(self):
+        """Closes the rule book queued for a next step (after the device is idle)."""
+        if self.pending is not None:
+            self.torch.cuda.synchronize()
+            self.pending[0].close()
+            self.pending = None
+
+    def step_in_sequence(self):
+        """The same step with every phase in sequence on one stream, bracketed by events (the
+        per-phase report)."""
+        P, L, torch = self.P, self.L, self.torch
+        self.drain()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
+        self.events.append(ev)
+        ev[0].record()
+        W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt, out=self.Wb[0])
+        ev[1].record()
         # asynchronous build: the forward is queued behind it without a host round trip (a bf16
         # forward needs only the neighbour map; the backward settles the build)
         rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, L.stride, L.submanifold, asynchronous=True)
-        if ev:
-            ev[2].record()
-        else:
-            main.wait_stream(self.side)
+        ev[2].record()
         out = P.forward(self.feats, rb, W)
-        if ev:
-            ev[3].record()
+        ev[3].record()
         P.backward(self.feats, self.grad, rb, W, self.desc, self.basis, n_coeff=self.n_coeff, workspace=self.ws)
-        if ev:
-            ev[4].record()
+        ev[4].record()
         rb.close()
         return out
 
