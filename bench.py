@@ -238,9 +238,9 @@ class SingleLayer:
         rb.close()
         self.ws = torch.empty((ws,), dtype=torch.uint8, device=dev)
         K = self.L.ksize ** 3
-        self.Wb = [torch.empty((K, self.L.cout, self.L.cin), dtype=self.dt, device=dev) for _ in range(2)]
+        self.W = torch.empty((K, self.L.cout, self.L.cin), dtype=self.dt, device=dev)
         self.side = torch.cuda.Stream(device=dev)  # default priority, like every stream here
-        self.pending = None     # (rule book, W) of the next step, queued on the side stream
+        self.pending = None     # rule book of the next step, queued on the side stream
         self.order = StreamOrder()
         self.events = None      # per-step [synth, rulebook, forward, backward] boundaries when set
 
@@ -253,38 +253,36 @@ class SingleLayer:
             self._out = torch.empty((self.n_out, L.cout), dtype=self.dt, device=self.feats.device)
         P.forward(self.feats, self._rb, self._W, out=self._out)
 
-    def _prepare(self, W):
-        """Synthesis into W and the rule-book build of one step, queued on the side stream."""
-        P, L = self.P, self.L
-        P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt, out=W, stream=self.side)
-        rb = P.Rulebook(self.coords, self.spec.grid, L.ksize, L.stride, L.submanifold, stream=self.side,
-                        asynchronous=True)
-        return rb, W
+    def _build_next(self):
+        """The rule-book build of a next step, queued on the side stream."""
+        L = self.L
+        return self.P.Rulebook(self.coords, self.spec.grid, L.ksize, L.stride, L.submanifold, stream=self.side,
+                               asynchronous=True)
 
     def step(self):
         """One training step of the layer: synthesis, rule book, forward, backward.
 
-        Timed steps are software-pipelined over two streams: a step's synthesis and rule book
-        (short, latency-bound launches that need only the coefficients and the coordinates) are
-        queued on the side stream behind the previous step's forward, so they run beside that
-        step's backward (its kernel gradient), not beside a gather; the main stream waits for
-        them before its forward.  Every step still synthesises one kernel, builds one rule book
-        and runs one forward and one backward.  W alternates between two buffers (the side
-        stream's wait for a forward also orders it after the backward before, the last reader of
-        the buffer it writes); the side stream waits for each backward before the rule book's
-        blocks are freed on it."""
+        Timed steps prefetch the rule book: it needs only the coordinates (the next batch's are
+        known to a training loop), so each step's build is queued on the side stream behind the
+        previous step's forward and runs beside that step's backward (its kernel gradient, not a
+        gather); the main stream waits for it before its forward.  The synthesis stays at the
+        head of the step on the main stream, after the previous backward in stream order: it
+        needs the coefficients as updated from that backward's gradient.  Every step still
+        synthesises one kernel, builds one rule book and runs one forward and one backward.  The
+        side stream waits for each backward before the rule book's blocks are freed on it."""
         if self.events is not None:
             return self.step_in_sequence()
         P, torch = self.P, self.torch
         main = torch.cuda.current_stream()
         if self.pending is None:
             self.order.wait(self.side, main)
-            self.pending = self._prepare(self.Wb[0])
-        rb, W = self.pending
+            self.pending = self._build_next()
+        rb = self.pending
+        W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt, out=self.W)
         self.order.wait(main, self.side)
         out = P.forward(self.feats, rb, W)
         self.order.wait(self.side, main)
-        self.pending = self._prepare(self.Wb[1] if W is self.Wb[0] else self.Wb[0])
+        self.pending = self._build_next()
         P.backward(self.feats, self.grad, rb, W, self.desc, self.basis, n_coeff=self.n_coeff, workspace=self.ws)
         self.order.wait(self.side, main)
         rb.close()   # stream-ordered on the side stream (its build stream), after this backward
@@ -294,7 +292,7 @@ class SingleLayer:
         """Closes the rule book queued for a next step (after the device is idle)."""
         if self.pending is not None:
             self.torch.cuda.synchronize()
-            self.pending[0].close()
+            self.pending.close()
             self.pending = None
 
     def step_in_sequence(self):
@@ -305,7 +303,7 @@ class SingleLayer:
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(5)]
         self.events.append(ev)
         ev[0].record()
-        W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt, out=self.Wb[0])
+        W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt, out=self.W)
         ev[1].record()
         # asynchronous build: the forward is queued behind it without a host round trip (a bf16
         # forward needs only the neighbour map; the backward settles the build)

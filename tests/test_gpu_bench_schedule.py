@@ -1,8 +1,7 @@
-"""The benchmark's timed single-layer step runs software-pipelined over two streams (the next
-step's synthesis and rule book queued on a side stream behind the current forward, W in two
-alternating buffers).  Its results must be bit-identical to the same step with every phase in
-sequence on one stream: forward output, input-feature gradient and coefficient gradient of
-every pipelined step."""
+"""The benchmark's timed single-layer step prefetches the rule book over two streams (the next
+step's build queued on a side stream behind the current forward, ordered by fence-free events).
+Its results must be bit-identical to the same step with every phase in sequence on one stream:
+forward output, input-feature gradient and coefficient gradient of every pipelined step."""
 import pytest
 
 pytestmark = pytest.mark.gpu
