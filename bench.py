@@ -241,6 +241,7 @@ class SingleLayer:
         self.W = torch.empty((K, self.L.cout, self.L.cin), dtype=self.dt, device=dev)
         self.side = torch.cuda.Stream(device=dev)  # default priority, like every stream here
         self.pending = None     # rule book of the next step, queued on the side stream
+        self.done = None        # rule book of the previous step, closed once its backward is ordered
         self.order = StreamOrder()
         self.events = None      # per-step [synth, rulebook, forward, backward] boundaries when set
 
@@ -268,8 +269,10 @@ class SingleLayer:
         gather); the main stream waits for it before its forward.  The synthesis stays at the
         head of the step on the main stream, after the previous backward in stream order: it
         needs the coefficients as updated from that backward's gradient.  Every step still
-        synthesises one kernel, builds one rule book and runs one forward and one backward.  The
-        side stream waits for each backward before the rule book's blocks are freed on it."""
+        synthesises one kernel, builds one rule book and runs one forward and one backward.  A
+        step's rule book is closed (its blocks freed, stream-ordered on the side stream) in the
+        next step, after the side stream's wait for that step's forward, which follows the
+        backward that last read it."""
         if self.events is not None:
             return self.step_in_sequence()
         P, torch = self.P, self.torch
@@ -282,18 +285,21 @@ class SingleLayer:
         self.order.wait(main, self.side)
         out = P.forward(self.feats, rb, W)
         self.order.wait(self.side, main)
+        if self.done is not None:
+            self.done.close()
         self.pending = self._build_next()
         P.backward(self.feats, self.grad, rb, W, self.desc, self.basis, n_coeff=self.n_coeff, workspace=self.ws)
-        self.order.wait(self.side, main)
-        rb.close()   # stream-ordered on the side stream (its build stream), after this backward
+        self.done = rb
         return out
 
     def drain(self):
-        """Closes the rule book queued for a next step (after the device is idle)."""
-        if self.pending is not None:
+        """Closes the rule books still held by the pipelined steps (after the device is idle)."""
+        if self.pending is not None or self.done is not None:
             self.torch.cuda.synchronize()
-            self.pending.close()
-            self.pending = None
+        for rb in (self.pending, self.done):
+            if rb is not None:
+                rb.close()
+        self.pending = self.done = None
 
     def step_in_sequence(self):
         """The same step with every phase in sequence on one stream, bracketed by events (the
