@@ -281,8 +281,8 @@ class SingleLayer:
             self.order.wait(self.side, main)
             self.pending = self._build_next()
         rb = self.pending
+        self.order.wait(main, self.side)   # next to the step boundary's records, not between kernels
         W = P.synth_kernel(self.desc, self.basis, self.coeffs, self.dt, out=self.W)
-        self.order.wait(main, self.side)
         out = P.forward(self.feats, rb, W)
         self.order.wait(self.side, main)
         if self.done is not None:
