@@ -950,9 +950,14 @@ def write_stats_summary(args):
     if g:
         durs = [(e - b) / 1e3 for b, e in g]
         n_timed = bench["roofline"]["launches_timed"] if bench else 0
-        timed = durs[len(durs) - n_timed:] if n_timed else durs
+        # the timed steps follow the warmup ones (setup launches no gather-GEMM); the phase pass,
+        # if any, comes after them
+        per_step = n_timed // steps if n_timed else 0
+        first = per_step * warmup
+        timed = durs[first:first + n_timed] if n_timed and first + n_timed <= len(durs) else durs
         out += ["", f"{kname} dispatches in launch order (us): " + " ".join(f"{x:.0f}" for x in durs),
-                f"{kname} average over the {len(timed)} timed dispatches (trace): {np.mean(timed):.1f} us"]
+                f"{kname} average over the {len(timed)} timed dispatches (trace; launches {first + 1}-"
+                f"{first + len(timed)}): {np.mean(timed):.1f} us"]
         if bench:
             r = bench["roofline"]
             out.append(f"{kname} average launch time measured by the benchmark's HIP events in the same run: "

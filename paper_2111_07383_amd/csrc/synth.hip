@@ -6,6 +6,8 @@
 // The adjoint dw[off + q] = sum_{s,a,b} dW[s][o][i] B_q[s][a][b] uses one wavefront (or one
 // workgroup) per (out field, in field) pair with a fixed reduction order; dW comes
 // field-pair-blocked (dw_block_pos), so a pair's values are one contiguous run.
+#include <algorithm>
+
 #include "synth.hpp"
 
 namespace ssconv {
@@ -67,14 +69,18 @@ __device__ __forceinline__ int field_entry(const FieldTab& t, int f) {
 constexpr int kQL = 8;
 constexpr int kSU = 4;
 
-// One wavefront per (out field, in field) pair, four per workgroup.  Lane t takes the block's
-// elements e = t, t + 64, ... in (s, a, b) order (e = (s (2k+1) + a)(2l+1) + b, the basis layout)
-// and writes W[s][ro + a][cc + b]; the sum over q runs in q order for every element.
+// nch wavefronts per (out field, in field) pair, four per workgroup: wavefront c of a pair takes
+// the block's elements [c span, (c + 1) span) in (s, a, b) order (e = (s (2k+1) + a)(2l+1) + b,
+// the basis layout; span a multiple of 64 kSU, nch span covering the layer's largest block), lane
+// t the elements t, t + 64, ... of that chunk, kSU per pass, and writes W[s][ro + a][cc + b]; the
+// sum over q runs in q order for every element.
 template <typename T>
 __global__ __launch_bounds__(256) void synth_kernel(SynthArgs a, const float* __restrict__ basis,
-                                                    const float* __restrict__ coeffs, T* __restrict__ W) {
+                                                    const float* __restrict__ coeffs, T* __restrict__ W, int nch,
+                                                    int span) {
   const int lane = threadIdx.x & 63;
-  const int pair = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
+  const int wid = __builtin_amdgcn_readfirstlane(blockIdx.x * 4 + (threadIdx.x >> 6));
+  const int pair = wid / nch, chunk = wid - pair * nch;
   if (pair >= a.n_in_fields * a.n_out_fields) return;  // uniform per wavefront
   const int fi_all = pair % a.n_in_fields, fo_all = pair / a.n_in_fields;
   const int eo = field_entry(a.out, fo_all), ei = field_entry(a.in, fi_all);
@@ -88,7 +94,8 @@ __global__ __launch_bounds__(256) void synth_kernel(SynthArgs a, const float* __
   const int n = a.K * dkl;
   const int64_t qstride = n;
   const int64_t plane = (int64_t)a.cout * a.cin;
-  for (int e0 = lane; e0 < n; e0 += 64 * kSU) {
+  const int e_end = min(n, (chunk + 1) * span);
+  for (int e0 = chunk * span + lane; e0 < e_end; e0 += 64 * kSU) {
     float acc[kSU];
 #pragma unroll
     for (int u = 0; u < kSU; ++u) acc[u] = 0.f;
@@ -240,11 +247,23 @@ int launch_synth(const SynthArgs& a, const float* basis, const float* coeffs, ss
   if (plane == 0 || a.K == 0) return SSCONV_OK;
   if (plane > 0x7fffffffll) return fail(SSCONV_E_INVALID, "Cout * Cin must be below 2^31");
   const int64_t pairs = (int64_t)a.n_in_fields * a.n_out_fields;
-  const unsigned g = (unsigned)cdiv(pairs, 4);
+  int kmax = 0, lmax = 0;
+  for (int e = 0; e < a.out.n; ++e) kmax = std::max(kmax, a.out.l[e]);
+  for (int e = 0; e < a.in.n; ++e) lmax = std::max(lmax, a.in.l[e]);
+  // chunks per pair: enough for one pass per wavefront over the largest block, but no more than
+  // one round of the chip's wavefront slots holds (256 CUs x 4 SIMDs x 8): past that, extra
+  // wavefronts only repeat the per-pair setup (6400 pairs of up to 675 elements: one chunk,
+  // 16 us against 17.5 with three; 1600 pairs of up to 3125 elements: five chunks of three
+  // passes, 16-18 us, against 36 us for one chunk of thirteen)
+  const int64_t one_pass = cdiv((int64_t)a.K * (2 * kmax + 1) * (2 * lmax + 1), 64 * kSU);
+  const int nch = (int)std::max<int64_t>(1, std::min<int64_t>(one_pass, 8192 / std::max<int64_t>(pairs, 1)));
+  const int span = (int)(cdiv(one_pass, nch) * 64 * kSU);  // elements per chunk, whole passes
+  if (pairs * nch > 0x7fffffffll) return fail(SSCONV_E_INVALID, "too many field pairs for the synthesis launch");
+  const unsigned g = (unsigned)cdiv(pairs * nch, 4);
   if (dt == SSCONV_F32)
-    synth_kernel<float><<<g, 256, 0, st>>>(a, basis, coeffs, (float*)W);
+    synth_kernel<float><<<g, 256, 0, st>>>(a, basis, coeffs, (float*)W, nch, span);
   else
-    synth_kernel<uint16_t><<<g, 256, 0, st>>>(a, basis, coeffs, (uint16_t*)W);
+    synth_kernel<uint16_t><<<g, 256, 0, st>>>(a, basis, coeffs, (uint16_t*)W, nch, span);
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;
 }
