@@ -169,11 +169,12 @@ __global__ __launch_bounds__(256) void synth_adjoint_kernel(SynthArgs a, const f
     }
 #pragma unroll
     for (int j = 0; j < kQB; ++j) {
-      if (q0 + j >= nq) break;  // uniform per workgroup: no butterflies for absent coefficients
-      float v = acc[j];
+      if (q0 + j < nq) {  // uniform per workgroup: no butterflies for absent coefficients
+        float v = acc[j];
 #pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
-      if (lane == 0) red[w][j] = v;
+        for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+        if (lane == 0) red[w][j] = v;
+      }
     }
     __syncthreads();
     if (threadIdx.x < kQB && q0 + (int)threadIdx.x < nq) {
@@ -229,11 +230,12 @@ __global__ __launch_bounds__(256) void synth_adjoint_wave_kernel(SynthArgs a, co
     float mine = 0.f;  // lane j keeps coefficient j's sum
 #pragma unroll
     for (int j = 0; j < kQB; ++j) {
-      if (q0 + j >= nq) break;  // uniform per wavefront: no butterflies for absent coefficients
-      float v = acc[j];
+      if (q0 + j < nq) {  // uniform per wavefront: no butterflies for absent coefficients
+        float v = acc[j];
 #pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
-      if (lane == j) mine = v;
+        for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m);
+        if (lane == j) mine = v;
+      }
     }
     if (lane < kQB && q0 + lane < nq) dcoef[off + q0 + lane] = mine;
   }
