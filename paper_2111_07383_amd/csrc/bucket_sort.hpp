@@ -2,8 +2,13 @@
 // interpolation adjoints).  The order of a bucket on exit is independent of the order it was
 // filled in, which makes the sums over buckets deterministic.
 //
-// Buckets of up to 64 entries: one wavefront each, a 64-lane bitonic network on cross-lane
-// shuffles (padding sorts last).  Larger buckets are appended to a list on the device and sorted
+// Buckets of up to 64 entries are sorted by bitonic networks on cross-lane shuffles (padding
+// sorts last).  For lists of mostly tiny buckets (voxelisation: a few points per site) a
+// wavefront takes eight consecutive buckets, those of up to 8 entries on eight lanes each and
+// those of 9 to 64 entries then one at a time on the whole wavefront (a wavefront per bucket left
+// most lanes sorting padding there: 59 -> 14 us for 158k sites); otherwise (interpolation
+// adjoint: ~32 entries per site) a wavefront takes one bucket, the 64-lane network.
+// Larger buckets are appended to a list on the device and sorted
 // by a second kernel, one workgroup per bucket: the bitonic network in its all-ascending form
 // (each merge starts by comparing i with its mirror i ^ (k - 1) in the block of k, then halves
 // with i ^ j; every comparator puts the smaller value at the lower index).  In that form entries
@@ -20,34 +25,57 @@ namespace {  // one copy per translation unit that includes this header
 constexpr int kBigLds = 8192;  // largest bucket sorted in LDS (32 KB)
 
 // Bucket r = a[start[r] .. start[r] + cnt[r]) for r < *n_rows (n_rows read on the device, or
-// n_rows_host when n_rows is null); four buckets per 256-thread workgroup.  A bucket of more than
-// 64 entries is appended to big[1 ..] (big[0] counts them; zero at launch).
+// n_rows_host when n_rows is null); BPW buckets per wavefront (1 or 8), 4 BPW per 256-thread
+// workgroup.  A bucket of more than 64 entries is appended to big[1 ..] (big[0] counts them; zero
+// at launch).
+template <int BPW>
 __global__ __launch_bounds__(256) void bucket_sort_kernel(const int64_t* __restrict__ n_rows, int64_t n_rows_host,
                                                           const int64_t* __restrict__ start,
                                                           const int32_t* __restrict__ cnt, int32_t* __restrict__ a,
                                                           int32_t* __restrict__ big) {
-  const int lane = threadIdx.x & 63;
-  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  constexpr int GW = 64 / BPW;  // lanes per bucket in the first pass
+  const int lane = threadIdx.x & 63, grp = lane / GW, sub = lane % GW;
   const int64_t nr = n_rows ? *n_rows : n_rows_host;
-  if (r >= nr) return;  // uniform per wavefront: no cross-wavefront barrier below
-  int32_t* b = a + start[r];
-  const int m = cnt[r];
-  if (m <= 1) return;
-  if (m > 64) {
-    if (lane == 0) big[1 + atomicAdd(big, 1)] = (int32_t)r;
-    return;
-  }
-  int32_t v = lane < m ? b[lane] : 0x7fffffff;
+  const int64_t r0 = ((int64_t)blockIdx.x * 4 + (threadIdx.x >> 6)) * BPW;
+  if (r0 >= nr) return;  // uniform per wavefront: no cross-wavefront barrier below
+  const int64_t r = r0 + grp;
+  const int m = r < nr ? cnt[r] : 0;
+  const bool small = m > 1 && m <= GW;
+  int32_t* b = small ? a + start[r] : nullptr;
+  {
+    int32_t v = small && sub < m ? b[sub] : 0x7fffffff;
 #pragma unroll
-  for (int k = 2; k <= 64; k <<= 1) {
+    for (int k = 2; k <= GW; k <<= 1) {
 #pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const int32_t p = __shfl_xor(v, j, 64);
-      const bool asc = (lane & k) == 0, lower = (lane & j) == 0;
-      v = (lower == asc) ? min(v, p) : max(v, p);
+      for (int j = k >> 1; j > 0; j >>= 1) {
+        const int32_t p = __shfl_xor(v, j, 64);  // j < GW: the partner is in the same group
+        const bool asc = (sub & k) == 0, lower = (sub & j) == 0;
+        v = (lower == asc) ? min(v, p) : max(v, p);
+      }
     }
+    if (small && sub < m) b[sub] = v;
   }
-  if (lane < m) b[lane] = v;
+  if (sub == 0 && m > 64) big[1 + atomicAdd(big, 1)] = (int32_t)r;
+  if constexpr (BPW == 1) return;
+  uint64_t mid = __ballot(sub == 0 && m > GW && m <= 64);
+  while (mid) {  // uniform: the ballot is the same in every lane
+    const int g = (__ffsll((unsigned long long)mid) - 1) / GW;
+    mid &= mid - 1;
+    const int64_t rr = r0 + g;
+    const int mm = cnt[rr];
+    int32_t* bb = a + start[rr];
+    int32_t v = lane < mm ? bb[lane] : 0x7fffffff;
+#pragma unroll
+    for (int k = 2; k <= 64; k <<= 1) {
+#pragma unroll
+      for (int j = k >> 1; j > 0; j >>= 1) {
+        const int32_t p = __shfl_xor(v, j, 64);
+        const bool asc = (lane & k) == 0, lower = (lane & j) == 0;
+        v = (lower == asc) ? min(v, p) : max(v, p);
+      }
+    }
+    if (lane < mm) bb[lane] = v;
+  }
 }
 
 // Comparator t (0 <= t < p2 / 2) of the stage (k, j) of the all-ascending network over p2
@@ -108,12 +136,16 @@ __global__ __launch_bounds__(256) void bucket_sort_big_kernel(const int32_t* __r
   }
 }
 
-// Sorts every bucket: big must hold n_max + 1 int32 (n_max = the largest number of buckets).
+// Sorts every bucket: big must hold n_max + 1 int32 (n_max = the largest number of buckets);
+// tiny: most buckets hold at most 8 entries (eight buckets per wavefront).
 inline int sort_buckets(const int64_t* n_rows, int64_t n_rows_host, int64_t n_max, const int64_t* start,
-                        const int32_t* cnt, int32_t* a, int32_t* big, hipStream_t st) {
+                        const int32_t* cnt, int32_t* a, int32_t* big, bool tiny, hipStream_t st) {
   if (n_max <= 0) return SSCONV_OK;
   SSC_HIP(hipMemsetAsync(big, 0, 4, st));
-  bucket_sort_kernel<<<cdiv(n_max, 4), 256, 0, st>>>(n_rows, n_rows_host, start, cnt, a, big);
+  if (tiny)
+    bucket_sort_kernel<8><<<cdiv(n_max, 32), 256, 0, st>>>(n_rows, n_rows_host, start, cnt, a, big);
+  else
+    bucket_sort_kernel<1><<<cdiv(n_max, 4), 256, 0, st>>>(n_rows, n_rows_host, start, cnt, a, big);
   bucket_sort_big_kernel<<<256, 256, 0, st>>>(big, start, cnt, a);
   SSC_HIP(hipGetLastError());
   return SSCONV_OK;

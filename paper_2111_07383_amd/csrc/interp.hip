@@ -225,7 +225,7 @@ extern "C" int ssconv_interpolate_backward(ssconv_rulebook_t rb, const float* gr
     interp_count_kernel<<<cdiv(ne, 256), 256, 0, stream>>>(rows, ne, cnt);
     SSC_TRY(exclusive_scan(cnt, n, start, tmp + scan_tmp_elems(n), tmp, stream));
     interp_fill_kernel<<<cdiv(ne, 256), 256, 0, stream>>>(rows, ne, start, fillc, ent);
-    SSC_TRY(sort_buckets(nullptr, n, n, start, cnt, ent, big, stream));
+    SSC_TRY(sort_buckets(nullptr, n, n, start, cnt, ent, big, false, stream));
     if (channels % 4 == 0 && aligned16(grad) && aligned16(grad_feats))
       interp_bwd_kernel<4><<<cdiv(n * channels / 4, 256), 256, 0, stream>>>(grad, channels, wts, start, cnt, ent, n,
                                                                             grad_feats);

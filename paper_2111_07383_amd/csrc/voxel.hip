@@ -169,7 +169,7 @@ extern "C" int ssconv_voxelize(const float* points, const int32_t* batch, const 
       // rows past the site count have zero counts, so the scan over n rows is exact
       SSC_TRY(exclusive_scan(cnt, n, start, d_pts, stmp, st));
       vox_fill_kernel<<<cdiv(n, 256), 256, 0, st>>>(prow, n, start, fillc, idx);
-      SSC_TRY(sort_buckets(d_sites, 0, n, start, cnt, idx, big, st));
+      SSC_TRY(sort_buckets(d_sites, 0, n, start, cnt, idx, big, true, st));
       vox_mean_kernel<<<cdiv(n * channels, 256), 256, 0, st>>>(feats, channels, d_sites, start, cnt, idx, feats_out);
     }
     SSC_HIP(hipGetLastError());
