@@ -6,9 +6,10 @@
 // round-to-nearest; points whose cell is outside the grid (or not finite) are dropped.  The active
 // cells are marked in a bitmap over (batch, grid), whose popcount scan gives every cell its row
 // in lexicographic (b, x, y, z) order.  Averages are deterministic without floating-point
-// atomics: per-row point counts (integer atomics), a scan to bucket offsets, a bucket fill whose
-// order inside a bucket is arbitrary, a pass that sorts every bucket by point index, and a pass
-// that adds each site's points in that order and divides by the count.
+// atomics: per-row point counts (integer atomics, whose returned values give each point a slot in
+// its row's bucket), a scan to bucket offsets, a bucket fill (a plain scatter; the order inside a
+// bucket is arbitrary), a pass that sorts every bucket by point index, and a pass that adds each
+// site's points in that order and divides by the count.
 #include <algorithm>
 #include <cmath>
 
@@ -46,10 +47,11 @@ __global__ void vox_cell_kernel(const float* __restrict__ pts, const int32_t* __
   if (any_bad && (threadIdx.x & 63) == __ffsll((unsigned long long)any_bad) - 1) atomicOr(flags, kFlagBadBatch);
 }
 
-// Row of every point (rank of its cell's bit) and the per-row point counts.
+// Row of every point (rank of its cell's bit), the per-row point counts and each point's slot in
+// its row's bucket (the count before its own increment).
 __global__ void vox_row_kernel(const uint32_t* __restrict__ key, int64_t n, const uint32_t* __restrict__ bits,
                                const int64_t* __restrict__ woff, int32_t* __restrict__ point_row,
-                               int32_t* __restrict__ cnt) {
+                               int32_t* __restrict__ cnt, int32_t* __restrict__ slot) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const uint32_t k = key[i];
@@ -57,35 +59,38 @@ __global__ void vox_row_kernel(const uint32_t* __restrict__ key, int64_t n, cons
   if (k != kDropped) {
     const uint32_t w = k >> 5, b = k & 31u;
     r = (int32_t)(woff[w] + __popc(bits[w] & ((1u << b) - 1u)));
-    atomicAdd(&cnt[r], 1);
+    slot[i] = atomicAdd(&cnt[r], 1);
   }
   point_row[i] = r;
 }
 
-// One thread per bitmap bit: a set bit writes its site's coordinates at its rank.
-__global__ void vox_emit_kernel(const uint32_t* __restrict__ bits, int64_t nbits, const int64_t* __restrict__ woff,
+// One thread per bitmap word: its set bits, in ascending order, write their sites' coordinates at
+// consecutive ranks from the word's offset (only bits of cells inside the grid are ever set).
+__global__ void vox_emit_kernel(const uint32_t* __restrict__ bits, int64_t nw, const int64_t* __restrict__ woff,
                                 int g0, int g1, int g2, int32_t* __restrict__ coords) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= nbits) return;
-  const uint32_t k = (uint32_t)i, b = k & 31u;
-  const uint32_t m = bits[k >> 5];
-  if (!((m >> b) & 1u)) return;
-  const int64_t r = woff[k >> 5] + __popc(m & ((1u << b) - 1u));
+  const int64_t wd = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (wd >= nw) return;
+  uint32_t m = bits[wd];
+  int64_t r = woff[wd];
   const uint32_t g12 = (uint32_t)g1 * (uint32_t)g2, per_b = (uint32_t)g0 * g12;
-  const uint32_t bb = k / per_b, rem = k - bb * per_b;
-  const uint32_t x = rem / g12, yz = rem - x * g12;
-  const uint32_t y = yz / (uint32_t)g2, z = yz - y * (uint32_t)g2;
-  reinterpret_cast<int4*>(coords)[r] = make_int4((int)bb, (int)x, (int)y, (int)z);
+  while (m) {
+    const uint32_t k = (uint32_t)(wd * 32) + (uint32_t)(__ffs(m) - 1);
+    m &= m - 1u;
+    const uint32_t bb = k / per_b, rem = k - bb * per_b;
+    const uint32_t x = rem / g12, yz = rem - x * g12;
+    const uint32_t y = yz / (uint32_t)g2, z = yz - y * (uint32_t)g2;
+    reinterpret_cast<int4*>(coords)[r++] = make_int4((int)bb, (int)x, (int)y, (int)z);
+  }
 }
 
-// Bucket fill: point i goes to an unspecified slot of its row's bucket [start[r], start[r]+cnt[r]).
+// Bucket fill: point i goes to slot slot[i] of its row's bucket [start[r], start[r]+cnt[r]).
 __global__ void vox_fill_kernel(const int32_t* __restrict__ point_row, int64_t n, const int64_t* __restrict__ start,
-                                int32_t* __restrict__ fill, int32_t* __restrict__ idx) {
+                                const int32_t* __restrict__ slot, int32_t* __restrict__ idx) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const int32_t r = point_row[i];
   if (r < 0) return;
-  idx[start[r] + atomicAdd(&fill[r], 1)] = (int32_t)i;
+  idx[start[r] + slot[i]] = (int32_t)i;
 }
 
 
@@ -148,7 +153,7 @@ extern "C" int ssconv_voxelize(const float* points, const int32_t* batch, const 
   uint32_t* key = (uint32_t*)(ws + o_key);
   int32_t* prow = point_row ? point_row : (int32_t*)(ws + o_row);
   int32_t* cnt = (int32_t*)(ws + o_cnt);
-  int32_t* fillc = (int32_t*)(ws + o_fill);
+  int32_t* slot = (int32_t*)(ws + o_fill);  // each point's slot in its row's bucket
   int64_t* start = (int64_t*)(ws + o_start);
   int32_t* idx = (int32_t*)(ws + o_idx);
   int* flags = (int*)(ws + o_flags);
@@ -158,17 +163,16 @@ extern "C" int ssconv_voxelize(const float* points, const int32_t* batch, const 
   auto run = [&]() -> int {
     SSC_HIP(hipMemsetAsync(bits, 0, (size_t)nw * 4, st));
     SSC_HIP(hipMemsetAsync(cnt, 0, (size_t)n * 4, st));
-    SSC_HIP(hipMemsetAsync(fillc, 0, (size_t)n * 4, st));
     SSC_HIP(hipMemsetAsync(flags, 0, 4, st));
     vox_cell_kernel<<<cdiv(n, 256), 256, 0, st>>>(points, batch, n, origin[0], origin[1], origin[2], voxel, grid[0],
                                                   grid[1], grid[2], nbatch, key, bits, flags);
     SSC_TRY(exclusive_scan_popc(bits, nw, woff, d_sites, stmp, st));
-    vox_row_kernel<<<cdiv(n, 256), 256, 0, st>>>(key, n, bits, woff, prow, cnt);
-    vox_emit_kernel<<<cdiv(nbits, 256), 256, 0, st>>>(bits, nbits, woff, grid[0], grid[1], grid[2], coords_out);
+    vox_row_kernel<<<cdiv(n, 256), 256, 0, st>>>(key, n, bits, woff, prow, cnt, slot);
+    vox_emit_kernel<<<cdiv(nw, 256), 256, 0, st>>>(bits, nw, woff, grid[0], grid[1], grid[2], coords_out);
     if (channels > 0) {
       // rows past the site count have zero counts, so the scan over n rows is exact
       SSC_TRY(exclusive_scan(cnt, n, start, d_pts, stmp, st));
-      vox_fill_kernel<<<cdiv(n, 256), 256, 0, st>>>(prow, n, start, fillc, idx);
+      vox_fill_kernel<<<cdiv(n, 256), 256, 0, st>>>(prow, n, start, slot, idx);
       SSC_TRY(sort_buckets(d_sites, 0, n, start, cnt, idx, big, true, st));
       vox_mean_kernel<<<cdiv(n * channels, 256), 256, 0, st>>>(feats, channels, d_sites, start, cnt, idx, feats_out);
     }
