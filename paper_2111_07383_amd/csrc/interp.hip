@@ -8,8 +8,9 @@
 // has weight prod_a (c_a ? w_a : 1 - w_a).  Corners are found in the rule book's coordinate hash;
 // corners outside the grid or inactive contribute nothing, and points never read sites of
 // another batch entry.  The backward pass is the exact adjoint, deterministic: the (point,
-// corner) entries of every site are bucketed (integer-atomic counts, scan, fill), each bucket is
-// sorted by entry index, and every site adds weight * grad over its bucket in that order.
+// corner) entries of every site are bucketed (integer-atomic counts, whose returned values are the
+// entries' slots in their buckets, a scan, a plain scatter), each bucket is sorted by entry index,
+// and every site adds weight * grad over its bucket in that order.
 #include <algorithm>
 #include <cmath>
 
@@ -88,18 +89,21 @@ __global__ void interp_fwd_kernel(const float* __restrict__ feats, int C, const 
     out[i * C + c] = s[0];
 }
 
-__global__ void interp_count_kernel(const int32_t* __restrict__ rows, int64_t ne, int32_t* __restrict__ cnt) {
+// Per-site entry counts; slot[e] = the count before entry e's own increment (its bucket slot).
+__global__ void interp_count_kernel(const int32_t* __restrict__ rows, int64_t ne, int32_t* __restrict__ cnt,
+                                    int32_t* __restrict__ slot) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e < ne && rows[e] >= 0) atomicAdd(&cnt[rows[e]], 1);
+  if (e < ne && rows[e] >= 0) slot[e] = atomicAdd(&cnt[rows[e]], 1);
 }
 
-// Bucket fill: entry e = 8 * point + corner goes to an unspecified slot of its site's bucket.
+// Bucket fill: entry e = 8 * point + corner goes to slot slot[e] of its site's bucket (the order
+// inside a bucket is that of the atomics, sorted afterwards).
 __global__ void interp_fill_kernel(const int32_t* __restrict__ rows, int64_t ne, const int64_t* __restrict__ start,
-                                   int32_t* __restrict__ fill, int32_t* __restrict__ ent) {
+                                   const int32_t* __restrict__ slot, int32_t* __restrict__ ent) {
   const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (e >= ne) return;
   const int32_t r = rows[e];
-  if (r >= 0) ent[start[r] + atomicAdd(&fill[r], 1)] = (int32_t)e;
+  if (r >= 0) ent[start[r] + slot[e]] = (int32_t)e;
 }
 
 // grad_feats[r][c..c+V) = sum over the sorted bucket of weight * grad[point][c..c+V); every site
@@ -205,7 +209,7 @@ extern "C" int ssconv_interpolate_backward(ssconv_rulebook_t rb, const float* gr
   }
   const int64_t ne = m * 8;
   auto up = [](size_t b) { return (b + 255) & ~(size_t)255; };
-  const size_t o_w = up(ne * 4), o_cnt = o_w + up(ne * 4), o_fill = o_cnt + up(n * 4), o_start = o_fill + up(n * 4);
+  const size_t o_w = up(ne * 4), o_cnt = o_w + up(ne * 4), o_fill = o_cnt + up(n * 4), o_start = o_fill + up(ne * 4);
   const size_t o_ent = o_start + up(n * 8), o_tmp = o_ent + up(ne * 4);
   const size_t o_big = o_tmp + up((size_t)(scan_tmp_elems(n) + 1) * 8), total = o_big + up((n + 1) * 4);
   char* ws = nullptr;
@@ -213,18 +217,17 @@ extern "C" int ssconv_interpolate_backward(ssconv_rulebook_t rb, const float* gr
   int32_t* rows = (int32_t*)ws;
   float* wts = (float*)(ws + o_w);
   int32_t* cnt = (int32_t*)(ws + o_cnt);
-  int32_t* fillc = (int32_t*)(ws + o_fill);
+  int32_t* slot = (int32_t*)(ws + o_fill);  // each entry's slot in its site's bucket
   int64_t* start = (int64_t*)(ws + o_start);
   int32_t* ent = (int32_t*)(ws + o_ent);
   int64_t* tmp = (int64_t*)(ws + o_tmp);
   int32_t* big = (int32_t*)(ws + o_big);
   auto run = [&]() -> int {
     SSC_HIP(hipMemsetAsync(cnt, 0, (size_t)n * 4, stream));
-    SSC_HIP(hipMemsetAsync(fillc, 0, (size_t)n * 4, stream));
     launch_corners(rb, points, batch, m, origin, voxel, rows, wts, stream);
-    interp_count_kernel<<<cdiv(ne, 256), 256, 0, stream>>>(rows, ne, cnt);
+    interp_count_kernel<<<cdiv(ne, 256), 256, 0, stream>>>(rows, ne, cnt, slot);
     SSC_TRY(exclusive_scan(cnt, n, start, tmp + scan_tmp_elems(n), tmp, stream));
-    interp_fill_kernel<<<cdiv(ne, 256), 256, 0, stream>>>(rows, ne, start, fillc, ent);
+    interp_fill_kernel<<<cdiv(ne, 256), 256, 0, stream>>>(rows, ne, start, slot, ent);
     SSC_TRY(sort_buckets(nullptr, n, n, start, cnt, ent, big, false, stream));
     if (channels % 4 == 0 && aligned16(grad) && aligned16(grad_feats))
       interp_bwd_kernel<4><<<cdiv(n * channels / 4, 256), 256, 0, stream>>>(grad, channels, wts, start, cnt, ent, n,
