@@ -659,6 +659,10 @@ static int build_impl(const int32_t* coords, int64_t n, const int32_t* grid, int
     const int flags0 = ((int*)host)[0], maxb = ((int*)host)[1];
     if (flags0 & kFlagBounds) return fail(SSCONV_E_BOUNDS, "a site lies outside the grid, has b < 0, or (max b + 1) * grid volume exceeds the 32-bit key space");
     if (maxb > max_batch(grid)) return fail(SSCONV_E_BOUNDS, "(max b + 1) * grid volume exceeds the 32-bit key space");
+    // no valid rule book follows a duplicate site or a full table: the build ends here, before the
+    // output set and the map are built
+    if (flags0 & kFlagDup) return fail(SSCONV_E_DUPLICATE, "duplicate input site");
+    if (flags0 & kFlagFull) return fail(SSCONV_E_HASH_FULL, "coordinate hash table is full");
     rb->nbatch = maxb + 1;
   }
 

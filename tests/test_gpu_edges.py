@@ -38,6 +38,9 @@ def test_error_codes():
     c = torch.from_numpy(_coords(0, 50, 8)).to(DEV)
     dup = torch.cat([c, c[:1]])
     assert _code(lambda: P.Rulebook(dup, 8, 3)) == E_DUPLICATE
+    # generated output sets (stride 2, 2x2x2 pooling windows) stop before writing any map entry
+    assert _code(lambda: P.Rulebook(dup, 8, 3, 2, False)) == E_DUPLICATE
+    assert _code(lambda: P.Rulebook(dup, 8, 2, 2, False)) == E_DUPLICATE
     bad = c.clone()
     bad[3, 2] = 8
     assert _code(lambda: P.Rulebook(bad, 8, 3)) == E_BOUNDS
@@ -53,6 +56,7 @@ def test_error_codes():
     P.debug_set(1, 16)                                  # 16 slots for 50 sites
     try:
         assert _code(lambda: P.Rulebook(c, 8, 3)) == E_HASH_FULL
+        assert _code(lambda: P.Rulebook(c, 8, 3, stride=2, submanifold=False)) == E_HASH_FULL
     finally:
         P.debug_set(1, 0)
     P.debug_set(2, 1)                                   # a submanifold build's one allocation fails
